@@ -1,0 +1,218 @@
+"""Float64 CPU oracle of the DART policy-update hot path.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py``, never by the product package.
+It shares no code with the HIP path.
+
+Two independent implementations live here:
+
+* ``liboracle.so`` built from ``dart_oracle.c`` (float64, OpenMP over rows),
+  wrapped by the functions of this module;
+* ``oracle.mini``, pure Python with ``math`` only, for tiny shapes.
+
+Both follow the paper's definitions (DART, arXiv 2509.23866): token entropy and
+log-prob (Sec. 4.3, Eq. 1), the step mean entropy and the top-rho step mask
+(Sec. 4.3, the indicator of Eq. 2), the truncated importance-sampling weight
+(Sec. 4.4) and the clipped surrogate of Eq. (2), and the gradient of the loss
+with respect to the logits. Every function is pinned by the ``-m "not gpu"``
+tests in ``tests/test_oracle_*.py`` against closed forms, invariants, brute
+force, a library routine and finite differences.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+# ORACLE_LIB lets the mutation tests load a deliberately broken build
+LIB = os.environ.get("ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
+SRC = os.path.join(HERE, "dart_oracle.c")
+
+
+def build(verbose: bool = False, src: str = SRC, out: str = os.path.join(HERE, "liboracle.so")) -> None:
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", src, "-o", out, "-lm"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_D = ctypes.c_double
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError(f"{LIB} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB)
+        lib.oracle_token_stats.restype = None
+        lib.oracle_token_stats.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
+                                           ctypes.c_int]
+        lib.oracle_step_entropy.restype = None
+        lib.oracle_step_entropy.argtypes = [_P, _P, _I64, _P, _P]
+        lib.oracle_kept_steps.restype = _I64
+        lib.oracle_kept_steps.argtypes = [_I64, _D]
+        lib.oracle_step_mask.restype = _I64
+        lib.oracle_step_mask.argtypes = [_P, _I64, _D, _P]
+        lib.oracle_tis_loss.restype = _D
+        lib.oracle_tis_loss.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, _D, _D, _D, _P, _P,
+                                        _P, _P]
+        lib.oracle_dlogits.restype = None
+        lib.oracle_dlogits.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
+                                       ctypes.c_int]
+        _lib = lib
+    return _lib
+
+
+def default_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _logits_arg(z):
+    """float32 array -> dtype 0; uint16 (bfloat16 bit patterns) -> dtype 1."""
+    z = np.asarray(z)
+    if z.ndim != 2 or z.strides[1] != z.itemsize:
+        raise ValueError("logits must be a 2-D array with contiguous rows")
+    if z.dtype == np.float32:
+        return z, 0
+    if z.dtype == np.uint16:
+        return z, 1
+    raise TypeError("logits must be float32 or bfloat16 bit patterns (uint16)")
+
+
+def token_stats(z, target, nthreads=None):
+    """Per-row (logp, H, lse) in float64 for logits rows ``z`` [n, V]."""
+    lib = _load()
+    z, dt = _logits_arg(z)
+    n, V = z.shape
+    ld = z.strides[0] // z.itemsize
+    target = _c(target, np.int32)
+    assert target.shape == (n,)
+    logp = np.empty(n, np.float64)
+    H = np.empty(n, np.float64)
+    lse = np.empty(n, np.float64)
+    lib.oracle_token_stats(z.ctypes.data, dt, n, V, ld, target.ctypes.data, logp.ctypes.data,
+                           H.ctypes.data, lse.ctypes.data, nthreads or default_threads())
+    return logp, H, lse
+
+
+def step_entropy(H, off):
+    """(Hs float64 [S], Hs32 float32 [S]) for token entropies H and offsets off."""
+    lib = _load()
+    H = _c(H, np.float64)
+    off = _c(off, np.int32)
+    S = off.size - 1
+    Hs = np.empty(S, np.float64)
+    Hs32 = np.empty(S, np.float32)
+    lib.oracle_step_entropy(H.ctypes.data, off.ctypes.data, S, Hs.ctypes.data, Hs32.ctypes.data)
+    return Hs, Hs32
+
+
+def kept_steps(S, rho):
+    return int(_load().oracle_kept_steps(int(S), float(rho)))
+
+
+def step_mask(Hs32, rho):
+    """(mask uint8 [S], k) decided on the float32 step entropies."""
+    lib = _load()
+    Hs32 = _c(Hs32, np.float32)
+    mask = np.empty(Hs32.size, np.uint8)
+    k = lib.oracle_step_mask(Hs32.ctypes.data, Hs32.size, float(rho), mask.ctypes.data)
+    return mask, int(k)
+
+
+def tis_loss(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C):
+    """Returns dict(L, g, ell, boundary, stats)."""
+    lib = _load()
+    logp = _c(logp, np.float64)
+    T = logp.size
+    lp_old = _c(lp_old, np.float32)
+    lp_roll = _c(lp_roll, np.float32)
+    adv = _c(adv, np.float32)
+    off = _c(off, np.int32)
+    mask = _c(mask, np.uint8)
+    S = off.size - 1
+    assert lp_old.size == T and lp_roll.size == T and adv.size == T and mask.size == S
+    assert off[0] == 0 and off[-1] == T
+    g = np.empty(T, np.float64)
+    ell = np.empty(T, np.float64)
+    boundary = np.empty(T, np.uint8)
+    stats = np.empty(4, np.float64)
+    L = lib.oracle_tis_loss(T, logp.ctypes.data, lp_old.ctypes.data, lp_roll.ctypes.data,
+                            adv.ctypes.data, off.ctypes.data, S, mask.ctypes.data,
+                            float(eps_low), float(eps_high), float(C), g.ctypes.data,
+                            ell.ctypes.data, boundary.ctypes.data, stats.ctypes.data)
+    return dict(L=float(L), g=g, ell=ell, boundary=boundary.astype(bool), stats=stats)
+
+
+def dlogits(z, target, lse, g, nthreads=None):
+    """float64 [n, V] gradient rows for logits rows ``z``."""
+    lib = _load()
+    z, dt = _logits_arg(z)
+    n, V = z.shape
+    ld = z.strides[0] // z.itemsize
+    target = _c(target, np.int32)
+    lse = _c(lse, np.float64)
+    g = _c(g, np.float64)
+    out = np.empty((n, V), np.float64)
+    lib.oracle_dlogits(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
+                       g.ctypes.data, out.ctypes.data, nthreads or default_threads())
+    return out
+
+
+def forward_backward(z, target, lp_old, lp_roll, adv, off, rho, eps_low, eps_high, C,
+                     nthreads=None, mask=None):
+    """The whole path on full logits: stats -> step entropy -> mask -> loss -> dlogits.
+    ``mask`` may be given to skip the selection (it is then an input)."""
+    logp, H, lse = token_stats(z, target, nthreads)
+    Hs, Hs32 = step_entropy(H, off)
+    if mask is None:
+        mask, k = step_mask(Hs32, rho)
+    else:
+        k = int(np.sum(mask))
+    res = tis_loss(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C)
+    dz = dlogits(z, target, lse, res["g"], nthreads)
+    res.update(logp=logp, H=H, lse=lse, Hs=Hs, Hs32=Hs32, mask=mask, k=k, dz=dz)
+    return res
+
+
+def f64_to_bf16_bits(x):
+    """Correctly rounded (nearest-even) float64 -> bfloat16 bit patterns,
+    including bfloat16 subnormals; used only to compare with bf16 outputs."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    ax = np.abs(x)
+    sub = ax < 2.0 ** -126
+    # normal range: round the double's 52-bit fraction to 7 bits
+    u = x.view(np.uint64)
+    half = np.uint64((1 << 44) - 1)
+    r = (u + half + ((u >> np.uint64(45)) & np.uint64(1))) & ~np.uint64((1 << 45) - 1)
+    f = r.view(np.float64).astype(np.float32)
+    out[...] = (f.view(np.uint32) >> 16).astype(np.uint16)
+    if np.any(sub):
+        q = np.rint(x[sub] / 2.0 ** -133) * 2.0 ** -133  # rint is round-half-even
+        out[sub] = (q.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return out
+
+
+def bf16_ulp(bits):
+    """Spacing of bfloat16 numbers at the magnitude of ``bits`` (float64)."""
+    f = (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    a = np.abs(f.astype(np.float64))
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
+    return np.where(a < 2.0 ** -126, 2.0 ** -133, 2.0 ** (e - 7))

@@ -1,0 +1,60 @@
+"""Planted mistakes in the oracle (on the CPU) must each fail a pin.
+
+Each mutation rewrites one line of ``oracle/dart_oracle.c``, builds it into a
+temporary library and runs the pins of ``test_oracle_pins.py`` against it
+*excluding* the comparison with the pure-Python mini oracle, so what catches the
+mistake is a closed form, an invariant, brute force, a library routine or the
+finite differences, not the second implementation.
+"""
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTATIONS = {
+    "entropy_in_bits": ("ksum_add(&h, -p * log(p))", "ksum_add(&h, -p * log2(p))"),
+    "logp_vs_max_not_normaliser": ("target[t]) - log_norm;", "target[t]) - m;"),
+    "step_mean_wrong_denominator": ("/ (double)(off[s + 1] - off[s]);",
+                                    "/ (double)(off[s + 1] - off[s] + 1);"),
+    "kept_count_floor": ("ceil(rho * (double)S - 1e-6)", "floor(rho * (double)S)"),
+    "ties_to_higher_index": ("Hs32[o] == Hs32[s] && o < s", "Hs32[o] == Hs32[s] && o > s"),
+    "selection_keeps_lowest": ("Hs32[o] > Hs32[s] ||", "Hs32[o] < Hs32[s] ||"),
+    "ratio_inverted": ("exp(logp[t] - (double)lp_old[t])", "exp((double)lp_old[t] - logp[t])"),
+    "tis_weight_dropped": ("const double w = ratio_tis < C ? ratio_tis : C;",
+                           "const double w = 1.0;"),
+    "tis_weight_uncapped": ("const double w = ratio_tis < C ? ratio_tis : C;",
+                            "const double w = ratio_tis;"),
+    "clip_bounds_swapped": ("if (rc < 1.0 - eps_low) rc = 1.0 - eps_low;",
+                            "if (rc < 1.0 - eps_high) rc = 1.0 - eps_high;"),
+    "loss_sign": ("lt = -M * w * o / (double)N;", "lt = M * w * o / (double)N;"),
+    "gradient_through_clip": ("gt = u <= c ? -M * w * A * r / (double)N : 0.0;",
+                              "gt = -M * w * A * r / (double)N;"),
+    "mean_over_all_tokens": ("if (mask[s]) N += off[s + 1] - off[s];", "N += off[s + 1] - off[s];"),
+    "dlogits_wrong_sign_softmax": ("out[t * V + v] = g[t] * (delta - p);",
+                                   "out[t * V + v] = g[t] * (delta + p);"),
+    "dlogits_wrong_target": ("const double delta = v == target[t] ? 1.0 : 0.0;",
+                             "const double delta = v == (target[t] + 1) % V ? 1.0 : 0.0;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name, tmp_path):
+    old, new = MUTATIONS[name]
+    src = open(oracle.SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    mutated = tmp_path / "mutated.c"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mut.so"
+    oracle.build(src=str(mutated), out=str(lib))
+    env = dict(os.environ, ORACLE_LIB=str(lib))
+    proc = subprocess.run(
+        [sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+         os.path.join(ROOT, "tests", "test_oracle_pins.py"), "-k", "not mini"],
+        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert proc.returncode != 0, f"mutation {name} survived the pins:\n{proc.stdout[-2000:]}"
