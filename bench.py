@@ -1,0 +1,215 @@
+#!/usr/bin/env python3
+"""Benchmark of the DART policy-update hot path on one MI355X (gfx950).
+
+One step = one pass of the whole path over one step group held in HBM:
+dart_tok_stats -> dart_step_select -> dart_tis_loss_fwd -> dart_tis_grad, on
+one stream. The default workload is the 7B-VLM vocabulary group: T = 4096
+action tokens in 64 steps, V = 152064, bf16 logits, separate gradient buffer.
+
+Prints one JSON line. `value` is logit elements per second (T*V per step
+time); `hbm_frac_step` counts 2 reads + 1 write of the T x V logits per step
+against 8 TB/s; `roofline` covers the dominant kernel (the gradient pass, one
+read + one write of T x V), timed with HIP events on its own stream;
+`cpu_baseline` times the float64 oracle on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "logit elements/s for fused entropy+TIS loss fwd+bwd; % of HBM peak"
+HBM_PEAK_GBS = 8000.0
+DOMINANT = "tis_grad_kernel"
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="vlm7b",
+                    choices=["tiny", "vlm7b", "microbatch", "longhorizon", "edge"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="0 = the process's CPU affinity (max 16)")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    src = os.path.join(ROOT, "paper_2509_23866_amd", "csrc", "dart.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the dominant kernel from the committed PMC
+    summary, if it was taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, threads):
+    """The float64 oracle, as it stands, over the whole workload: token stats,
+    step entropy, selection, loss and the gradient (rows streamed in chunks,
+    gradient rows discarded). Input generation and the old-policy log-probs
+    (an untimed oracle pass) are outside the timed region."""
+    import numpy as np
+
+    import oracle
+    import synth
+    import synth.native as sn
+
+    z = sn.logits_rows_host(wl, np.arange(wl.T), nthreads=threads)
+    logp0, _, _ = oracle.token_stats(z, wl.target, nthreads=threads)
+    lp_old, lp_roll = synth.perturbed_logprobs(wl, logp0)
+    f = lambda x: float(np.float32(x))  # noqa: E731
+    t0 = time.perf_counter()
+    logp, H, lse = oracle.token_stats(z, wl.target, nthreads=threads)
+    _, Hs32 = oracle.step_entropy(H, wl.off)
+    mask, _ = oracle.step_mask(Hs32, wl.rho)
+    res = oracle.tis_loss(logp, lp_old, lp_roll, wl.adv, wl.off, mask, f(wl.eps_low),
+                          f(wl.eps_high), f(wl.C))
+    chunk = 256
+    for r0 in range(0, wl.T, chunk):
+        r1 = min(wl.T, r0 + chunk)
+        oracle.dlogits(z[r0:r1], wl.target[r0:r1], lse[r0:r1], res["g"][r0:r1], nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": wl.T * wl.V / dt, "unit": "logit elements/s", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"whole workload ({wl.T} rows x {wl.V}), float64 C oracle, OpenMP over rows"}
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2509_23866_amd as dart
+    import synth
+    import synth.native as sn
+
+    wl = synth.make_workload(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    esize = 4 if wl.dtype == "f32" else 2
+    T, V, S = wl.T, wl.V, wl.S
+
+    # ---- inputs resident in HBM (untimed set-up)
+    logits = torch.empty((T, V), dtype=tdt, device=dev)
+    sn.fill_logits_device(sn.DeviceRecipe(wl), logits)
+    pristine = logits.clone() if wl.inplace else None
+    target = torch.from_numpy(wl.target).to(dev)
+    adv = torch.from_numpy(wl.adv).to(dev)
+    off = torch.from_numpy(wl.off).to(dev)
+    logp, ent, lse = dart.dart_tok_stats(logits, target)
+    # old/rollout log-probs: the workload's perturbation of the current policy's
+    # log-prob of each target (the same pass a trainer runs for pi_old)
+    base = logp.double()
+    lp_old = (base + torch.from_numpy(wl.old_offset).to(dev)).float()
+    lp_roll = (lp_old.double() + torch.from_numpy(wl.roll_offset).to(dev)).float()
+    step_H = torch.empty(S, dtype=torch.float32, device=dev)
+    mask = torch.empty(S, dtype=torch.uint8, device=dev)
+    n_kept = torch.empty(1, dtype=torch.int32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    coef = torch.empty(T, dtype=torch.float32, device=dev)
+    stats = torch.empty(4, dtype=torch.float32, device=dev)
+    dlogits = logits if wl.inplace else torch.empty((T, V), dtype=tdt, device=dev)
+    eps_low, eps_high, C = float(np.float32(wl.eps_low)), float(np.float32(wl.eps_high)), float(np.float32(wl.C))
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream)
+        if ev:
+            ev[1].record(stream)
+        dart.dart_step_select(ent, off, wl.rho, step_H, mask, n_kept, stream=stream)
+        dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C,
+                               loss, coef, stats, stream=stream)
+        if ev:
+            ev[2].record(stream)
+        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream)
+        if ev:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        if pristine is not None:
+            logits.copy_(pristine)
+        step()
+    torch.cuda.synchronize(dev)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if pristine is not None:
+            logits.copy_(pristine)  # untimed: outside the step's events
+        step(evs[i])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+
+    step_ms = [e[0].elapsed_time(e[3]) for e in evs]
+    k1_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    grad_ms = [e[2].elapsed_time(e[3]) for e in evs]
+    ms_per_step = float(np.mean(step_ms))
+    if pristine is None:
+        ms_per_step = max(ms_per_step, wall * 1e3 / args.steps)
+    elems = T * V
+    value = elems / (ms_per_step * 1e-3)
+    grad_s = float(np.mean(grad_ms)) * 1e-3
+    grad_bytes = 2 * elems * esize
+    achieved = grad_bytes / grad_s / 1e9
+    traffic = measured_traffic(args.workload)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "logit elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded counter-based generator; shapes of the workload description)",
+        "config": {"workload": f"{wl.name}: {wl.description}", "T": T, "V": V, "S": S,
+                   "rho": wl.rho, "eps_low": wl.eps_low, "eps_high": wl.eps_high, "C": wl.C,
+                   "in_place": wl.inplace, "logits_bytes": elems * esize},
+        "hbm_frac_step": (3 * elems * esize / (ms_per_step * 1e-3) / 1e9) / HBM_PEAK_GBS,
+        "kernel_ms": {"tok_stats_kernel": float(np.mean(k1_ms)), "tis_grad_kernel": float(np.mean(grad_ms)),
+                      "step_select+tis_coef": float(np.mean(np.array(step_ms) - np.array(k1_ms) - np.array(grad_ms)))},
+        "roofline": {"kernel": DOMINANT, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "algorithmic_bytes_per_launch": grad_bytes},
+    }
+    if not args.no_cpu_baseline:
+        threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+        line["cpu_baseline"] = cpu_baseline(wl, threads)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,158 @@
+/* libdart — the trainer-side hot path of DART's policy update on MI355X (gfx950).
+ *
+ * Paper: "Efficient Multi-turn RL for GUI Agents via Decoupled Training and
+ * Adaptive Data Curation" (DART), arXiv 2509.23866.
+ *
+ * The path maps the policy's vocabulary logits for every action token of a
+ * step group (all steps of the N rollouts of one task, Sec. 3.3) to:
+ *   1. per-token log-prob of the generated token and entropy   dart_tok_stats
+ *   2. per-step mean entropy and the high-entropy step mask     dart_step_select
+ *   3. the truncated-importance-sampling-weighted clipped
+ *      policy-gradient loss and its gradient w.r.t. the logits  dart_tis_loss_fwd_bwd
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Array arguments are DEVICE pointers unless a comment says otherwise. The
+ *   caller owns every buffer; the library allocates no memory and keeps no
+ *   state between calls, so concurrent calls on different streams are safe.
+ * - Every call is asynchronous on `stream` (0 = the null stream): it checks its
+ *   scalar arguments on the host, enqueues its kernels and returns. Outputs are
+ *   valid once the stream is synchronised. Device data (target ids in range,
+ *   increasing offsets) is a precondition and is not checked.
+ * - Logits are row-major [T, ld] with ld >= V (elements, not bytes). Rows whose
+ *   start is 16-byte aligned (base aligned and ld * element size a multiple of
+ *   16) take the vectorised path; other rows are still correct, only slower.
+ * - Status codes: DART_OK; DART_ERR_INVALID_ARG for a bad scalar argument or a
+ *   null required pointer (nothing is enqueued); DART_ERR_HIP when HIP reports a
+ *   launch error. No call aborts or throws.
+ * - Results are deterministic: no atomics on any floating-point result, fixed
+ *   reduction orders; identical rows at identical alignment give bit-identical
+ *   entropies.
+ */
+#ifndef DART_H
+#define DART_H
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DART_OK = 0,
+    DART_ERR_INVALID_ARG = 1,
+    DART_ERR_UNSUPPORTED = 2,
+    DART_ERR_HIP = 3
+} dart_status_t;
+
+typedef enum { DART_F32 = 0, DART_BF16 = 1 } dart_dtype_t;
+
+/* Token statistics (Sec. 4.3, definition of the token entropy H_{t,i} and of
+ * p = pi_theta(v | ...); Eq. (1), log pi_theta of the generated token).
+ *
+ * For every row t of `logits` ([T, ld], dtype `dtype`, first V columns used):
+ *   lse[t]     = log sum_v exp(z_tv)                        (natural log)
+ *   logp[t]    = z_{t, target[t]} - lse[t]
+ *   entropy[t] = -sum_v p_tv log p_tv,  p_tv = exp(z_tv - lse[t])   (nats, >= 0)
+ * computed in one streaming pass in float32 (online max / normaliser /
+ * entropy). logp stays accurate when p_target is close to 1.
+ *   target:  [T] int32, 0 <= target[t] < V (precondition).
+ *   logp, entropy, lse: [T] float32 outputs.
+ * Errors: INVALID_ARG if a pointer is null, T < 1, V < 1, ld < V or dtype is
+ * unknown. Finite logits are required; -inf entries are allowed (probability
+ * 0) as long as each row has a finite entry; NaN gives undefined results. */
+dart_status_t dart_tok_stats(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                             int64_t ld, const int32_t* target, float* logp, float* entropy,
+                             float* lse, hipStream_t stream);
+
+/* Step entropy and high-entropy step selection (Sec. 4.3: the step entropy is
+ * the mean token entropy over the step's thought and action tokens; only the
+ * top-rho fraction of steps of the group by step entropy is trained, rho = 0.8
+ * in the paper; the indicator of Eq. (2)).
+ *   entropy:       [T] float32 token entropies (from dart_tok_stats).
+ *   step_offsets:  [S+1] int32, step s = tokens [off[s], off[s+1]),
+ *                  0 = off[0] < off[1] < ... < off[S] = T (precondition).
+ *   rho:           kept fraction in [0, 1]; k = dart_kept_steps(S, rho) steps are kept.
+ *   step_entropy:  [S] float32 output, the mean (summed in float64, rounded once).
+ *   step_mask:     [S] uint8 output, 1 = kept. Exactly k ones: the k largest
+ *                  step entropies, ties broken towards the lower step index.
+ *   n_kept_steps:  [1] int32 output (k), may be NULL.
+ * Errors: INVALID_ARG if a required pointer is null, T < 1, S < 1, S > T or
+ * rho is outside [0, 1] or NaN. */
+dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* step_offsets,
+                               int64_t S, double rho, float* step_entropy, uint8_t* step_mask,
+                               int32_t* n_kept_steps, hipStream_t stream);
+
+/* TIS-weighted clipped policy-gradient loss and its gradient w.r.t. the logits
+ * (Eq. (2) without the KL term; the truncated importance weight of Sec. 4.4;
+ * the clipped ratio of Eq. (1) with the asymmetric bounds of Appendix A.4).
+ *
+ * Per token t of step s(t), with M = step_mask[s(t)] and N = number of tokens
+ * in kept steps:
+ *   r = exp(logp - logp_old),  w = min(exp(logp_old - logp_rollout), C)
+ *   u = r A,  c = clip(r, 1 - eps_low, 1 + eps_high) A
+ *   loss      = -(1/N) sum_t M w min(u, c)                 (token mean over kept tokens)
+ *   tok_coef  = dloss/dlogp_t = -(M w A r / N) if u <= c else 0
+ *   dlogits   = tok_coef_t * (onehot(target_t) - softmax(z_t))
+ * w, M and N are constants of the differentiation; N = 0 gives loss 0 and a
+ * zero gradient.
+ *   logits, dtype, T, V, ld, target: as for dart_tok_stats.
+ *   logp, lse:   [T] float32 from dart_tok_stats on the same logits.
+ *   logp_old, logp_rollout, adv: [T] float32 (old trainer policy, rollout
+ *                policy log-probs of the targets; per-token advantages).
+ *   step_offsets, S: as for dart_step_select; step_mask: [S] uint8 (0/1).
+ *   eps_low, eps_high: clip bounds >= 0; C > 0 (may be +INFINITY: no truncation).
+ *   dlogits:     [T, ld_out] output of dtype `dtype` (bf16 rounded to nearest
+ *                even). It may be the logits buffer itself (in place) when
+ *                ld_out == ld; any other overlap with logits is rejected.
+ *   loss:        [1] float64 output (summed in float64 in a fixed order).
+ *   tok_coef:    [T] float32 output (required: it carries the coefficient from
+ *                the loss kernel to the gradient kernel).
+ *   stats:       [4] float32 output or NULL: clip fraction, mean TIS weight,
+ *                fraction of weights at the cap, N (all over kept tokens).
+ * Errors: INVALID_ARG for a null required pointer, T < 1, V < 1, ld < V,
+ * ld_out < V, S < 1, S > T, eps < 0 or NaN, C <= 0 or NaN, an unknown dtype,
+ * or a partial overlap of dlogits with logits. */
+dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                                    int64_t ld, const int32_t* target, const float* logp,
+                                    const float* lse, const float* logp_old,
+                                    const float* logp_rollout, const float* adv,
+                                    const int32_t* step_offsets, int64_t S,
+                                    const uint8_t* step_mask, float eps_low, float eps_high,
+                                    float C, void* dlogits, int64_t ld_out, double* loss,
+                                    float* tok_coef, float* stats, hipStream_t stream);
+
+/* The two halves of dart_tis_loss_fwd_bwd, for callers that want the loss
+ * without the gradient, or that time the two kernels separately.
+ * dart_tis_loss_fwd computes loss, tok_coef and stats exactly as above (the
+ * logits are not read); dart_tis_grad then writes
+ *   dlogits[t, v] = tok_coef[t] * (onehot(target[t])[v] - exp(z_tv - lse[t]))
+ * (Eq. (2) through the softmax derivative) from the coefficients of the first
+ * half. Same argument meanings, layouts and error rules as
+ * dart_tis_loss_fwd_bwd. */
+dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_old,
+                                const float* logp_rollout, const float* adv,
+                                const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
+                                float eps_low, float eps_high, float C, double* loss,
+                                float* tok_coef, float* stats, hipStream_t stream);
+
+dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                            int64_t ld, const int32_t* target, const float* logp,
+                            const float* lse, const float* tok_coef, void* dlogits,
+                            int64_t ld_out, hipStream_t stream);
+
+/* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
+ * number of steps dart_step_select keeps (the guard absorbs the representation
+ * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside
+ * [0, 1]. */
+int64_t dart_kept_steps(int64_t S, double rho);
+
+/* Host helper: a static, human-readable name for a status code. */
+const char* dart_status_string(dart_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DART_H */

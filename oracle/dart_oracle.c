@@ -58,31 +58,42 @@ static double logit_at(const void* z, int dtype, int64_t ld, int64_t t, int64_t 
 
 /* Sec. 4.3: p_v = softmax(z)_v, H = -sum_v p_v log p_v (nats, R10: natural log),
  * and log pi(y) = z_y - log sum_v exp(z_v) for the target id y (Eq. 1 numerator).
- * Two passes per row: (1) the maximum and the normaliser, (2) the entropy
- * summed from its definition. A term with p_v == 0 contributes 0 (R9: -inf
+ * Per row: (1) the maximum m; (2) e_v = exp(z_v - m) and their sum s, so that
+ * lse = m + log s; (3) p_v = e_v / s and log p_v = z_v - lse, summed into the
+ * entropy from its definition. A term with p_v == 0 contributes 0 (R9: -inf
  * logits allowed, 0 log 0 := 0). */
 void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
                         const int32_t* target, double* logp, double* H, double* lse,
                         int nthreads) {
     if (nthreads < 1) nthreads = 1;
-#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
-    for (int64_t t = 0; t < nrows; ++t) {
-        double m = -INFINITY;
-        for (int64_t v = 0; v < V; ++v) {
-            double x = logit_at(z, dtype, ld, t, v);
-            if (x > m) m = x;
+#pragma omp parallel num_threads(nthreads)
+    {
+        double* e = (double*)malloc((size_t)V * sizeof(double));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t t = 0; t < nrows; ++t) {
+            double m = -INFINITY;
+            for (int64_t v = 0; v < V; ++v) {
+                double x = logit_at(z, dtype, ld, t, v);
+                if (x > m) m = x;
+            }
+            ksum_t s = {0.0, 0.0};
+            for (int64_t v = 0; v < V; ++v) {
+                e[v] = exp(logit_at(z, dtype, ld, t, v) - m);
+                ksum_add(&s, e[v]);
+            }
+            const double sum = ksum_value(&s);
+            const double log_norm = m + log(sum);
+            ksum_t h = {0.0, 0.0};
+            for (int64_t v = 0; v < V; ++v) {
+                const double p = e[v] / sum;
+                const double log_p = logit_at(z, dtype, ld, t, v) - log_norm;
+                if (p > 0.0) ksum_add(&h, -p * log_p);
+            }
+            lse[t] = log_norm;
+            H[t] = ksum_value(&h);
+            logp[t] = logit_at(z, dtype, ld, t, target[t]) - log_norm;
         }
-        ksum_t s = {0.0, 0.0};
-        for (int64_t v = 0; v < V; ++v) ksum_add(&s, exp(logit_at(z, dtype, ld, t, v) - m));
-        const double log_norm = m + log(ksum_value(&s));
-        ksum_t h = {0.0, 0.0};
-        for (int64_t v = 0; v < V; ++v) {
-            double p = exp(logit_at(z, dtype, ld, t, v) - log_norm);
-            if (p > 0.0) ksum_add(&h, -p * log(p));
-        }
-        lse[t] = log_norm;
-        H[t] = ksum_value(&h);
-        logp[t] = logit_at(z, dtype, ld, t, target[t]) - log_norm;
+        free(e);
     }
 }
 

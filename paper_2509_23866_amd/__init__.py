@@ -1,0 +1,265 @@
+"""Python binding of libdart (the C ABI declared in include/dart.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``csrc/dart.hip``. torch supplies device memory and the stream. The library must
+be built (``__graft_entry__.build()``); if it is missing, importing a function
+raises — there is no CPU fallback.
+
+Functions carry the C names: ``dart_tok_stats``, ``dart_step_select``,
+``dart_tis_loss_fwd_bwd``, ``dart_kept_steps``, ``dart_status_string``.
+``policy_update`` chains the three device calls.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdart.so")
+
+DART_OK = 0
+DART_ERR_INVALID_ARG = 1
+DART_ERR_UNSUPPORTED = 2
+DART_ERR_HIP = 3
+DART_F32 = 0
+DART_BF16 = 1
+
+EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
+            "dart_tis_grad", "dart_kept_steps", "dart_status_string")
+
+
+class DartError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} failed: {dart_status_string(code)} ({code})")
+        self.code = code
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+
+
+def load_library():
+    """Open libdart.so (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB_PATH)
+        lib.dart_tok_stats.restype = ctypes.c_int
+        lib.dart_tok_stats.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]
+        lib.dart_step_select.restype = ctypes.c_int
+        lib.dart_step_select.argtypes = [_P, _I64, _P, _I64, ctypes.c_double, _P, _P, _P, _P]
+        lib.dart_tis_loss_fwd_bwd.restype = ctypes.c_int
+        lib.dart_tis_loss_fwd_bwd.argtypes = [
+            _P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P,
+            ctypes.c_float, ctypes.c_float, ctypes.c_float, _P, _I64, _P, _P, _P, _P]
+        lib.dart_tis_loss_fwd.restype = ctypes.c_int
+        lib.dart_tis_loss_fwd.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, ctypes.c_float,
+                                          ctypes.c_float, ctypes.c_float, _P, _P, _P, _P]
+        lib.dart_tis_grad.restype = ctypes.c_int
+        lib.dart_tis_grad.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P,
+                                      _I64, _P]
+        lib.dart_kept_steps.restype = _I64
+        lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
+        lib.dart_status_string.restype = ctypes.c_char_p
+        lib.dart_status_string.argtypes = [ctypes.c_int]
+        _lib = lib
+    return _lib
+
+
+def dart_status_string(code: int) -> str:
+    return load_library().dart_status_string(int(code)).decode()
+
+
+def dart_kept_steps(S: int, rho: float) -> int:
+    return int(load_library().dart_kept_steps(int(S), float(rho)))
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream_handle(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _check_vec(name, t, dtype, n, device):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype != dtype or t.device != device or t.dim() != 1 or t.numel() != n or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} vector of {n} elements on {device}")
+
+
+def _logits_meta(logits):
+    torch = _torch()
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a 2-D tensor with contiguous rows")
+    if logits.dtype == torch.bfloat16:
+        dt = DART_BF16
+    elif logits.dtype == torch.float32:
+        dt = DART_F32
+    else:
+        raise TypeError("logits must be bfloat16 or float32")
+    if not logits.is_cuda:
+        raise ValueError("logits must be on a GPU")
+    return dt, logits.shape[0], logits.shape[1], logits.stride(0)
+
+
+def dart_tok_stats(logits, target, logp=None, entropy=None, lse=None, stream=None):
+    """Per-token log-prob of the target, entropy and log-normaliser (float32 [T] each)."""
+    torch = _torch()
+    dt, T, V, ld = _logits_meta(logits)
+    dev = logits.device
+    _check_vec("target", target, torch.int32, T, dev)
+    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
+    entropy = torch.empty(T, dtype=torch.float32, device=dev) if entropy is None else entropy
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    for n, v in (("logp", logp), ("entropy", entropy), ("lse", lse)):
+        _check_vec(n, v, torch.float32, T, dev)
+    rc = load_library().dart_tok_stats(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
+                                       logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
+                                       _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_tok_stats", rc)
+    return logp, entropy, lse
+
+
+def dart_step_select(entropy, step_offsets, rho, step_entropy=None, step_mask=None,
+                     n_kept_steps=None, stream=None):
+    """Per-step mean entropy (float32 [S]), kept-step mask (uint8 [S]) and the
+    kept count (int32 [1])."""
+    torch = _torch()
+    dev = entropy.device
+    T = entropy.numel()
+    S = step_offsets.numel() - 1
+    _check_vec("entropy", entropy, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    step_entropy = torch.empty(S, dtype=torch.float32, device=dev) if step_entropy is None else step_entropy
+    step_mask = torch.empty(S, dtype=torch.uint8, device=dev) if step_mask is None else step_mask
+    n_kept_steps = torch.empty(1, dtype=torch.int32, device=dev) if n_kept_steps is None else n_kept_steps
+    _check_vec("step_entropy", step_entropy, torch.float32, S, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    _check_vec("n_kept_steps", n_kept_steps, torch.int32, 1, dev)
+    rc = load_library().dart_step_select(entropy.data_ptr(), T, step_offsets.data_ptr(), S,
+                                         float(rho), step_entropy.data_ptr(), step_mask.data_ptr(),
+                                         n_kept_steps.data_ptr(), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_step_select", rc)
+    return step_entropy, step_mask, n_kept_steps
+
+
+def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv, step_offsets,
+                          step_mask, eps_low, eps_high, C, dlogits=None, loss=None, tok_coef=None,
+                          stats=None, with_stats=True, stream=None):
+    """Loss (float64 [1]), dlogits (dtype and shape of logits; pass ``dlogits=logits``
+    for the in-place gradient), per-token coefficient (float32 [T]) and stats
+    (float32 [4]: clip fraction, mean TIS weight, capped fraction, N)."""
+    torch = _torch()
+    dt, T, V, ld = _logits_meta(logits)
+    dev = logits.device
+    S = step_offsets.numel() - 1
+    _check_vec("target", target, torch.int32, T, dev)
+    for n, v in (("logp", logp), ("lse", lse), ("logp_old", logp_old),
+                 ("logp_rollout", logp_rollout), ("adv", adv)):
+        _check_vec(n, v, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    if dlogits is None:
+        dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+    if (dlogits.dtype != logits.dtype or dlogits.dim() != 2 or tuple(dlogits.shape) != (T, V)
+            or dlogits.stride(1) != 1 or dlogits.device != dev):
+        raise ValueError("dlogits must match logits in dtype and shape, with contiguous rows")
+    loss = torch.empty(1, dtype=torch.float64, device=dev) if loss is None else loss
+    tok_coef = torch.empty(T, dtype=torch.float32, device=dev) if tok_coef is None else tok_coef
+    if stats is None and with_stats:
+        stats = torch.empty(4, dtype=torch.float32, device=dev)
+    _check_vec("loss", loss, torch.float64, 1, dev)
+    _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
+    if stats is not None:
+        _check_vec("stats", stats, torch.float32, 4, dev)
+    rc = load_library().dart_tis_loss_fwd_bwd(
+        logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
+        logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(), step_offsets.data_ptr(), S,
+        step_mask.data_ptr(), float(eps_low), float(eps_high), float(C), dlogits.data_ptr(),
+        dlogits.stride(0), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats),
+        _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_tis_loss_fwd_bwd", rc)
+    return loss, dlogits, tok_coef, stats
+
+
+def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask, eps_low,
+                      eps_high, C, loss=None, tok_coef=None, stats=None, with_stats=True,
+                      stream=None):
+    """Loss (float64 [1]), per-token coefficient (float32 [T]) and stats; the
+    logits are not needed."""
+    torch = _torch()
+    dev = logp.device
+    T = logp.numel()
+    S = step_offsets.numel() - 1
+    for n, v in (("logp", logp), ("logp_old", logp_old), ("logp_rollout", logp_rollout),
+                 ("adv", adv)):
+        _check_vec(n, v, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev) if loss is None else loss
+    tok_coef = torch.empty(T, dtype=torch.float32, device=dev) if tok_coef is None else tok_coef
+    if stats is None and with_stats:
+        stats = torch.empty(4, dtype=torch.float32, device=dev)
+    _check_vec("loss", loss, torch.float64, 1, dev)
+    _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
+    if stats is not None:
+        _check_vec("stats", stats, torch.float32, 4, dev)
+    rc = load_library().dart_tis_loss_fwd(
+        T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(),
+        step_offsets.data_ptr(), S, step_mask.data_ptr(), float(eps_low), float(eps_high),
+        float(C), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_tis_loss_fwd", rc)
+    return loss, tok_coef, stats
+
+
+def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None):
+    """dlogits = tok_coef * (onehot(target) - softmax(logits)), dtype of logits."""
+    torch = _torch()
+    dt, T, V, ld = _logits_meta(logits)
+    dev = logits.device
+    _check_vec("target", target, torch.int32, T, dev)
+    for n, v in (("logp", logp), ("lse", lse), ("tok_coef", tok_coef)):
+        _check_vec(n, v, torch.float32, T, dev)
+    if dlogits is None:
+        dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+    if (dlogits.dtype != logits.dtype or dlogits.dim() != 2 or tuple(dlogits.shape) != (T, V)
+            or dlogits.stride(1) != 1 or dlogits.device != dev):
+        raise ValueError("dlogits must match logits in dtype and shape, with contiguous rows")
+    rc = load_library().dart_tis_grad(
+        logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
+        tok_coef.data_ptr(), dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_tis_grad", rc)
+    return dlogits
+
+
+def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
+                  eps_high, C, dlogits=None, stream=None):
+    """tok_stats -> step_select -> tis_loss_fwd_bwd on one stream. Returns a dict
+    of device tensors (nothing is synchronised)."""
+    logp, ent, lse = dart_tok_stats(logits, target, stream=stream)
+    step_ent, mask, n_kept = dart_step_select(ent, step_offsets, rho, stream=stream)
+    loss, dz, coef, stats = dart_tis_loss_fwd_bwd(
+        logits, target, logp, lse, logp_old, logp_rollout, adv, step_offsets, mask, eps_low,
+        eps_high, C, dlogits=dlogits, stream=stream)
+    return dict(logp=logp, entropy=ent, lse=lse, step_entropy=step_ent, step_mask=mask,
+                n_kept_steps=n_kept, loss=loss, dlogits=dz, tok_coef=coef, stats=stats)

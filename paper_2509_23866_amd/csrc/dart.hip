@@ -1,0 +1,746 @@
+// libdart: DART's policy-update hot path as hand-written HIP for gfx950 (CDNA4).
+//
+// Paper: DART, arXiv 2509.23866 — token entropy and step entropy (Sec. 4.3),
+// high-entropy step selection (Sec. 4.3, indicator of Eq. 2), truncated
+// importance sampling (Sec. 4.4), clipped surrogate (Eq. 1, Eq. 2).
+//
+// Four kernels, all launched on the caller's stream:
+//   tok_stats_kernel    one workgroup per logits row; one streaming pass with an
+//                       online (max, normaliser, entropy) triple in fp32 per lane,
+//                       merged across lanes and waves; target logit gathered.
+//   step_select_kernel  one workgroup: per-step mean entropy (fp64 sums in a fixed
+//                       order), radix select of the k-th largest 32-bit key over
+//                       steps with LDS histograms, index-ordered tie resolution.
+//   tis_coef_kernel     one workgroup: per-token ratio, TIS weight, clip gate and
+//                       loss coefficient; loss summed in fp64 in a fixed order.
+//   tis_grad_kernel     one workgroup per row; second streaming pass writing
+//                       coef * (onehot - softmax) in the logits dtype.
+// The two streaming kernels are HBM-bound (no matrix contraction anywhere):
+// 16-byte non-temporal loads, 4 loads in flight per lane, base-2 exponentials.
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "dart.h"
+
+namespace {
+
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kLn2 = 0.69314718055994530942f;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------------
+// element access
+// ------------------------------------------------------------------------
+
+template <dart_dtype_t D>
+struct Elt;
+template <>
+struct Elt<DART_BF16> {
+    using T = uint16_t;
+    static constexpr int kPerVec = 8;  // elements per 16-byte vector
+};
+template <>
+struct Elt<DART_F32> {
+    using T = float;
+    static constexpr int kPerVec = 4;
+};
+
+template <dart_dtype_t D>
+__device__ __forceinline__ void unpack(const u32x4 v, float* z);
+
+template <>
+__device__ __forceinline__ void unpack<DART_BF16>(const u32x4 v, float* z) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        z[2 * i] = __uint_as_float(v[i] << 16);
+        z[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
+    }
+}
+
+template <>
+__device__ __forceinline__ void unpack<DART_F32>(const u32x4 v, float* z) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) z[i] = __uint_as_float(v[i]);
+}
+
+template <dart_dtype_t D>
+__device__ __forceinline__ float load_one(const void* row, int64_t col) {
+    if constexpr (D == DART_BF16)
+        return __uint_as_float((uint32_t)static_cast<const uint16_t*>(row)[col] << 16);
+    else
+        return static_cast<const float*>(row)[col];
+}
+
+template <dart_dtype_t D>
+__device__ __forceinline__ void store_one(void* row, int64_t col, float x) {
+    if constexpr (D == DART_BF16) {
+        __hip_bfloat16 b = __float2bfloat16(x);  // round to nearest even
+        static_cast<__hip_bfloat16*>(row)[col] = b;
+    } else {
+        static_cast<float*>(row)[col] = x;
+    }
+}
+
+template <dart_dtype_t D>
+__device__ __forceinline__ u32x4 pack(const float* d);
+
+template <>
+__device__ __forceinline__ u32x4 pack<DART_BF16>(const float* d) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        __hip_bfloat162 p = __float22bfloat162_rn(make_float2(d[2 * i], d[2 * i + 1]));
+        v[i] = *reinterpret_cast<const uint32_t*>(&p);
+    }
+    return v;
+}
+
+template <>
+__device__ __forceinline__ u32x4 pack<DART_F32>(const float* d) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(d[i]);
+    return v;
+}
+
+// ------------------------------------------------------------------------
+// online (max, normaliser, entropy) triple
+// ------------------------------------------------------------------------
+// For the elements seen so far, with m their maximum and x_v = (z_v - m) log2(e):
+//   s = sum_v 2^{x_v},   w = sum_v 2^{x_v} x_v.
+// Then lse = m + ln2 log2(s) and H = ln2 (log2(s) - w / s). Two triples merge
+// by rescaling to the larger maximum: s' = 2^{d} s, w' = 2^{d} (w + d s),
+// d = (m - m_new) log2(e). An empty triple has s == 0 and m == -inf.
+struct Triple {
+    float m, s, w;
+};
+
+__device__ __forceinline__ Triple triple_empty() { return Triple{-INFINITY, 0.f, 0.f}; }
+
+// Adds N elements. The running maximum is updated once per call; each element
+// then costs one FMA, one clamp, one exp2, one add and one FMA. The clamp keeps
+// 2^x * x finite for -inf logits (2^-256 is 0 in fp32, so no finite value moves).
+template <int N>
+__device__ __forceinline__ void triple_add(Triple& a, const float* z) {
+    float cm = z[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) cm = fmaxf(cm, z[i]);
+    if (cm > a.m) {
+        if (a.s > 0.f) {
+            const float d = (a.m - cm) * kLog2e;
+            const float sc = __builtin_amdgcn_exp2f(d);
+            a.w = sc * fmaf(d, a.s, a.w);
+            a.s *= sc;
+        }
+        a.m = cm;
+    }
+    if (a.m == -INFINITY) return;
+    const float mb = a.m * kLog2e;
+    float s = 0.f, w = 0.f;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const float x = fmaxf(fmaf(z[i], kLog2e, -mb), -256.f);
+        const float e = __builtin_amdgcn_exp2f(x);
+        s += e;
+        w = fmaf(e, x, w);
+    }
+    a.s += s;
+    a.w += w;
+}
+
+__device__ __forceinline__ Triple triple_merge(const Triple a, const Triple b) {
+    if (b.s == 0.f) return a;
+    if (a.s == 0.f) return b;
+    const float m = fmaxf(a.m, b.m);
+    const float da = (a.m - m) * kLog2e;
+    const float db = (b.m - m) * kLog2e;
+    const float ca = __builtin_amdgcn_exp2f(da);
+    const float cb = __builtin_amdgcn_exp2f(db);
+    Triple r;
+    r.m = m;
+    r.s = ca * a.s + cb * b.s;
+    r.w = ca * fmaf(da, a.s, a.w) + cb * fmaf(db, b.s, b.w);
+    return r;
+}
+
+__device__ __forceinline__ Triple triple_wave_reduce(Triple a) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        Triple b;
+        b.m = __shfl_xor(a.m, off);
+        b.s = __shfl_xor(a.s, off);
+        b.w = __shfl_xor(a.w, off);
+        a = triple_merge(a, b);
+    }
+    return a;
+}
+
+// Streaming kernels use BLOCK threads per row and UNROLL 16-byte vectors per
+// lane per iteration: vector j of the aligned body is read by lane j % BLOCK in
+// iteration j / (BLOCK * UNROLL), so every wave reads 1 KiB contiguous per load.
+constexpr int kRowThreads = 256;
+constexpr int kUnroll = 4;
+
+struct RowLayout {
+    int64_t head;      // scalar elements before the first 16-byte boundary
+    int64_t nvec;      // aligned 16-byte vectors
+    int64_t body_end;  // first element after the vectors
+    bool vector_ok;
+};
+
+template <dart_dtype_t D>
+__device__ __forceinline__ RowLayout row_layout(const void* row, int64_t V) {
+    using E = typename Elt<D>::T;
+    constexpr int EPV = Elt<D>::kPerVec;
+    RowLayout L;
+    const uintptr_t addr = reinterpret_cast<uintptr_t>(row);
+    L.vector_ok = (addr % sizeof(E)) == 0;
+    int64_t head = (int64_t)(((16 - (addr & 15)) & 15) / sizeof(E));
+    if (!L.vector_ok) head = V;
+    if (head > V) head = V;
+    L.head = head;
+    L.nvec = (V - head) / EPV;
+    L.body_end = head + L.nvec * EPV;
+    return L;
+}
+
+// ------------------------------------------------------------------------
+// K1: token statistics
+// ------------------------------------------------------------------------
+
+template <dart_dtype_t D>
+__global__ void __launch_bounds__(kRowThreads)
+tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
+                 const int32_t* __restrict__ target, float* __restrict__ logp,
+                 float* __restrict__ entropy, float* __restrict__ lse) {
+    using E = typename Elt<D>::T;
+    constexpr int EPV = Elt<D>::kPerVec;
+    constexpr int PER_IT = kRowThreads * kUnroll;
+    __shared__ Triple partial[kRowThreads / 64];
+
+    const int64_t t = blockIdx.x;
+    const int tid = threadIdx.x;
+    const E* row = static_cast<const E*>(logits) + t * ld;
+    // an out-of-range target id (a broken precondition) yields NaN, never a stray read
+    const int64_t y_in = target[t];
+    const bool y_ok = y_in >= 0 && y_in < V;
+    const int64_t y = y_ok ? y_in : -1;
+    const RowLayout L = row_layout<D>(row, V);
+    const u32x4* vrow = reinterpret_cast<const u32x4*>(row + L.head);
+
+    // The target element is left out of the lane sums and added once at the
+    // end, so that 1 - p_target (and logp near 0) keep full relative accuracy.
+    const int64_t vy = (y >= L.head && y < L.body_end) ? (y - L.head) / EPV : -1;
+    const int64_t it_y = vy >= 0 ? vy / PER_IT : -1;
+    const int64_t nfull = L.nvec / PER_IT;
+
+    Triple acc = triple_empty();
+    for (int64_t it = 0; it < nfull; ++it) {
+        u32x4 v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            v[u] = __builtin_nontemporal_load(vrow + it * PER_IT + u * kRowThreads + tid);
+        float z[kUnroll * EPV];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) unpack<D>(v[u], z + u * EPV);
+        if (it == it_y) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) {
+                    const int64_t col = L.head + (it * PER_IT + u * kRowThreads + tid) * EPV + e;
+                    if (col == y) z[u * EPV + e] = -INFINITY;
+                }
+        }
+        triple_add<kUnroll * EPV>(acc, z);
+    }
+    for (int64_t j = nfull * PER_IT + tid; j < L.nvec; j += kRowThreads) {
+        float z[EPV];
+        unpack<D>(__builtin_nontemporal_load(vrow + j), z);
+        if (j == vy) {
+#pragma unroll
+            for (int e = 0; e < EPV; ++e)
+                if (L.head + j * EPV + e == y) z[e] = -INFINITY;
+        }
+        triple_add<EPV>(acc, z);
+    }
+    const int64_t nscalar = L.head + (V - L.body_end);
+    for (int64_t k = tid; k < nscalar; k += kRowThreads) {
+        const int64_t col = k < L.head ? k : L.body_end + (k - L.head);
+        float z1[1] = {col == y ? -INFINITY : load_one<D>(row, col)};
+        triple_add<1>(acc, z1);
+    }
+
+    acc = triple_wave_reduce(acc);
+    const int wave = tid >> 6;
+    if ((tid & 63) == 0) partial[wave] = acc;
+    __syncthreads();
+    if (tid != 0) return;
+    Triple x = partial[0];
+#pragma unroll
+    for (int i = 1; i < kRowThreads / 64; ++i) x = triple_merge(x, partial[i]);
+
+    // add the target element
+    const float zy = y_ok ? load_one<D>(row, y) : __builtin_nanf("");
+    const float M = fmaxf(x.m, zy);
+    float sx = 0.f, wx = 0.f;
+    if (x.s > 0.f) {
+        const float dx = (x.m - M) * kLog2e;
+        const float cx = __builtin_amdgcn_exp2f(dx);
+        sx = cx * x.s;
+        wx = cx * fmaf(dx, x.s, x.w);
+    }
+    const float xy = (zy - M) * kLog2e;
+    const float ey = zy == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(xy);
+    const float s = sx + ey;
+    const float w = ey > 0.f ? fmaf(ey, xy, wx) : wx;
+    const float log2s = log2f(s);
+    const float ln_s = log2s * kLn2;
+    lse[t] = M + ln_s;
+    entropy[t] = fmaxf(kLn2 * (log2s - w / s), 0.f);
+    // p_y = ey / (sx + ey): -log1p(sx / ey) is exact to a few ulps when p_y -> 1
+    logp[t] = sx < ey ? -log1pf(sx / ey) : (zy - M) - ln_s;
+}
+
+// ------------------------------------------------------------------------
+// K2: step entropy + top-k step selection
+// ------------------------------------------------------------------------
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+    return x;
+}
+
+// Token range of step s, clamped to [0, T] so that malformed offsets (a broken
+// precondition) give meaningless numbers but never an out-of-bounds access.
+__device__ __forceinline__ void step_bounds(const int32_t* off, int64_t s, int64_t T, int64_t& b,
+                                            int64_t& e) {
+    b = min(max((int64_t)off[s], (int64_t)0), T);
+    e = min(max((int64_t)off[s + 1], b), T);
+}
+
+// Order-preserving map of a float to uint32 (larger float -> larger key); -0 == +0.
+__device__ __forceinline__ uint32_t float_key(float f) {
+    uint32_t u = __float_as_uint(f == 0.f ? 0.f : f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__global__ void __launch_bounds__(kSelThreads)
+step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
+                   int64_t S, int64_t k, float* __restrict__ step_H, uint8_t* __restrict__ mask,
+                   int32_t* __restrict__ n_kept) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sel_bin;
+    __shared__ int64_t sel_remaining;
+    __shared__ int64_t wave_count[kSelWaves];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+
+    // step means: one wave per step, lanes stride the step's tokens, fixed
+    // butterfly order (identical steps give identical means)
+    for (int64_t s = wave; s < S; s += kSelWaves) {
+        int64_t b, e;
+        step_bounds(off, s, T, b, e);
+        double sum = 0.0;
+        for (int64_t i = b + lane; i < e; i += 64) sum += (double)H[i];
+        sum = wave_sum(sum);
+        if (lane == 0) step_H[s] = (float)(sum / (double)(e - b));
+    }
+    __syncthreads();
+
+    if (k <= 0 || k >= S) {
+        for (int64_t s = tid; s < S; s += kSelThreads) mask[s] = k > 0 ? 1 : 0;
+        if (tid == 0 && n_kept) *n_kept = (int32_t)(k > 0 ? S : 0);
+        return;
+    }
+
+    // radix select of the k-th largest key, 8 bits per pass from the top
+    uint32_t prefix = 0, pmask = 0;
+    int64_t remaining = k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
+        __syncthreads();
+        for (int64_t s = tid; s < S; s += kSelThreads) {
+            const uint32_t key = float_key(step_H[s]);
+            if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (wave == 0) {
+            // lane l holds bins 255-4l .. 252-4l (descending key order)
+            const int b0 = 255 - 4 * lane;
+            const uint32_t c0 = hist[b0], c1 = hist[b0 - 1], c2 = hist[b0 - 2], c3 = hist[b0 - 3];
+            const int64_t local = (int64_t)c0 + c1 + c2 + c3;
+            int64_t incl = local;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int64_t o = __shfl_up(incl, d);
+                if (lane >= d) incl += o;
+            }
+            const int64_t excl = incl - local;
+            if (excl < remaining && remaining <= incl) {
+                int64_t r = remaining - excl;
+                int bin = b0;
+                if (r > c0) {
+                    r -= c0;
+                    bin = b0 - 1;
+                    if (r > c1) {
+                        r -= c1;
+                        bin = b0 - 2;
+                        if (r > c2) {
+                            r -= c2;
+                            bin = b0 - 3;
+                        }
+                    }
+                }
+                sel_bin = (uint32_t)bin;
+                sel_remaining = r;
+            }
+        }
+        __syncthreads();
+        prefix |= sel_bin << shift;
+        pmask |= 255u << shift;
+        remaining = sel_remaining;
+        __syncthreads();
+    }
+
+    // keep keys above the k-th; of the keys equal to it keep the first
+    // `remaining` in step order (block scan over tiles of kSelThreads steps)
+    int64_t carry = 0;
+    for (int64_t base = 0; base < S; base += kSelThreads) {
+        const int64_t s = base + tid;
+        const uint32_t key = s < S ? float_key(step_H[s]) : 0u;
+        const bool eq = s < S && key == prefix;
+        const uint64_t ballot = __ballot(eq);
+        const int before = __popcll(ballot & ((1ull << lane) - 1ull));
+        if (lane == 0) wave_count[wave] = __popcll(ballot);
+        __syncthreads();
+        int64_t wave_before = 0, total = 0;
+        for (int i = 0; i < kSelWaves; ++i) {
+            if (i < wave) wave_before += wave_count[i];
+            total += wave_count[i];
+        }
+        if (s < S) {
+            const int64_t rank = carry + wave_before + before;
+            mask[s] = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
+        }
+        carry += total;
+        __syncthreads();
+    }
+    if (tid == 0 && n_kept) *n_kept = (int32_t)k;
+}
+
+// ------------------------------------------------------------------------
+// K3: per-token TIS / clip coefficient and the loss
+// ------------------------------------------------------------------------
+
+constexpr int kCoefThreads = 1024;
+constexpr int kCoefWaves = kCoefThreads / 64;
+
+__global__ void __launch_bounds__(kCoefThreads)
+tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
+                const float* __restrict__ lp_roll, const float* __restrict__ adv,
+                const int32_t* __restrict__ off, int64_t S, const uint8_t* __restrict__ mask,
+                float eps_low, float eps_high, float C, float log_C, float* __restrict__ coef,
+                double* __restrict__ loss, float* __restrict__ stats) {
+    __shared__ int64_t red_i[kCoefWaves];
+    __shared__ double red_d[4][kCoefWaves];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+
+    int64_t n_local = 0;
+    for (int64_t s = tid; s < S; s += kCoefThreads) {
+        int64_t b, e;
+        step_bounds(off, s, T, b, e);
+        if (mask[s]) n_local += e - b;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) n_local += __shfl_xor(n_local, o);
+    if (lane == 0) red_i[wave] = n_local;
+    __syncthreads();
+    int64_t N = 0;
+    for (int i = 0; i < kCoefWaves; ++i) N += red_i[i];
+
+    const double inv_n = N > 0 ? 1.0 / (double)N : 0.0;
+    const float lo = 1.f - eps_low, hi = 1.f + eps_high;
+    double l_acc = 0.0, w_acc = 0.0, n_clip = 0.0, n_cap = 0.0;
+    for (int64_t s = wave; s < S; s += kCoefWaves) {
+        int64_t b, e;
+        step_bounds(off, s, T, b, e);
+        const bool kept = mask[s] != 0 && N > 0;
+        for (int64_t t = b + lane; t < e; t += 64) {
+            if (!kept) {
+                coef[t] = 0.f;
+                continue;
+            }
+            const float A = adv[t];
+            const float r = expf(logp[t] - lp_old[t]);
+            const float d = lp_old[t] - lp_roll[t];
+            const bool capped = d >= log_C;
+            const float w = capped ? C : fminf(expf(d), C);
+            const float rc = fminf(fmaxf(r, lo), hi);
+            const float u = r * A;
+            const float c = rc * A;
+            const bool gate = u <= c;
+            l_acc -= (double)w * (double)fminf(u, c) * inv_n;
+            coef[t] = gate ? (float)(-(double)w * (double)A * (double)r * inv_n) : 0.f;
+            w_acc += (double)w;
+            n_clip += gate ? 0.0 : 1.0;
+            n_cap += capped ? 1.0 : 0.0;
+        }
+    }
+    l_acc = wave_sum(l_acc);
+    w_acc = wave_sum(w_acc);
+    n_clip = wave_sum(n_clip);
+    n_cap = wave_sum(n_cap);
+    if (lane == 0) {
+        red_d[0][wave] = l_acc;
+        red_d[1][wave] = w_acc;
+        red_d[2][wave] = n_clip;
+        red_d[3][wave] = n_cap;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double L = 0.0, W = 0.0, NC = 0.0, NK = 0.0;
+        for (int i = 0; i < kCoefWaves; ++i) {
+            L += red_d[0][i];
+            W += red_d[1][i];
+            NC += red_d[2][i];
+            NK += red_d[3][i];
+        }
+        loss[0] = L;
+        if (stats) {
+            stats[0] = (float)(NC * inv_n);
+            stats[1] = (float)(W * inv_n);
+            stats[2] = (float)(NK * inv_n);
+            stats[3] = (float)N;
+        }
+    }
+}
+
+// ------------------------------------------------------------------------
+// K4: dlogits = coef * (onehot(target) - softmax(z))
+// ------------------------------------------------------------------------
+
+template <dart_dtype_t D>
+__global__ void __launch_bounds__(kRowThreads)
+tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __restrict__ target,
+                const float* __restrict__ lse, const float* __restrict__ logp,
+                const float* __restrict__ coef, void* dlogits, int64_t ld_out) {
+    using E = typename Elt<D>::T;
+    constexpr int EPV = Elt<D>::kPerVec;
+    constexpr int PER_IT = kRowThreads * kUnroll;
+
+    const int64_t t = blockIdx.x;
+    const int tid = threadIdx.x;
+    const E* row = static_cast<const E*>(logits) + t * ld;
+    E* orow = static_cast<E*>(dlogits) + t * ld_out;
+    const int64_t y_in = target[t];
+    const int64_t y = (y_in >= 0 && y_in < V) ? y_in : -1;
+    const float g = coef[t];
+    const float neg_g = -g;
+    const float lb = lse[t] * kLog2e;
+    // 1 - p_y = -expm1(logp_y), accurate when p_y -> 1
+    const float dy = g * -expm1f(logp[t]);
+
+    RowLayout L = row_layout<D>(row, V);
+    const RowLayout Lo = row_layout<D>(orow, V);
+    if (L.head != Lo.head || !Lo.vector_ok) L = RowLayout{V, 0, V, false};
+    const u32x4* vrow = reinterpret_cast<const u32x4*>(row + L.head);
+    u32x4* vout = reinterpret_cast<u32x4*>(orow + L.head);
+    const int64_t vy = (y >= L.head && y < L.body_end) ? (y - L.head) / EPV : -1;
+    const int64_t it_y = vy >= 0 ? vy / PER_IT : -1;
+    const int64_t nfull = L.nvec / PER_IT;
+
+    for (int64_t it = 0; it < nfull; ++it) {
+        u32x4 v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            v[u] = __builtin_nontemporal_load(vrow + it * PER_IT + u * kRowThreads + tid);
+        float z[kUnroll * EPV];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) unpack<D>(v[u], z + u * EPV);
+#pragma unroll
+        for (int i = 0; i < kUnroll * EPV; ++i)
+            z[i] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[i], kLog2e, -lb));
+        if (it == it_y) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) {
+                    const int64_t col = L.head + (it * PER_IT + u * kRowThreads + tid) * EPV + e;
+                    if (col == y) z[u * EPV + e] = dy;
+                }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            __builtin_nontemporal_store(pack<D>(z + u * EPV),
+                                        vout + it * PER_IT + u * kRowThreads + tid);
+    }
+    for (int64_t j = nfull * PER_IT + tid; j < L.nvec; j += kRowThreads) {
+        float z[EPV];
+        unpack<D>(__builtin_nontemporal_load(vrow + j), z);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) {
+            z[e] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[e], kLog2e, -lb));
+            if (L.head + j * EPV + e == y) z[e] = dy;
+        }
+        __builtin_nontemporal_store(pack<D>(z), vout + j);
+    }
+    const int64_t nscalar = L.head + (V - L.body_end);
+    for (int64_t k = tid; k < nscalar; k += kRowThreads) {
+        const int64_t col = k < L.head ? k : L.body_end + (k - L.head);
+        const float x = load_one<D>(row, col);
+        const float d = col == y ? dy : neg_g * __builtin_amdgcn_exp2f(fmaf(x, kLog2e, -lb));
+        store_one<D>(orow, col, d);
+    }
+}
+
+// ------------------------------------------------------------------------
+// host helpers
+// ------------------------------------------------------------------------
+
+bool bad_dtype(dart_dtype_t d) { return d != DART_F32 && d != DART_BF16; }
+
+size_t elem_size(dart_dtype_t d) { return d == DART_F32 ? 4 : 2; }
+
+dart_status_t launch_status() {
+    return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dart_status_string(dart_status_t status) {
+    switch (status) {
+        case DART_OK: return "DART_OK";
+        case DART_ERR_INVALID_ARG: return "DART_ERR_INVALID_ARG";
+        case DART_ERR_UNSUPPORTED: return "DART_ERR_UNSUPPORTED";
+        case DART_ERR_HIP: return "DART_ERR_HIP";
+    }
+    return "DART_ERR_UNKNOWN";
+}
+
+int64_t dart_kept_steps(int64_t S, double rho) {
+    if (S < 0 || !(rho >= 0.0 && rho <= 1.0)) return -1;
+    double k = ceil(rho * (double)S - 1e-6);
+    if (k < 0.0) k = 0.0;
+    if (k > (double)S) k = (double)S;
+    return (int64_t)k;
+}
+
+dart_status_t dart_tok_stats(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                             int64_t ld, const int32_t* target, float* logp, float* entropy,
+                             float* lse, hipStream_t stream) {
+    if (!logits || !target || !logp || !entropy || !lse) return DART_ERR_INVALID_ARG;
+    if (bad_dtype(dtype) || T < 1 || V < 1 || ld < V || T > 0x7FFFFFFFll)
+        return DART_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(logits) % elem_size(dtype)) return DART_ERR_INVALID_ARG;
+    const dim3 grid((unsigned)T), block(kRowThreads);
+    if (dtype == DART_BF16)
+        hipLaunchKernelGGL(tok_stats_kernel<DART_BF16>, grid, block, 0, stream, logits, V, ld,
+                           target, logp, entropy, lse);
+    else
+        hipLaunchKernelGGL(tok_stats_kernel<DART_F32>, grid, block, 0, stream, logits, V, ld,
+                           target, logp, entropy, lse);
+    return launch_status();
+}
+
+dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* step_offsets,
+                               int64_t S, double rho, float* step_entropy, uint8_t* step_mask,
+                               int32_t* n_kept_steps, hipStream_t stream) {
+    if (!entropy || !step_offsets || !step_entropy || !step_mask) return DART_ERR_INVALID_ARG;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
+    const int64_t k = dart_kept_steps(S, rho);
+    if (k < 0) return DART_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(step_select_kernel, dim3(1), dim3(kSelThreads), 0, stream, entropy, T,
+                       step_offsets, S, k, step_entropy, step_mask, n_kept_steps);
+    return launch_status();
+}
+
+dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_old,
+                                const float* logp_rollout, const float* adv,
+                                const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
+                                float eps_low, float eps_high, float C, double* loss,
+                                float* tok_coef, float* stats, hipStream_t stream) {
+    if (!logp || !logp_old || !logp_rollout || !adv || !step_offsets || !step_mask || !loss ||
+        !tok_coef)
+        return DART_ERR_INVALID_ARG;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
+    if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
+    const float log_C = isinf(C) ? INFINITY : (float)log((double)C);
+    hipLaunchKernelGGL(tis_coef_kernel, dim3(1), dim3(kCoefThreads), 0, stream, T, logp, logp_old,
+                       logp_rollout, adv, step_offsets, S, step_mask, eps_low, eps_high, C, log_C,
+                       tok_coef, loss, stats);
+    return launch_status();
+}
+
+dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                            int64_t ld, const int32_t* target, const float* logp,
+                            const float* lse, const float* tok_coef, void* dlogits,
+                            int64_t ld_out, hipStream_t stream) {
+    if (!logits || !target || !logp || !lse || !tok_coef || !dlogits) return DART_ERR_INVALID_ARG;
+    if (bad_dtype(dtype) || T < 1 || V < 1 || ld < V || ld_out < V || T > 0x7FFFFFFFll)
+        return DART_ERR_INVALID_ARG;
+    const size_t es = elem_size(dtype);
+    if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
+        return DART_ERR_INVALID_ARG;
+    // in place is allowed only as an exact alias with the same row stride
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits);
+    const uintptr_t a1 = a0 + (uintptr_t)(((T - 1) * ld + V) * (int64_t)es);
+    const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits);
+    const uintptr_t b1 = b0 + (uintptr_t)(((T - 1) * ld_out + V) * (int64_t)es);
+    const bool alias = a0 == b0 && ld == ld_out;
+    if (!alias && a0 < b1 && b0 < a1) return DART_ERR_INVALID_ARG;
+    const dim3 grid((unsigned)T), block(kRowThreads);
+    if (dtype == DART_BF16)
+        hipLaunchKernelGGL(tis_grad_kernel<DART_BF16>, grid, block, 0, stream, logits, V, ld,
+                           target, lse, logp, tok_coef, dlogits, ld_out);
+    else
+        hipLaunchKernelGGL(tis_grad_kernel<DART_F32>, grid, block, 0, stream, logits, V, ld,
+                           target, lse, logp, tok_coef, dlogits, ld_out);
+    return launch_status();
+}
+
+dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                                    int64_t ld, const int32_t* target, const float* logp,
+                                    const float* lse, const float* logp_old,
+                                    const float* logp_rollout, const float* adv,
+                                    const int32_t* step_offsets, int64_t S,
+                                    const uint8_t* step_mask, float eps_low, float eps_high,
+                                    float C, void* dlogits, int64_t ld_out, double* loss,
+                                    float* tok_coef, float* stats, hipStream_t stream) {
+    // validate both halves before enqueuing either
+    if (!logits || !target || !lse || !dlogits) return DART_ERR_INVALID_ARG;
+    if (bad_dtype(dtype) || V < 1 || ld < V || ld_out < V) return DART_ERR_INVALID_ARG;
+    const size_t es = elem_size(dtype);
+    if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
+        return DART_ERR_INVALID_ARG;
+    if (T >= 1) {
+        const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits);
+        const uintptr_t a1 = a0 + (uintptr_t)(((T - 1) * ld + V) * (int64_t)es);
+        const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits);
+        const uintptr_t b1 = b0 + (uintptr_t)(((T - 1) * ld_out + V) * (int64_t)es);
+        const bool alias = a0 == b0 && ld == ld_out;
+        if (!alias && a0 < b1 && b0 < a1) return DART_ERR_INVALID_ARG;
+    }
+    dart_status_t st = dart_tis_loss_fwd(T, logp, logp_old, logp_rollout, adv, step_offsets, S,
+                                         step_mask, eps_low, eps_high, C, loss, tok_coef, stats,
+                                         stream);
+    if (st != DART_OK) return st;
+    return dart_tis_grad(logits, dtype, T, V, ld, target, logp, lse, tok_coef, dlogits, ld_out,
+                         stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,125 @@
+"""The C-ABI library loads, exports every function include/dart.h declares,
+and rejects bad scalar arguments on the host (no device work is enqueued for
+any case here)."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2509_23866_amd as dart
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names.update(re.findall(r"\b(dart_[a-z_0-9]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = dart.load_library()
+    declared = _declared_functions()
+    assert {"dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), f"{name} is declared in include/ but not exported"
+    assert set(dart.EXPORTED) == declared
+
+
+def test_kept_steps_host_helper():
+    for rho, S, k in [(0.8, 240, 192), (0.8, 64, 52), (0.5, 16, 8), (0.5, 1600, 800),
+                      (0.25, 256, 64), (0.0, 9, 0), (1.0, 9, 9), (0.01, 3, 1)]:
+        assert dart.dart_kept_steps(S, rho) == k
+    assert dart.dart_kept_steps(10, 1.5) == -1
+    assert dart.dart_kept_steps(10, -0.1) == -1
+    assert dart.dart_kept_steps(10, float("nan")) == -1
+    assert dart.dart_kept_steps(-1, 0.5) == -1
+
+
+def test_status_strings():
+    assert dart.dart_status_string(0) == "DART_OK"
+    assert dart.dart_status_string(1) == "DART_ERR_INVALID_ARG"
+    assert dart.dart_status_string(3) == "DART_ERR_HIP"
+    assert dart.dart_status_string(42) == "DART_ERR_UNKNOWN"
+
+
+def _gpu_visible():
+    import torch
+
+    return torch.cuda.device_count() > 0
+
+
+# Fake, never-dereferenced addresses. Every call below fails a host-side check
+# before any launch; on a machine with a GPU the module skips them anyway.
+P = 4096
+INF = float("inf")
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("args", [
+    (0, 1, 4, 8, 8, P, P, P, P),          # null logits
+    (P, 1, 4, 8, 8, 0, P, P, P),          # null target
+    (P, 1, 4, 8, 8, P, 0, P, P),          # null logp
+    (P, 1, 0, 8, 8, P, P, P, P),          # T = 0
+    (P, 1, 4, 0, 8, P, P, P, P),          # V = 0
+    (P, 1, 4, 8, 7, P, P, P, P),          # ld < V
+    (P, 7, 4, 8, 8, P, P, P, P),          # unknown dtype
+    (P + 1, 1, 4, 8, 8, P, P, P, P),      # bf16 logits not 2-byte aligned
+])
+def test_tok_stats_rejects(args):
+    lib = dart.load_library()
+    assert lib.dart_tok_stats(*args, None) == dart.DART_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("T,S,rho,null", [
+    (10, 0, 0.5, None), (10, 11, 0.5, None), (0, 1, 0.5, None), (10, 2, 1.01, None),
+    (10, 2, -0.01, None), (10, 2, float("nan"), None), (10, 2, 0.5, 0), (10, 2, 0.5, 2),
+    (10, 2, 0.5, 5), (10, 2, 0.5, 6),
+])
+def test_step_select_rejects(T, S, rho, null):
+    lib = dart.load_library()
+    ptrs = [P, P, P, P, P]  # entropy, offsets, step_entropy, mask, n_kept
+    idx = {0: 0, 2: 1, 5: 2, 6: 3}
+    if null is not None:
+        ptrs[idx[null]] = 0
+    rc = lib.dart_step_select(ptrs[0], T, ptrs[1], S, rho, ptrs[2], ptrs[3], ptrs[4], None)
+    assert rc == dart.DART_ERR_INVALID_ARG
+
+
+def _tis_args(**kw):
+    a = dict(logits=P, dtype=1, T=4, V=8, ld=8, target=P, logp=P, lse=P, lp_old=P, lp_roll=P,
+             adv=P, off=P, S=2, mask=P, eps_low=0.2, eps_high=0.2, C=2.0, dlogits=1 << 20,
+             ld_out=8, loss=P, coef=P, stats=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(logits=0), dict(target=0), dict(logp=0), dict(lse=0), dict(lp_old=0), dict(lp_roll=0),
+    dict(adv=0), dict(off=0), dict(mask=0), dict(dlogits=0), dict(loss=0), dict(coef=0),
+    dict(T=0), dict(V=0), dict(ld=7), dict(ld_out=7), dict(S=0), dict(S=5), dict(dtype=3),
+    dict(eps_low=-0.1), dict(eps_high=float("nan")), dict(C=0.0), dict(C=-1.0),
+    dict(C=float("nan")), dict(dlogits=P + 2),  # partial overlap with logits
+    dict(dlogits=P, ld_out=9),  # same base, different stride
+    dict(dlogits=(1 << 20) + 1),  # bf16 output not 2-byte aligned
+])
+def test_tis_loss_rejects(kw):
+    lib = dart.load_library()
+    assert lib.dart_tis_loss_fwd_bwd(*_tis_args(**kw), None) == dart.DART_ERR_INVALID_ARG
+
+
+def test_python_binding_requires_built_library(monkeypatch, tmp_path):
+    """No CPU fallback: a missing library is an error, not a silent path."""
+    monkeypatch.setattr(dart, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(dart, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        dart.load_library()

@@ -18,7 +18,9 @@ import oracle
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 MUTATIONS = {
-    "entropy_in_bits": ("ksum_add(&h, -p * log(p))", "ksum_add(&h, -p * log2(p))"),
+    "entropy_in_bits": ("ksum_add(&h, -p * log_p)", "ksum_add(&h, -p * log_p / log(2.0))"),
+    "entropy_sign": ("ksum_add(&h, -p * log_p)", "ksum_add(&h, p * log_p)"),
+    "probability_unnormalised": ("const double p = e[v] / sum;", "const double p = e[v];"),
     "logp_vs_max_not_normaliser": ("target[t]) - log_norm;", "target[t]) - m;"),
     "step_mean_wrong_denominator": ("/ (double)(off[s + 1] - off[s]);",
                                     "/ (double)(off[s + 1] - off[s] + 1);"),
