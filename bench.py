@@ -40,6 +40,9 @@ def parse_args():
                     choices=["tiny", "vlm7b", "microbatch", "longhorizon", "edge"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="0 = the process's CPU affinity (max 16)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the timed steps, run one plain device copy of this many MiB "
+                         "(torch copy kernel) so that hardware counters can be scaled by it")
     return ap.parse_args()
 
 
@@ -151,6 +154,17 @@ def main():
         dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream)
         if ev:
             ev[3].record(stream)
+
+    if args.calib_copy_mib:
+        # a plain elementwise kernel that reads and writes exactly this many
+        # bytes (a same-dtype copy_ would go to the DMA engine, not a kernel)
+        n = args.calib_copy_mib * (1 << 20) // 2
+        src = torch.ones(n, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize(dev)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize(dev)
+        del src, dst
 
     for _ in range(args.warmup):
         if pristine is not None:
