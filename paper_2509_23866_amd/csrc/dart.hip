@@ -120,11 +120,12 @@ struct Triple {
 
 __device__ __forceinline__ Triple triple_empty() { return Triple{-INFINITY, 0.f, 0.f}; }
 
-// Adds N elements. The running maximum is updated once per call; each element
-// then costs one FMA, one clamp, one exp2, one add and one FMA. The clamp keeps
-// 2^x * x finite for -inf logits (2^-256 is 0 in fp32, so no finite value moves).
+// Adds N elements exactly: the running maximum is updated once per call, then
+// every element costs one FMA, one clamp, one exp2, one add and one FMA. The
+// clamp keeps 2^x * x finite for -inf logits (2^-256 is 0 in fp32, so no finite
+// value moves).
 template <int N>
-__device__ __forceinline__ void triple_add(Triple& a, const float* z) {
+__device__ __forceinline__ void triple_add_exact(Triple& a, const float* z) {
     float cm = z[0];
 #pragma unroll
     for (int i = 1; i < N; ++i) cm = fmaxf(cm, z[i]);
@@ -149,6 +150,36 @@ __device__ __forceinline__ void triple_add(Triple& a, const float* z) {
     }
     a.s += s;
     a.w += w;
+}
+
+// Adds N elements against a lazy reference: the triple's m need not be the
+// maximum, only some value that keeps every 2^x term small. A lane takes its
+// first finite element as the reference and keeps it while a chunk's terms sum
+// below 2^30 (x <= ~30, so fp32 keeps H and lse to a few 1e-6) and are not NaN;
+// otherwise (a much larger logit, or a -inf logit making 0 * -inf) the chunk is
+// redone exactly, which also moves the reference to the chunk maximum. Per
+// element this costs one FMA, one exp2, one add and one FMA: the per-element
+// maximum and clamp leave the hot loop.
+template <int N>
+__device__ __forceinline__ void triple_add(Triple& a, const float* z) {
+    if (a.m == -INFINITY) a.m = z[0];
+    if (a.m != -INFINITY) {
+        const float mb = a.m * kLog2e;
+        float s = 0.f, w = 0.f;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const float x = fmaf(z[i], kLog2e, -mb);
+            const float e = __builtin_amdgcn_exp2f(x);
+            s += e;
+            w = fmaf(e, x, w);
+        }
+        if (s < 0x1p30f && w == w) {
+            a.s += s;
+            a.w += w;
+            return;
+        }
+    }
+    triple_add_exact<N>(a, z);
 }
 
 __device__ __forceinline__ Triple triple_merge(const Triple a, const Triple b) {
