@@ -52,6 +52,16 @@ def _load():
         if not os.path.exists(LIB):
             raise RuntimeError(f"{LIB} is not built; run __graft_entry__.build()")
         lib = ctypes.CDLL(LIB)
+        lib.oracle_token_stats_ex.restype = None
+        lib.oracle_token_stats_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _D, _P, _P,
+                                              _P, ctypes.c_int]
+        lib.oracle_tis_loss_ex.restype = _D
+        lib.oracle_tis_loss_ex.argtypes = [_I64, _P, _P, _P, _P, _P, _P, _I64, _P, _D, _D, _D,
+                                           ctypes.c_int, _D, ctypes.c_int, ctypes.c_int, _P, _P,
+                                           _P, _P]
+        lib.oracle_dlogits_ex.restype = None
+        lib.oracle_dlogits_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _D, _P,
+                                          ctypes.c_int]
         lib.oracle_token_stats.restype = None
         lib.oracle_token_stats.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
                                            ctypes.c_int]
@@ -95,8 +105,9 @@ def _logits_arg(z):
     raise TypeError("logits must be float32 or bfloat16 bit patterns (uint16)")
 
 
-def token_stats(z, target, nthreads=None):
-    """Per-row (logp, H, lse) in float64 for logits rows ``z`` [n, V]."""
+def token_stats(z, target, nthreads=None, inv_temp=1.0):
+    """Per-row (logp, H, lse) in float64 for logits rows ``z`` [n, V], of the
+    distribution softmax(inv_temp * z)."""
     lib = _load()
     z, dt = _logits_arg(z)
     n, V = z.shape
@@ -106,8 +117,13 @@ def token_stats(z, target, nthreads=None):
     logp = np.empty(n, np.float64)
     H = np.empty(n, np.float64)
     lse = np.empty(n, np.float64)
-    lib.oracle_token_stats(z.ctypes.data, dt, n, V, ld, target.ctypes.data, logp.ctypes.data,
-                           H.ctypes.data, lse.ctypes.data, nthreads or default_threads())
+    if inv_temp == 1.0:
+        lib.oracle_token_stats(z.ctypes.data, dt, n, V, ld, target.ctypes.data, logp.ctypes.data,
+                               H.ctypes.data, lse.ctypes.data, nthreads or default_threads())
+    else:
+        lib.oracle_token_stats_ex(z.ctypes.data, dt, n, V, ld, target.ctypes.data,
+                                  float(inv_temp), logp.ctypes.data, H.ctypes.data,
+                                  lse.ctypes.data, nthreads or default_threads())
     return logp, H, lse
 
 
@@ -160,7 +176,43 @@ def tis_loss(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C):
     return dict(L=float(L), g=g, ell=ell, boundary=boundary.astype(bool), stats=stats)
 
 
-def dlogits(z, target, lse, g, nthreads=None):
+KL = {"none": 0, "k1": 1, "k2": 2, "k3": 3}
+AGG = {"token_mean": 0, "token_mean_all": 1, "step_mean": 2}
+RATIO = {"token": 0, "step_geomean": 1, "step_product": 2}
+
+
+def tis_loss_ex(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C, lp_ref=None,
+                kl="none", beta=0.0, agg="token_mean", ratio="token"):
+    """The loss with the KL term, aggregation and ratio level selectable.
+    Returns dict(L, g, ell, boundary, stats[6])."""
+    lib = _load()
+    logp = _c(logp, np.float64)
+    T = logp.size
+    lp_old = _c(lp_old, np.float32)
+    lp_roll = _c(lp_roll, np.float32)
+    adv = _c(adv, np.float32)
+    off = _c(off, np.int32)
+    mask = _c(mask, np.uint8)
+    S = off.size - 1
+    if KL[kl] != 0:
+        lp_ref = _c(lp_ref, np.float32)
+        assert lp_ref.size == T
+    assert lp_old.size == T and lp_roll.size == T and adv.size == T and mask.size == S
+    assert off[0] == 0 and off[-1] == T
+    g = np.empty(T, np.float64)
+    ell = np.empty(T, np.float64)
+    boundary = np.empty(T, np.uint8)
+    stats = np.empty(6, np.float64)
+    L = lib.oracle_tis_loss_ex(T, logp.ctypes.data, lp_old.ctypes.data, lp_roll.ctypes.data,
+                               None if KL[kl] == 0 else lp_ref.ctypes.data, adv.ctypes.data,
+                               off.ctypes.data, S, mask.ctypes.data, float(eps_low),
+                               float(eps_high), float(C), KL[kl], float(beta), AGG[agg],
+                               RATIO[ratio], g.ctypes.data, ell.ctypes.data, boundary.ctypes.data,
+                               stats.ctypes.data)
+    return dict(L=float(L), g=g, ell=ell, boundary=boundary.astype(bool), stats=stats)
+
+
+def dlogits(z, target, lse, g, nthreads=None, inv_temp=1.0):
     """float64 [n, V] gradient rows for logits rows ``z``."""
     lib = _load()
     z, dt = _logits_arg(z)
@@ -170,8 +222,13 @@ def dlogits(z, target, lse, g, nthreads=None):
     lse = _c(lse, np.float64)
     g = _c(g, np.float64)
     out = np.empty((n, V), np.float64)
-    lib.oracle_dlogits(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
-                       g.ctypes.data, out.ctypes.data, nthreads or default_threads())
+    if inv_temp == 1.0:
+        lib.oracle_dlogits(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
+                           g.ctypes.data, out.ctypes.data, nthreads or default_threads())
+    else:
+        lib.oracle_dlogits_ex(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
+                              g.ctypes.data, float(inv_temp), out.ctypes.data,
+                              nthreads or default_threads())
     return out
 
 

@@ -58,13 +58,14 @@ static double logit_at(const void* z, int dtype, int64_t ld, int64_t t, int64_t 
 
 /* Sec. 4.3: p_v = softmax(z)_v, H = -sum_v p_v log p_v (nats, R10: natural log),
  * and log pi(y) = z_y - log sum_v exp(z_v) for the target id y (Eq. 1 numerator).
- * Per row: (1) the maximum m; (2) e_v = exp(z_v - m) and their sum s, so that
- * lse = m + log s; (3) p_v = e_v / s and log p_v = z_v - lse, summed into the
- * entropy from its definition. A term with p_v == 0 contributes 0 (R9: -inf
- * logits allowed, 0 log 0 := 0). */
-void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
-                        const int32_t* target, double* logp, double* H, double* lse,
-                        int nthreads) {
+ * The logits are first multiplied by inv_temp (an inverse sampling temperature;
+ * 1 in the paper, App. A.4). Per row: (1) the maximum m; (2) e_v = exp(z_v - m)
+ * and their sum s, so that lse = m + log s; (3) p_v = e_v / s and
+ * log p_v = z_v - lse, summed into the entropy from its definition. A term with
+ * p_v == 0 contributes 0 (R9: -inf logits allowed, 0 log 0 := 0). */
+void oracle_token_stats_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
+                           const int32_t* target, double inv_temp, double* logp, double* H,
+                           double* lse, int nthreads) {
     if (nthreads < 1) nthreads = 1;
 #pragma omp parallel num_threads(nthreads)
     {
@@ -73,12 +74,12 @@ void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int6
         for (int64_t t = 0; t < nrows; ++t) {
             double m = -INFINITY;
             for (int64_t v = 0; v < V; ++v) {
-                double x = logit_at(z, dtype, ld, t, v);
+                double x = inv_temp * logit_at(z, dtype, ld, t, v);
                 if (x > m) m = x;
             }
             ksum_t s = {0.0, 0.0};
             for (int64_t v = 0; v < V; ++v) {
-                e[v] = exp(logit_at(z, dtype, ld, t, v) - m);
+                e[v] = exp(inv_temp * logit_at(z, dtype, ld, t, v) - m);
                 ksum_add(&s, e[v]);
             }
             const double sum = ksum_value(&s);
@@ -86,15 +87,21 @@ void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int6
             ksum_t h = {0.0, 0.0};
             for (int64_t v = 0; v < V; ++v) {
                 const double p = e[v] / sum;
-                const double log_p = logit_at(z, dtype, ld, t, v) - log_norm;
+                const double log_p = inv_temp * logit_at(z, dtype, ld, t, v) - log_norm;
                 if (p > 0.0) ksum_add(&h, -p * log_p);
             }
             lse[t] = log_norm;
             H[t] = ksum_value(&h);
-            logp[t] = logit_at(z, dtype, ld, t, target[t]) - log_norm;
+            logp[t] = inv_temp * logit_at(z, dtype, ld, t, target[t]) - log_norm;
         }
         free(e);
     }
+}
+
+void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
+                        const int32_t* target, double* logp, double* H, double* lse,
+                        int nthreads) {
+    oracle_token_stats_ex(z, dtype, nrows, V, ld, target, 1.0, logp, H, lse, nthreads);
 }
 
 /* Sec. 4.3: the step entropy is the mean of the token entropies over the
@@ -138,47 +145,120 @@ int64_t oracle_step_mask(const float* Hs32, int64_t S, double rho, uint8_t* mask
     return k;
 }
 
-/* Eq. (2) without the KL term (R7), per token t of step s(t):
+/* KL estimators of D_KL(pi_theta || pi_ref) from the sampled token, with
+ * delta = log pi_ref - log pi_theta (the paper leaves the estimator unstated;
+ * k3 is the one GRPO uses): k1 = -delta, k2 = delta^2 / 2,
+ * k3 = exp(delta) - delta - 1, and their derivatives w.r.t. log pi_theta. */
+enum { KL_NONE = 0, KL_K1 = 1, KL_K2 = 2, KL_K3 = 3 };
+enum { AGG_TOKEN_MEAN = 0, AGG_TOKEN_MEAN_ALL = 1, AGG_STEP_MEAN = 2 };
+enum { RATIO_TOKEN = 0, RATIO_STEP_GEOMEAN = 1, RATIO_STEP_PRODUCT = 2 };
+
+static double kl_value(int kl, double delta) {
+    if (kl == KL_K1) return -delta;
+    if (kl == KL_K2) return 0.5 * delta * delta;
+    if (kl == KL_K3) return exp(delta) - delta - 1.0;
+    return 0.0;
+}
+
+static double kl_dlogp(int kl, double delta) {
+    if (kl == KL_K1) return 1.0;
+    if (kl == KL_K2) return -delta;
+    if (kl == KL_K3) return 1.0 - exp(delta);
+    return 0.0;
+}
+
+/* Eq. (2), per token t of step s(t), as the loss L = -J (R15):
  *   r  = pi_theta / pi_old            = exp(logp - lp_old)             (Eq. 1)
  *   w  = min(pi_old / pi_rollout, C)  = min(exp(lp_old - lp_roll), C)  (Sec. 4.4)
  *   u  = r A,  c = clip(r, 1 - eps_low, 1 + eps_high) A,  o = min(u, c)
- *   l_t = -M_s w o / N,   N = number of tokens in kept steps (R1: token mean)
- *   L  = sum_t l_t        (the loss is the negated objective)
- *   g_t = dL/dlogp_t = -(M_s w / N) * d o / d logp_t, and d o / d logp_t = r A
- *         when u <= c (the unclipped branch is the minimum), 0 when u > c (the
- *         clipped branch is a constant) (R6; w, M and N are constants, R5).
- * Per-token ratios, weights and clips (R2). If N == 0, L = 0 and g = 0 (R8).
- * boundary[t] = 1 marks tokens with |u - c| <= 1e-6 max(1, |A|), where the gate
- * of g may legitimately differ between precisions. stats: clip fraction, mean
- * TIS weight, fraction of weights at the cap, N (all over kept tokens; zeros
- * if N == 0). Returns L. */
-double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const float* lp_roll,
-                       const float* adv, const int32_t* off, int64_t S, const uint8_t* mask,
-                       double eps_low, double eps_high, double C, double* g, double* ell,
-                       uint8_t* boundary, double* stats) {
-    int64_t N = 0;
+ *   l_t = -M_s om_t (w o - beta kl_t)
+ *   L  = sum_t l_t
+ * om_t is the aggregation weight: 1/N with N the tokens of kept steps (R1,
+ * default), 1/T over all tokens, or 1/(K |s|) for the mean over the K kept
+ * steps of each step's token mean. With a step-level ratio (Eq. 1 written for
+ * the whole action) r, w and A are taken per step: log r_s and log w_s are the
+ * sum (product ratio) or mean (geometric-mean ratio) of the token log-ratios, A_s
+ * the mean advantage of the step, and every token of the step carries the
+ * step's w_s o_s.
+ *   g_t = dL/dlogp_t = -M (om_t w d o/dlogp_t - om_t beta dkl_t/dlogp_t), where
+ * d o / d logp_t = r A when u <= c (the unclipped branch is the minimum) and 0
+ * when u > c (the clipped branch is a constant) (R6); in step mode the step
+ * term differentiates through log r_s, whose derivative w.r.t. logp_t is 1
+ * (product) or 1/|s| (geometric mean), and the step's weights sum to
+ * Om_s = sum_{t in s} om_t. w, M, N, K are constants (R5). The KL term sits
+ * inside the indicator and outside the TIS weight, as in Eq. (2).
+ * boundary[t] = 1 marks tokens whose gate may legitimately differ between
+ * precisions (|u - c| <= 1e-6 max(1, |A|)). stats[6]: clip fraction, mean TIS
+ * weight, fraction of weights at the cap, N, mean KL, K (over kept tokens /
+ * steps; zeros when nothing is kept). Returns L. */
+double oracle_tis_loss_ex(int64_t T, const double* logp, const float* lp_old,
+                          const float* lp_roll, const float* lp_ref, const float* adv,
+                          const int32_t* off, int64_t S, const uint8_t* mask, double eps_low,
+                          double eps_high, double C, int kl, double beta, int agg, int ratio,
+                          double* g, double* ell, uint8_t* boundary, double* stats) {
+    int64_t N = 0, K = 0;
     for (int64_t s = 0; s < S; ++s)
-        if (mask[s]) N += off[s + 1] - off[s];
+        if (mask[s]) {
+            N += off[s + 1] - off[s];
+            K += 1;
+        }
     ksum_t L = {0.0, 0.0};
-    double n_clip = 0.0, sum_w = 0.0, n_cap = 0.0;
+    double n_clip = 0.0, sum_w = 0.0, n_cap = 0.0, sum_kl = 0.0;
     for (int64_t s = 0; s < S; ++s) {
+        const int64_t len = off[s + 1] - off[s];
+        const double M = mask[s] ? 1.0 : 0.0;
+        double om = 0.0;
+        if (agg == AGG_TOKEN_MEAN) om = N > 0 ? 1.0 / (double)N : 0.0;
+        if (agg == AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)T;
+        if (agg == AGG_STEP_MEAN) om = K > 0 ? 1.0 / ((double)K * (double)len) : 0.0;
+        /* step-level ratio, TIS weight and advantage */
+        double r_s = 0.0, w_s = 0.0, A_s = 0.0, ratio_tis_s = 0.0;
+        if (ratio != RATIO_TOKEN) {
+            double lr = 0.0, lw = 0.0, sa = 0.0;
+            for (int64_t t = off[s]; t < off[s + 1]; ++t) {
+                lr += logp[t] - (double)lp_old[t];
+                lw += (double)lp_old[t] - (double)lp_roll[t];
+                sa += (double)adv[t];
+            }
+            if (ratio == RATIO_STEP_GEOMEAN) {
+                lr /= (double)len;
+                lw /= (double)len;
+            }
+            r_s = exp(lr);
+            ratio_tis_s = exp(lw);
+            w_s = ratio_tis_s < C ? ratio_tis_s : C;
+            A_s = sa / (double)len;
+        }
         for (int64_t t = off[s]; t < off[s + 1]; ++t) {
-            const double M = mask[s] ? 1.0 : 0.0;
-            const double A = (double)adv[t];
-            const double r = exp(logp[t] - (double)lp_old[t]);
-            const double ratio_tis = exp((double)lp_old[t] - (double)lp_roll[t]);
-            const double w = ratio_tis < C ? ratio_tis : C;
+            double r, w, A, ratio_tis, dlog = 1.0, om_obj = om;
+            if (ratio == RATIO_TOKEN) {
+                A = (double)adv[t];
+                r = exp(logp[t] - (double)lp_old[t]);
+                ratio_tis = exp((double)lp_old[t] - (double)lp_roll[t]);
+                w = ratio_tis < C ? ratio_tis : C;
+            } else {
+                A = A_s;
+                r = r_s;
+                ratio_tis = ratio_tis_s;
+                w = w_s;
+                om_obj = om * (double)len; /* Om_s: the step term's weight */
+                dlog = ratio == RATIO_STEP_GEOMEAN ? 1.0 / (double)len : 1.0;
+            }
             double rc = r;
             if (rc < 1.0 - eps_low) rc = 1.0 - eps_low;
             if (rc > 1.0 + eps_high) rc = 1.0 + eps_high;
             const double u = r * A;
             const double c = rc * A;
             const double o = u < c ? u : c;
-            double lt = 0.0, gt = 0.0;
-            if (N > 0) {
-                lt = -M * w * o / (double)N;
-                gt = u <= c ? -M * w * A * r / (double)N : 0.0;
+            double klv = 0.0, kld = 0.0;
+            if (kl != KL_NONE) {
+                const double delta = (double)lp_ref[t] - logp[t];
+                klv = kl_value(kl, delta);
+                kld = kl_dlogp(kl, delta);
             }
+            const double lt = -M * om * (w * o - beta * klv);
+            const double d_obj = u <= c ? r * A * dlog : 0.0;
+            const double gt = -M * (om_obj * w * d_obj - om * beta * kld);
             if (ell) ell[t] = lt;
             if (g) g[t] = gt;
             if (boundary) boundary[t] = fabs(u - c) <= 1e-6 * fmax(1.0, fabs(A)) ? 1 : 0;
@@ -187,6 +267,7 @@ double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const
                 n_clip += u > c ? 1.0 : 0.0;
                 sum_w += w;
                 n_cap += ratio_tis >= C ? 1.0 : 0.0;
+                sum_kl += klv;
             }
         }
     }
@@ -195,24 +276,47 @@ double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const
         stats[1] = N > 0 ? sum_w / (double)N : 0.0;
         stats[2] = N > 0 ? n_cap / (double)N : 0.0;
         stats[3] = (double)N;
+        stats[4] = N > 0 ? sum_kl / (double)N : 0.0;
+        stats[5] = (double)K;
     }
     return ksum_value(&L);
 }
 
+/* The paper's default configuration: Eq. (2) without the KL term (R7),
+ * per-token ratios (R2), token mean over kept tokens (R1); stats[4]. */
+double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const float* lp_roll,
+                       const float* adv, const int32_t* off, int64_t S, const uint8_t* mask,
+                       double eps_low, double eps_high, double C, double* g, double* ell,
+                       uint8_t* boundary, double* stats) {
+    double st[6];
+    const double L = oracle_tis_loss_ex(T, logp, lp_old, lp_roll, NULL, adv, off, S, mask,
+                                        eps_low, eps_high, C, KL_NONE, 0.0, AGG_TOKEN_MEAN,
+                                        RATIO_TOKEN, g, ell, boundary, st);
+    if (stats)
+        for (int i = 0; i < 4; ++i) stats[i] = st[i];
+    return L;
+}
+
 /* Gradient of L w.r.t. the logits: dL/dz_{t,v} = g_t * d logp_t / d z_{t,v}
- * = g_t * (delta_{v, y_t} - p_{t,v}), with p = exp(z - lse) (softmax
- * derivative). Rows are the same rows as z (nrows of them); out is
- * [nrows, V] double. */
-void oracle_dlogits(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
-                    const int32_t* target, const double* lse, const double* g, double* out,
-                    int nthreads) {
+ * = inv_temp * g_t * (delta_{v, y_t} - p_{t,v}), with p = exp(inv_temp z - lse)
+ * (softmax derivative, and the chain rule through z -> inv_temp z). Rows are the
+ * same rows as z (nrows of them); out is [nrows, V] double. */
+void oracle_dlogits_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
+                       const int32_t* target, const double* lse, const double* g, double inv_temp,
+                       double* out, int nthreads) {
     if (nthreads < 1) nthreads = 1;
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
     for (int64_t t = 0; t < nrows; ++t) {
         for (int64_t v = 0; v < V; ++v) {
-            const double p = exp(logit_at(z, dtype, ld, t, v) - lse[t]);
+            const double p = exp(inv_temp * logit_at(z, dtype, ld, t, v) - lse[t]);
             const double delta = v == target[t] ? 1.0 : 0.0;
-            out[t * V + v] = g[t] * (delta - p);
+            out[t * V + v] = inv_temp * g[t] * (delta - p);
         }
     }
+}
+
+void oracle_dlogits(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
+                    const int32_t* target, const double* lse, const double* g, double* out,
+                    int nthreads) {
+    oracle_dlogits_ex(z, dtype, nrows, V, ld, target, lse, g, 1.0, out, nthreads);
 }

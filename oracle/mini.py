@@ -13,10 +13,12 @@ from __future__ import annotations
 import math
 
 
-def token_stats(rows, targets):
-    """Sec. 4.3: per row, log-prob of the target, entropy and log-normaliser."""
+def token_stats(rows, targets, inv_temp=1.0):
+    """Sec. 4.3: per row, log-prob of the target, entropy and log-normaliser of
+    softmax(inv_temp * z)."""
     out = []
-    for z, y in zip(rows, targets):
+    for z0, y in zip(rows, targets):
+        z = [inv_temp * x for x in z0]
         top = max(z)
         norm = top + math.log(math.fsum(math.exp(x - top) for x in z))
         probs = [math.exp(x - norm) for x in z]
@@ -74,12 +76,64 @@ def loss_and_coef(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C):
     return math.fsum(terms), coef
 
 
-def grad_rows(rows, targets, norms, coef):
-    """dL/dz_{t,v} = g_t (delta_{v,y} - p_v)."""
+def grad_rows(rows, targets, norms, coef, inv_temp=1.0):
+    """dL/dz_{t,v} = inv_temp g_t (delta_{v,y} - p_v)."""
     out = []
     for z, y, norm, gt in zip(rows, targets, norms, coef):
-        out.append([gt * ((1.0 if v == y else 0.0) - math.exp(x - norm)) for v, x in enumerate(z)])
+        out.append([inv_temp * gt * ((1.0 if v == y else 0.0) - math.exp(inv_temp * x - norm))
+                    for v, x in enumerate(z)])
     return out
+
+
+def _kl(kind, delta):
+    """(value, d value / d logp) of the KL estimator; delta = lp_ref - logp."""
+    if kind == "k1":
+        return -delta, 1.0
+    if kind == "k2":
+        return 0.5 * delta * delta, -delta
+    if kind == "k3":
+        return math.exp(delta) - delta - 1.0, 1.0 - math.exp(delta)
+    return 0.0, 0.0
+
+
+def loss_ex(logp, lp_old, lp_roll, lp_ref, adv, off, mask, eps_low, eps_high, C, kl="none",
+            beta=0.0, agg="token_mean", ratio="token"):
+    """Eq. (2) with the KL term, an aggregation weight per token and a token- or
+    step-level ratio; returns (L, g)."""
+    T = len(logp)
+    steps = [(off[s], off[s + 1]) for s in range(len(off) - 1)]
+    kept = [s for s in range(len(steps)) if mask[s]]
+    N = sum(steps[s][1] - steps[s][0] for s in kept)
+    K = len(kept)
+    terms, coef = [], [0.0] * T
+    for s in kept:
+        b, e = steps[s]
+        n = e - b
+        om = {"token_mean": 1.0 / N if N else 0.0, "token_mean_all": 1.0 / T,
+              "step_mean": 1.0 / (K * n) if K else 0.0}[agg]
+        if ratio == "token":
+            units = [([t], om, 1.0) for t in range(b, e)]
+        else:
+            units = [(list(range(b, e)), om * n, 1.0 / n if ratio == "step_geomean" else 1.0)]
+        for toks, weight, dlog in units:
+            lr = math.fsum(logp[t] - lp_old[t] for t in toks)
+            lw = math.fsum(lp_old[t] - lp_roll[t] for t in toks)
+            if ratio == "step_geomean":
+                lr, lw = lr / len(toks), lw / len(toks)
+            a = math.fsum(adv[t] for t in toks) / len(toks)
+            r, w = math.exp(lr), min(math.exp(lw), C)
+            clipped = min(max(r, 1.0 - eps_low), 1.0 + eps_high)
+            unclipped_term, clipped_term = r * a, clipped * a
+            terms.append(-weight * w * min(unclipped_term, clipped_term))
+            for t in toks:
+                if unclipped_term <= clipped_term:
+                    coef[t] -= weight * w * r * a * dlog
+        for t in range(b, e):
+            if kl != "none":
+                val, dval = _kl(kl, lp_ref[t] - logp[t])
+                terms.append(om * beta * val)
+                coef[t] += om * beta * dval
+    return math.fsum(terms), coef
 
 
 def forward_backward(rows, targets, lp_old, lp_roll, adv, off, rho, eps_low, eps_high, C):

@@ -28,18 +28,37 @@ MUTATIONS = {
     "ties_to_higher_index": ("Hs32[o] == Hs32[s] && o < s", "Hs32[o] == Hs32[s] && o > s"),
     "selection_keeps_lowest": ("Hs32[o] > Hs32[s] ||", "Hs32[o] < Hs32[s] ||"),
     "ratio_inverted": ("exp(logp[t] - (double)lp_old[t])", "exp((double)lp_old[t] - logp[t])"),
-    "tis_weight_dropped": ("const double w = ratio_tis < C ? ratio_tis : C;",
-                           "const double w = 1.0;"),
-    "tis_weight_uncapped": ("const double w = ratio_tis < C ? ratio_tis : C;",
-                            "const double w = ratio_tis;"),
+    "tis_weight_dropped": ("                w = ratio_tis < C ? ratio_tis : C;",
+                           "                w = 1.0;"),
+    "tis_weight_uncapped": ("                w = ratio_tis < C ? ratio_tis : C;",
+                            "                w = ratio_tis;"),
     "clip_bounds_swapped": ("if (rc < 1.0 - eps_low) rc = 1.0 - eps_low;",
                             "if (rc < 1.0 - eps_high) rc = 1.0 - eps_high;"),
-    "loss_sign": ("lt = -M * w * o / (double)N;", "lt = M * w * o / (double)N;"),
-    "gradient_through_clip": ("gt = u <= c ? -M * w * A * r / (double)N : 0.0;",
-                              "gt = -M * w * A * r / (double)N;"),
-    "mean_over_all_tokens": ("if (mask[s]) N += off[s + 1] - off[s];", "N += off[s + 1] - off[s];"),
-    "dlogits_wrong_sign_softmax": ("out[t * V + v] = g[t] * (delta - p);",
-                                   "out[t * V + v] = g[t] * (delta + p);"),
+    "loss_sign": ("const double lt = -M * om * (w * o - beta * klv);",
+                  "const double lt = M * om * (w * o - beta * klv);"),
+    "gradient_through_clip": ("const double d_obj = u <= c ? r * A * dlog : 0.0;",
+                              "const double d_obj = r * A * dlog;"),
+    "mean_over_all_tokens": ("        if (mask[s]) {\n            N += off[s + 1] - off[s];",
+                             "        if (1) {\n            N += off[s + 1] - off[s];"),
+    "dlogits_wrong_sign_softmax": ("out[t * V + v] = inv_temp * g[t] * (delta - p);",
+                                   "out[t * V + v] = inv_temp * g[t] * (delta + p);"),
+    "kl_k3_sign": ("return exp(delta) - delta - 1.0;", "return exp(delta) + delta - 1.0;"),
+    "kl_k3_derivative": ("if (kl == KL_K3) return 1.0 - exp(delta);",
+                         "if (kl == KL_K3) return exp(delta) - 1.0;"),
+    "kl_inside_tis_weight": ("const double lt = -M * om * (w * o - beta * klv);",
+                             "const double lt = -M * om * w * (o - beta * klv);"),
+    "step_mean_weight": ("om = K > 0 ? 1.0 / ((double)K * (double)len) : 0.0;",
+                         "om = K > 0 ? 1.0 / (double)K : 0.0;"),
+    "token_mean_all_weight": ("if (agg == AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)T;",
+                              "if (agg == AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)N;"),
+    "geomean_derivative": ("dlog = ratio == RATIO_STEP_GEOMEAN ? 1.0 / (double)len : 1.0;",
+                           "dlog = 1.0;"),
+    "step_ratio_product_vs_mean": ("            if (ratio == RATIO_STEP_GEOMEAN) {\n                lr /= (double)len;",
+                                   "            if (ratio == RATIO_STEP_PRODUCT) {\n                lr /= (double)len;"),
+    "temperature_not_in_gradient": ("out[t * V + v] = inv_temp * g[t] * (delta - p);",
+                                    "out[t * V + v] = g[t] * (delta - p);"),
+    "temperature_not_in_logp": ("logp[t] = inv_temp * logit_at(z, dtype, ld, t, target[t]) - log_norm;",
+                                "logp[t] = logit_at(z, dtype, ld, t, target[t]) - log_norm;"),
     "dlogits_wrong_target": ("const double delta = v == target[t] ? 1.0 : 0.0;",
                              "const double delta = v == (target[t] + 1) % V ? 1.0 : 0.0;"),
 }
@@ -57,6 +76,7 @@ def test_planted_mistake_is_caught(name, tmp_path):
     env = dict(os.environ, ORACLE_LIB=str(lib))
     proc = subprocess.run(
         [sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-         os.path.join(ROOT, "tests", "test_oracle_pins.py"), "-k", "not mini"],
+         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+         os.path.join(ROOT, "tests", "test_oracle_ext_pins.py"), "-k", "not mini"],
         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert proc.returncode != 0, f"mutation {name} survived the pins:\n{proc.stdout[-2000:]}"
