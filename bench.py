@@ -87,7 +87,8 @@ def cpu_baseline(wl, threads):
     chunk = 256
     for r0 in range(0, wl.T, chunk):
         r1 = min(wl.T, r0 + chunk)
-        oracle.dlogits(z[r0:r1], wl.target[r0:r1], lse[r0:r1], res["g"][r0:r1], nthreads=threads)
+        oracle.dlogits(z[r0:r1], wl.target[r0:r1], lse[r0:r1], logp[r0:r1], res["g"][r0:r1],
+                       nthreads=threads)
     dt = time.perf_counter() - t0
     return {"value": wl.T * wl.V / dt, "unit": "logit elements/s", "cores": threads,
             "kind": "oracle", "seconds": round(dt, 3),

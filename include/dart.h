@@ -142,6 +142,82 @@ dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, i
                             const float* lse, const float* tok_coef, void* dlogits,
                             int64_t ld_out, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Objective variants and options (same two passes over the logits)
+ * ------------------------------------------------------------------------ */
+
+/* KL estimator of D_KL(pi_theta || pi_ref) (the -beta D_KL term of Eq. (1) and
+ * Eq. (2); beta = 0.1 in Appendix A.4; the paper does not state the estimator).
+ * With delta = logp_ref - logp on the sampled token: K1 = -delta,
+ * K2 = delta^2 / 2, K3 = exp(delta) - delta - 1 (the GRPO estimator). */
+typedef enum { DART_KL_NONE = 0, DART_KL_K1 = 1, DART_KL_K2 = 2, DART_KL_K3 = 3 } dart_kl_t;
+
+/* Aggregation weight om_t of a kept token: TOKEN_MEAN = 1/N (N tokens in kept
+ * steps; the default), TOKEN_MEAN_ALL = 1/T, STEP_MEAN = 1/(K |s|) (mean over
+ * the K kept steps of each step's token mean). */
+typedef enum {
+    DART_AGG_TOKEN_MEAN = 0,
+    DART_AGG_TOKEN_MEAN_ALL = 1,
+    DART_AGG_STEP_MEAN = 2
+} dart_agg_t;
+
+/* Importance ratio level: per token (default), or per step (Eq. (1) is written
+ * for the whole action) as the geometric mean or the product of the step's
+ * token ratios; the TIS weight and the advantage are then taken per step too
+ * (the same mean or sum of token log-ratios; the mean advantage of the step). */
+typedef enum {
+    DART_RATIO_TOKEN = 0,
+    DART_RATIO_STEP_GEOMEAN = 1,
+    DART_RATIO_STEP_PRODUCT = 2
+} dart_ratio_t;
+
+/* Loss configuration (host memory, read during the call). */
+typedef struct {
+    float eps_low, eps_high; /* clip bounds, >= 0 */
+    float C;                 /* TIS cap, > 0, may be +INFINITY */
+    int32_t kl;              /* dart_kl_t */
+    float beta;              /* KL coefficient, >= 0 (ignored for DART_KL_NONE) */
+    int32_t aggregation;     /* dart_agg_t */
+    int32_t ratio;           /* dart_ratio_t */
+} dart_loss_config_t;
+
+/* Gradient flag: a row whose coefficient is exactly 0 (dropped step, clipped
+ * token, zero advantage) is written as zeros without reading its logits. The
+ * result is the same (+0 in place of -0); HBM traffic drops by the share of
+ * such rows. */
+#define DART_GRAD_SKIP_ZERO_ROWS 1u
+
+/* dart_tok_stats for softmax(inv_temp * z): inv_temp is an inverse sampling
+ * temperature (1 in the paper, Appendix A.4); finite and > 0. */
+dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                                int64_t ld, const int32_t* target, float inv_temp, float* logp,
+                                float* entropy, float* lse, hipStream_t stream);
+
+/* The loss of Eq. (2) including its KL term, under the configuration above:
+ *   loss = -sum_t M om_t (w o - beta kl_t),  o = min(r A, clip(r) A)
+ *   tok_coef[t] = dloss/dlogp_t
+ * (the KL term sits inside the step indicator and outside the TIS weight, as in
+ * Eq. (2)). logp_ref: [T] float32 reference-policy log-probs of the targets,
+ * required when config->kl != DART_KL_NONE, else ignored (may be NULL).
+ * stats: [6] float32 or NULL: clip fraction, mean TIS weight, fraction at the
+ * cap, N, mean KL, K (over kept tokens / steps). Other arguments and errors as
+ * dart_tis_loss_fwd; also INVALID_ARG for a null config, an unknown enum value,
+ * or beta < 0 / non-finite. */
+dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* logp_old,
+                                   const float* logp_rollout, const float* logp_ref,
+                                   const float* adv, const int32_t* step_offsets, int64_t S,
+                                   const uint8_t* step_mask, const dart_loss_config_t* config,
+                                   double* loss, float* tok_coef, float* stats,
+                                   hipStream_t stream);
+
+/* dart_tis_grad at inverse temperature inv_temp (the same value given to
+ * dart_tok_stats_ex): dlogits = inv_temp * tok_coef * (onehot - softmax(inv_temp z)).
+ * flags: 0 or DART_GRAD_SKIP_ZERO_ROWS; other bits are INVALID_ARG. */
+dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                               int64_t ld, const int32_t* target, const float* logp,
+                               const float* lse, const float* tok_coef, float inv_temp,
+                               uint32_t flags, void* dlogits, int64_t ld_out, hipStream_t stream);
+
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
  * number of steps dart_step_select keeps (the guard absorbs the representation
  * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside

@@ -60,8 +60,8 @@ def _load():
                                            ctypes.c_int, _D, ctypes.c_int, ctypes.c_int, _P, _P,
                                            _P, _P]
         lib.oracle_dlogits_ex.restype = None
-        lib.oracle_dlogits_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _D, _P,
-                                          ctypes.c_int]
+        lib.oracle_dlogits_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _D,
+                                          _P, ctypes.c_int]
         lib.oracle_token_stats.restype = None
         lib.oracle_token_stats.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
                                            ctypes.c_int]
@@ -75,7 +75,7 @@ def _load():
         lib.oracle_tis_loss.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, _D, _D, _D, _P, _P,
                                         _P, _P]
         lib.oracle_dlogits.restype = None
-        lib.oracle_dlogits.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
+        lib.oracle_dlogits.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P,
                                        ctypes.c_int]
         _lib = lib
     return _lib
@@ -212,22 +212,26 @@ def tis_loss_ex(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C, lp_
     return dict(L=float(L), g=g, ell=ell, boundary=boundary.astype(bool), stats=stats)
 
 
-def dlogits(z, target, lse, g, nthreads=None, inv_temp=1.0):
-    """float64 [n, V] gradient rows for logits rows ``z``."""
+def dlogits(z, target, lse, logp, g, nthreads=None, inv_temp=1.0):
+    """float64 [n, V] gradient rows for logits rows ``z`` (``lse`` and ``logp``
+    of the same rows from token_stats)."""
     lib = _load()
     z, dt = _logits_arg(z)
     n, V = z.shape
     ld = z.strides[0] // z.itemsize
     target = _c(target, np.int32)
     lse = _c(lse, np.float64)
+    logp = _c(logp, np.float64)
     g = _c(g, np.float64)
+    assert lse.shape == (n,) and logp.shape == (n,) and g.shape == (n,)
     out = np.empty((n, V), np.float64)
     if inv_temp == 1.0:
         lib.oracle_dlogits(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
-                           g.ctypes.data, out.ctypes.data, nthreads or default_threads())
+                           logp.ctypes.data, g.ctypes.data, out.ctypes.data,
+                           nthreads or default_threads())
     else:
         lib.oracle_dlogits_ex(z.ctypes.data, dt, n, V, ld, target.ctypes.data, lse.ctypes.data,
-                              g.ctypes.data, float(inv_temp), out.ctypes.data,
+                              logp.ctypes.data, g.ctypes.data, float(inv_temp), out.ctypes.data,
                               nthreads or default_threads())
     return out
 
@@ -243,7 +247,7 @@ def forward_backward(z, target, lp_old, lp_roll, adv, off, rho, eps_low, eps_hig
     else:
         k = int(np.sum(mask))
     res = tis_loss(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C)
-    dz = dlogits(z, target, lse, res["g"], nthreads)
+    dz = dlogits(z, target, lse, logp, res["g"], nthreads)
     res.update(logp=logp, H=H, lse=lse, Hs=Hs, Hs32=Hs32, mask=mask, k=k, dz=dz)
     return res
 

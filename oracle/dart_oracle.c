@@ -61,7 +61,7 @@ static double logit_at(const void* z, int dtype, int64_t ld, int64_t t, int64_t 
  * The logits are first multiplied by inv_temp (an inverse sampling temperature;
  * 1 in the paper, App. A.4). Per row: (1) the maximum m; (2) e_v = exp(z_v - m)
  * and their sum s, so that lse = m + log s; (3) p_v = e_v / s and
- * log p_v = z_v - lse, summed into the entropy from its definition. A term with
+ * log p_v = (z_v - m) - log s, summed into the entropy from its definition. A term with
  * p_v == 0 contributes 0 (R9: -inf logits allowed, 0 log 0 := 0). */
 void oracle_token_stats_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
                            const int32_t* target, double inv_temp, double* logp, double* H,
@@ -83,16 +83,20 @@ void oracle_token_stats_ex(const void* z, int dtype, int64_t nrows, int64_t V, i
                 ksum_add(&s, e[v]);
             }
             const double sum = ksum_value(&s);
-            const double log_norm = m + log(sum);
+            /* log s without rounding s: the largest term is exp(0) = 1, so
+             * s - 1 = (sum - 1) + compensation is exact to the compensation's
+             * accuracy and log s = log1p(s - 1) keeps full relative accuracy
+             * even when s - 1 ~ 1e-11 (a near-one-hot row) */
+            const double log_s = log1p((s.sum - 1.0) + s.comp);
             ksum_t h = {0.0, 0.0};
             for (int64_t v = 0; v < V; ++v) {
                 const double p = e[v] / sum;
-                const double log_p = inv_temp * logit_at(z, dtype, ld, t, v) - log_norm;
+                const double log_p = (inv_temp * logit_at(z, dtype, ld, t, v) - m) - log_s;
                 if (p > 0.0) ksum_add(&h, -p * log_p);
             }
-            lse[t] = log_norm;
+            lse[t] = m + log_s;
             H[t] = ksum_value(&h);
-            logp[t] = inv_temp * logit_at(z, dtype, ld, t, target[t]) - log_norm;
+            logp[t] = (inv_temp * logit_at(z, dtype, ld, t, target[t]) - m) - log_s;
         }
         free(e);
     }
@@ -188,7 +192,8 @@ static double kl_dlogp(int kl, double delta) {
  * Om_s = sum_{t in s} om_t. w, M, N, K are constants (R5). The KL term sits
  * inside the indicator and outside the TIS weight, as in Eq. (2).
  * boundary[t] = 1 marks tokens whose gate may legitimately differ between
- * precisions (|u - c| <= 1e-6 max(1, |A|)). stats[6]: clip fraction, mean TIS
+ * precisions: A != 0 and the ratio within 1e-4 (relative) of a clip bound.
+ * stats[6]: clip fraction, mean TIS
  * weight, fraction of weights at the cap, N, mean KL, K (over kept tokens /
  * steps; zeros when nothing is kept). Returns L. */
 double oracle_tis_loss_ex(int64_t T, const double* logp, const float* lp_old,
@@ -261,7 +266,13 @@ double oracle_tis_loss_ex(int64_t T, const double* logp, const float* lp_old,
             const double gt = -M * (om_obj * w * d_obj - om * beta * kld);
             if (ell) ell[t] = lt;
             if (g) g[t] = gt;
-            if (boundary) boundary[t] = fabs(u - c) <= 1e-6 * fmax(1.0, fabs(A)) ? 1 : 0;
+            /* R6: the gate u <= c can flip between precisions only when the ratio sits
+             * at a clip bound (inside the range clip(r) = r and u == c exactly) */
+            if (boundary)
+                boundary[t] = A != 0.0 && (fabs(r - (1.0 - eps_low)) <= 1e-4 * (1.0 - eps_low) ||
+                                           fabs(r - (1.0 + eps_high)) <= 1e-4 * (1.0 + eps_high))
+                                  ? 1
+                                  : 0;
             ksum_add(&L, lt);
             if (mask[s]) {
                 n_clip += u > c ? 1.0 : 0.0;
@@ -302,8 +313,8 @@ double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const
  * (softmax derivative, and the chain rule through z -> inv_temp z). Rows are the
  * same rows as z (nrows of them); out is [nrows, V] double. */
 void oracle_dlogits_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
-                       const int32_t* target, const double* lse, const double* g, double inv_temp,
-                       double* out, int nthreads) {
+                       const int32_t* target, const double* lse, const double* logp,
+                       const double* g, double inv_temp, double* out, int nthreads) {
     if (nthreads < 1) nthreads = 1;
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
     for (int64_t t = 0; t < nrows; ++t) {
@@ -312,11 +323,16 @@ void oracle_dlogits_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64
             const double delta = v == target[t] ? 1.0 : 0.0;
             out[t * V + v] = inv_temp * g[t] * (delta - p);
         }
+        /* at the target 1 - p_y = -expm1(log p_y): exact where p_y -> 1, where
+         * 1 - exp(z_y - lse) would keep only the digits lse has below its
+         * integer part */
+        const int64_t y = target[t];
+        out[t * V + y] = inv_temp * g[t] * -expm1(logp[t]);
     }
 }
 
 void oracle_dlogits(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
-                    const int32_t* target, const double* lse, const double* g, double* out,
-                    int nthreads) {
-    oracle_dlogits_ex(z, dtype, nrows, V, ld, target, lse, g, 1.0, out, nthreads);
+                    const int32_t* target, const double* lse, const double* logp, const double* g,
+                    double* out, int nthreads) {
+    oracle_dlogits_ex(z, dtype, nrows, V, ld, target, lse, logp, g, 1.0, out, nthreads);
 }

@@ -6,8 +6,10 @@ be built (``__graft_entry__.build()``); if it is missing, importing a function
 raises — there is no CPU fallback.
 
 Functions carry the C names: ``dart_tok_stats``, ``dart_step_select``,
-``dart_tis_loss_fwd_bwd``, ``dart_kept_steps``, ``dart_status_string``.
-``policy_update`` chains the three device calls.
+``dart_tis_loss_fwd_bwd`` (and its halves ``dart_tis_loss_fwd`` /
+``dart_tis_grad``), the ``_ex`` variants (inverse temperature, the KL term,
+aggregation and ratio level, zero-row skipping), ``dart_kept_steps`` and
+``dart_status_string``. ``policy_update`` chains the device calls.
 """
 
 from __future__ import annotations
@@ -25,8 +27,22 @@ DART_ERR_HIP = 3
 DART_F32 = 0
 DART_BF16 = 1
 
+DART_KL = {"none": 0, "k1": 1, "k2": 2, "k3": 3}
+DART_AGG = {"token_mean": 0, "token_mean_all": 1, "step_mean": 2}
+DART_RATIO = {"token": 0, "step_geomean": 1, "step_product": 2}
+DART_GRAD_SKIP_ZERO_ROWS = 1
+
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
-            "dart_tis_grad", "dart_kept_steps", "dart_status_string")
+            "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
+            "dart_kept_steps", "dart_status_string")
+
+
+class dart_loss_config_t(ctypes.Structure):
+    """Mirror of the C struct dart_loss_config_t."""
+
+    _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float), ("C", ctypes.c_float),
+                ("kl", ctypes.c_int32), ("beta", ctypes.c_float), ("aggregation", ctypes.c_int32),
+                ("ratio", ctypes.c_int32)]
 
 
 class DartError(RuntimeError):
@@ -61,6 +77,15 @@ def load_library():
         lib.dart_tis_grad.restype = ctypes.c_int
         lib.dart_tis_grad.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P,
                                       _I64, _P]
+        lib.dart_tok_stats_ex.restype = ctypes.c_int
+        lib.dart_tok_stats_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, ctypes.c_float,
+                                          _P, _P, _P, _P]
+        lib.dart_tis_loss_fwd_ex.restype = ctypes.c_int
+        lib.dart_tis_loss_fwd_ex.argtypes = [_I64, _P, _P, _P, _P, _P, _P, _I64, _P,
+                                             ctypes.POINTER(dart_loss_config_t), _P, _P, _P, _P]
+        lib.dart_tis_grad_ex.restype = ctypes.c_int
+        lib.dart_tis_grad_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
+                                         ctypes.c_float, ctypes.c_uint32, _P, _I64, _P]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
         lib.dart_status_string.restype = ctypes.c_char_p
@@ -117,8 +142,9 @@ def _logits_meta(logits):
     return dt, logits.shape[0], logits.shape[1], logits.stride(0)
 
 
-def dart_tok_stats(logits, target, logp=None, entropy=None, lse=None, stream=None):
-    """Per-token log-prob of the target, entropy and log-normaliser (float32 [T] each)."""
+def dart_tok_stats(logits, target, logp=None, entropy=None, lse=None, stream=None, inv_temp=1.0):
+    """Per-token log-prob of the target, entropy and log-normaliser (float32 [T]
+    each) of softmax(inv_temp * logits)."""
     torch = _torch()
     dt, T, V, ld = _logits_meta(logits)
     dev = logits.device
@@ -128,11 +154,19 @@ def dart_tok_stats(logits, target, logp=None, entropy=None, lse=None, stream=Non
     lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
     for n, v in (("logp", logp), ("entropy", entropy), ("lse", lse)):
         _check_vec(n, v, torch.float32, T, dev)
-    rc = load_library().dart_tok_stats(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
-                                       logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
-                                       _stream_handle(stream))
+    if inv_temp == 1.0:
+        rc = load_library().dart_tok_stats(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
+                                           logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
+                                           _stream_handle(stream))
+        name = "dart_tok_stats"
+    else:
+        rc = load_library().dart_tok_stats_ex(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
+                                              float(inv_temp), logp.data_ptr(),
+                                              entropy.data_ptr(), lse.data_ptr(),
+                                              _stream_handle(stream))
+        name = "dart_tok_stats_ex"
     if rc != DART_OK:
-        raise DartError("dart_tok_stats", rc)
+        raise DartError(name, rc)
     return logp, entropy, lse
 
 
@@ -231,8 +265,48 @@ def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask
     return loss, tok_coef, stats
 
 
-def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None):
-    """dlogits = tok_coef * (onehot(target) - softmax(logits)), dtype of logits."""
+def dart_tis_loss_fwd_ex(logp, logp_old, logp_rollout, adv, step_offsets, step_mask, eps_low,
+                         eps_high, C, logp_ref=None, kl="none", beta=0.0, aggregation="token_mean",
+                         ratio="token", loss=None, tok_coef=None, stats=None, with_stats=True,
+                         stream=None):
+    """The loss with the KL term, aggregation and ratio level selectable.
+    Returns (loss float64 [1], tok_coef float32 [T], stats float32 [6])."""
+    torch = _torch()
+    dev = logp.device
+    T = logp.numel()
+    S = step_offsets.numel() - 1
+    for n, v in (("logp", logp), ("logp_old", logp_old), ("logp_rollout", logp_rollout),
+                 ("adv", adv)):
+        _check_vec(n, v, torch.float32, T, dev)
+    if DART_KL[kl] != 0:
+        _check_vec("logp_ref", logp_ref, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev) if loss is None else loss
+    tok_coef = torch.empty(T, dtype=torch.float32, device=dev) if tok_coef is None else tok_coef
+    if stats is None and with_stats:
+        stats = torch.empty(6, dtype=torch.float32, device=dev)
+    _check_vec("loss", loss, torch.float64, 1, dev)
+    _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
+    if stats is not None:
+        _check_vec("stats", stats, torch.float32, 6, dev)
+    cfg = dart_loss_config_t(float(eps_low), float(eps_high), float(C), DART_KL[kl], float(beta),
+                             DART_AGG[aggregation], DART_RATIO[ratio])
+    rc = load_library().dart_tis_loss_fwd_ex(
+        T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(),
+        None if DART_KL[kl] == 0 else logp_ref.data_ptr(), adv.data_ptr(),
+        step_offsets.data_ptr(), S, step_mask.data_ptr(), ctypes.byref(cfg), loss.data_ptr(),
+        tok_coef.data_ptr(), _ptr(stats), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_tis_loss_fwd_ex", rc)
+    return loss, tok_coef, stats
+
+
+def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None, inv_temp=1.0,
+                  skip_zero_rows=False):
+    """dlogits = inv_temp * tok_coef * (onehot(target) - softmax(inv_temp * logits)),
+    dtype of logits; ``skip_zero_rows`` writes rows with a zero coefficient
+    without reading them."""
     torch = _torch()
     dt, T, V, ld = _logits_meta(logits)
     dev = logits.device
@@ -244,11 +318,20 @@ def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None
     if (dlogits.dtype != logits.dtype or dlogits.dim() != 2 or tuple(dlogits.shape) != (T, V)
             or dlogits.stride(1) != 1 or dlogits.device != dev):
         raise ValueError("dlogits must match logits in dtype and shape, with contiguous rows")
-    rc = load_library().dart_tis_grad(
-        logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
-        tok_coef.data_ptr(), dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+    if inv_temp == 1.0 and not skip_zero_rows:
+        rc = load_library().dart_tis_grad(
+            logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
+            tok_coef.data_ptr(), dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+        name = "dart_tis_grad"
+    else:
+        rc = load_library().dart_tis_grad_ex(
+            logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
+            tok_coef.data_ptr(), float(inv_temp),
+            DART_GRAD_SKIP_ZERO_ROWS if skip_zero_rows else 0, dlogits.data_ptr(),
+            dlogits.stride(0), _stream_handle(stream))
+        name = "dart_tis_grad_ex"
     if rc != DART_OK:
-        raise DartError("dart_tis_grad", rc)
+        raise DartError(name, rc)
     return dlogits
 
 

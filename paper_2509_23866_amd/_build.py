@@ -12,7 +12,7 @@ LIB = os.path.join(HERE, "libdart.so")
 INCLUDE = os.path.join(ROOT, "include")
 
 HIPCC_FLAGS = [
-    "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-shared",
+    "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-shared", "-Werror=shadow",
     # packed-FP32 VALU forms stay disabled: plain scalar fp32 code only
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

@@ -124,11 +124,15 @@ __device__ __forceinline__ Triple triple_empty() { return Triple{-INFINITY, 0.f,
 // every element costs one FMA, one clamp, one exp2, one add and one FMA. The
 // clamp keeps 2^x * x finite for -inf logits (2^-256 is 0 in fp32, so no finite
 // value moves).
+// The logits enter scaled by k = inv_temp * log2(e) (inv_temp > 0); m is kept
+// in units of inv_temp * z.
 template <int N>
-__device__ __forceinline__ void triple_add_exact(Triple& a, const float* z) {
+__device__ __forceinline__ void triple_add_exact(Triple& a, const float* z, float inv_temp,
+                                                 float k) {
     float cm = z[0];
 #pragma unroll
     for (int i = 1; i < N; ++i) cm = fmaxf(cm, z[i]);
+    cm *= inv_temp;
     if (cm > a.m) {
         if (a.s > 0.f) {
             const float d = (a.m - cm) * kLog2e;
@@ -143,7 +147,7 @@ __device__ __forceinline__ void triple_add_exact(Triple& a, const float* z) {
     float s = 0.f, w = 0.f;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        const float x = fmaxf(fmaf(z[i], kLog2e, -mb), -256.f);
+        const float x = fmaxf(fmaf(z[i], k, -mb), -256.f);
         const float e = __builtin_amdgcn_exp2f(x);
         s += e;
         w = fmaf(e, x, w);
@@ -161,14 +165,14 @@ __device__ __forceinline__ void triple_add_exact(Triple& a, const float* z) {
 // element this costs one FMA, one exp2, one add and one FMA: the per-element
 // maximum and clamp leave the hot loop.
 template <int N>
-__device__ __forceinline__ void triple_add(Triple& a, const float* z) {
-    if (a.m == -INFINITY) a.m = z[0];
+__device__ __forceinline__ void triple_add(Triple& a, const float* z, float inv_temp, float k) {
+    if (a.m == -INFINITY) a.m = z[0] * inv_temp;
     if (a.m != -INFINITY) {
         const float mb = a.m * kLog2e;
         float s = 0.f, w = 0.f;
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            const float x = fmaf(z[i], kLog2e, -mb);
+            const float x = fmaf(z[i], k, -mb);
             const float e = __builtin_amdgcn_exp2f(x);
             s += e;
             w = fmaf(e, x, w);
@@ -179,7 +183,7 @@ __device__ __forceinline__ void triple_add(Triple& a, const float* z) {
             return;
         }
     }
-    triple_add_exact<N>(a, z);
+    triple_add_exact<N>(a, z, inv_temp, k);
 }
 
 __device__ __forceinline__ Triple triple_merge(const Triple a, const Triple b) {
@@ -309,7 +313,7 @@ __device__ __forceinline__ void stream_iterations(const u32x4* vrow, int64_t nfu
 template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL>
 __global__ void __launch_bounds__(THREADS)
 tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
-                 const int32_t* __restrict__ target, float* __restrict__ logp,
+                 const int32_t* __restrict__ target, float inv_temp, float* __restrict__ logp,
                  float* __restrict__ entropy, float* __restrict__ lse) {
     using E = typename Elt<D>::T;
     constexpr int EPV = Elt<D>::kPerVec;
@@ -332,6 +336,7 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
     const int64_t it_y = vy >= 0 ? vy / PER_IT : -1;
     const int64_t nfull = L.nvec / PER_IT;
 
+    const float k = inv_temp * kLog2e;
     Triple acc = triple_empty();
     stream_iterations<THREADS, UNROLL, PIPE, NTL>(vrow, nfull, tid, [&](const u32x4* v, int64_t it) {
         float z[UNROLL * EPV];
@@ -346,7 +351,7 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
                     if (col == y) z[u * EPV + e] = -INFINITY;
                 }
         }
-        triple_add<UNROLL * EPV>(acc, z);
+        triple_add<UNROLL * EPV>(acc, z, inv_temp, k);
     });
     for (int64_t j = nfull * PER_IT + tid; j < L.nvec; j += THREADS) {
         float z[EPV];
@@ -356,13 +361,13 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
             for (int e = 0; e < EPV; ++e)
                 if (L.head + j * EPV + e == y) z[e] = -INFINITY;
         }
-        triple_add<EPV>(acc, z);
+        triple_add<EPV>(acc, z, inv_temp, k);
     }
     const int64_t nscalar = L.head + (V - L.body_end);
-    for (int64_t k = tid; k < nscalar; k += THREADS) {
-        const int64_t col = k < L.head ? k : L.body_end + (k - L.head);
+    for (int64_t q = tid; q < nscalar; q += THREADS) {
+        const int64_t col = q < L.head ? q : L.body_end + (q - L.head);
         float z1[1] = {col == y ? -INFINITY : load_one<D>(row, col)};
-        triple_add<1>(acc, z1);
+        triple_add<1>(acc, z1, inv_temp, k);
     }
 
     acc = triple_wave_reduce(acc);
@@ -375,7 +380,7 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
     for (int i = 1; i < THREADS / 64; ++i) x = triple_merge(x, partial[i]);
 
     // add the target element
-    const float zy = y_ok ? load_one<D>(row, y) : __builtin_nanf("");
+    const float zy = y_ok ? load_one<D>(row, y) * inv_temp : __builtin_nanf("");
     const float M = fmaxf(x.m, zy);
     float sx = 0.f, wx = 0.f;
     if (x.s > 0.f) {
@@ -536,85 +541,184 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
 constexpr int kCoefThreads = 1024;
 constexpr int kCoefWaves = kCoefThreads / 64;
 
+struct LossConfig {
+    float eps_low, eps_high, C, log_C;
+    int kl, agg, ratio;
+    float beta;
+};
+
+// KL estimators of D_KL(pi_theta || pi_ref) from the sampled token, with
+// delta = log pi_ref - log pi_theta: k1 = -delta, k2 = delta^2 / 2,
+// k3 = exp(delta) - delta - 1 (GRPO's), and their derivatives w.r.t.
+// log pi_theta. In double: k3 cancels to O(delta^2) for small delta.
+__device__ __forceinline__ void kl_terms(int kl, double delta, double& value, double& dlogp) {
+    value = 0.0;
+    dlogp = 0.0;
+    if (kl == DART_KL_K1) {
+        value = -delta;
+        dlogp = 1.0;
+    } else if (kl == DART_KL_K2) {
+        value = 0.5 * delta * delta;
+        dlogp = -delta;
+    } else if (kl == DART_KL_K3) {
+        const double e = exp(delta);
+        value = e - delta - 1.0;
+        dlogp = 1.0 - e;
+    }
+}
+
+// One wave per step, lanes over the step's tokens. Per token t of step s:
+//   loss term  l_t = -M om_t (w o - beta kl_t),  o = min(r A, clip(r) A)
+//   coefficient g_t = dL/dlogp_t = -M (Om w [u <= c] r A dlog - om_t beta dkl_t)
+// with om_t the aggregation weight (1/N, 1/T or 1/(K |s|)). Token ratios use
+// r = exp(logp - lp_old) and w = min(exp(lp_old - lp_roll), C) per token
+// (Om = om_t, dlog = 1); step ratios use the sum (product) or mean (geometric
+// mean) of the token log-ratios of the step and its mean advantage, shared by
+// all its tokens (Om = om |s|, dlog = 1 or 1/|s|). The loss and the counters
+// are summed per lane in token order, then in a fixed butterfly and wave order.
+// GENERAL = false compiles the paper's default configuration only (no KL term,
+// token ratios, token mean over kept tokens).
+template <bool GENERAL>
 __global__ void __launch_bounds__(kCoefThreads)
 tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
-                const float* __restrict__ lp_roll, const float* __restrict__ adv,
-                const int32_t* __restrict__ off, int64_t S, const uint8_t* __restrict__ mask,
-                float eps_low, float eps_high, float C, float log_C, float* __restrict__ coef,
-                double* __restrict__ loss, float* __restrict__ stats) {
-    __shared__ int64_t red_i[kCoefWaves];
-    __shared__ double red_d[4][kCoefWaves];
+                const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
+                const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
+                const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
+                double* __restrict__ loss, float* __restrict__ stats, int nstats) {
+    __shared__ int64_t red_i[2][kCoefWaves];
+    __shared__ double red_d[5][kCoefWaves];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
 
-    int64_t n_local = 0;
+    int64_t n_local = 0, k_local = 0;
     for (int64_t s = tid; s < S; s += kCoefThreads) {
         int64_t b, e;
         step_bounds(off, s, T, b, e);
-        if (mask[s]) n_local += e - b;
+        if (mask[s]) {
+            n_local += e - b;
+            k_local += 1;
+        }
     }
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) n_local += __shfl_xor(n_local, o);
-    if (lane == 0) red_i[wave] = n_local;
+    for (int o = 32; o >= 1; o >>= 1) {
+        n_local += __shfl_xor(n_local, o);
+        k_local += __shfl_xor(k_local, o);
+    }
+    if (lane == 0) {
+        red_i[0][wave] = n_local;
+        red_i[1][wave] = k_local;
+    }
     __syncthreads();
-    int64_t N = 0;
-    for (int i = 0; i < kCoefWaves; ++i) N += red_i[i];
+    int64_t N = 0, K = 0;
+    for (int i = 0; i < kCoefWaves; ++i) {
+        N += red_i[0][i];
+        K += red_i[1][i];
+    }
 
     const double inv_n = N > 0 ? 1.0 / (double)N : 0.0;
-    const float lo = 1.f - eps_low, hi = 1.f + eps_high;
-    double l_acc = 0.0, w_acc = 0.0, n_clip = 0.0, n_cap = 0.0;
+    const float lo = 1.f - cfg.eps_low, hi = 1.f + cfg.eps_high;
+    const bool step_ratio = GENERAL && cfg.ratio != DART_RATIO_TOKEN;
+    const bool with_kl = GENERAL && cfg.kl != DART_KL_NONE;
+    const double beta = (double)cfg.beta;
+    double l_acc = 0.0, w_acc = 0.0, n_clip = 0.0, n_cap = 0.0, kl_acc = 0.0;
     for (int64_t s = wave; s < S; s += kCoefWaves) {
         int64_t b, e;
         step_bounds(off, s, T, b, e);
+        const int64_t len = e - b;
         const bool kept = mask[s] != 0 && N > 0;
-        for (int64_t t = b + lane; t < e; t += 64) {
-            if (!kept) {
-                coef[t] = 0.f;
-                continue;
+        if (!kept) {
+            for (int64_t t = b + lane; t < e; t += 64) coef[t] = 0.f;
+            continue;
+        }
+        double om = inv_n;
+        if (GENERAL && cfg.agg == DART_AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)T;
+        if (GENERAL && cfg.agg == DART_AGG_STEP_MEAN) om = 1.0 / ((double)K * (double)len);
+
+        double r_s = 0.0, w_s = 0.0, A_s = 0.0, dlog = 1.0, om_obj = om;
+        bool cap_s = false;
+        if (step_ratio) {
+            double slr = 0.0, slw = 0.0, sa = 0.0;
+            for (int64_t t = b + lane; t < e; t += 64) {
+                slr += (double)logp[t] - (double)lp_old[t];
+                slw += (double)lp_old[t] - (double)lp_roll[t];
+                sa += (double)adv[t];
             }
-            const float A = adv[t];
-            const float r = expf(logp[t] - lp_old[t]);
-            const float d = lp_old[t] - lp_roll[t];
-            const bool capped = d >= log_C;
-            const float w = capped ? C : fminf(expf(d), C);
-            const float rc = fminf(fmaxf(r, lo), hi);
-            const float u = r * A;
-            const float c = rc * A;
-            const bool gate = u <= c;
-            l_acc -= (double)w * (double)fminf(u, c) * inv_n;
-            coef[t] = gate ? (float)(-(double)w * (double)A * (double)r * inv_n) : 0.f;
-            w_acc += (double)w;
+            slr = wave_sum(slr);
+            slw = wave_sum(slw);
+            sa = wave_sum(sa);
+            if (cfg.ratio == DART_RATIO_STEP_GEOMEAN) {
+                slr /= (double)len;
+                slw /= (double)len;
+                dlog = 1.0 / (double)len;
+            }
+            r_s = exp(slr);
+            cap_s = slw >= (double)cfg.log_C;
+            w_s = cap_s ? (double)cfg.C : fmin(exp(slw), (double)cfg.C);
+            A_s = sa / (double)len;
+            om_obj = om * (double)len;
+        }
+
+        for (int64_t t = b + lane; t < e; t += 64) {
+            double obj, dobj, w;
+            bool gate, capped;
+            if (!step_ratio) {
+                const float A = adv[t];
+                const float r = expf(logp[t] - lp_old[t]);
+                const float d = lp_old[t] - lp_roll[t];
+                capped = d >= cfg.log_C;
+                const float wf = capped ? cfg.C : fminf(expf(d), cfg.C);
+                const float rc = fminf(fmaxf(r, lo), hi);
+                const float u = r * A;
+                const float c = rc * A;
+                gate = u <= c;
+                w = (double)wf;
+                obj = w * (double)fminf(u, c);
+                dobj = gate ? w * (double)A * (double)r : 0.0;
+            } else {
+                const double rc = fmin(fmax(r_s, (double)lo), (double)hi);
+                const double u = r_s * A_s;
+                const double c = rc * A_s;
+                gate = u <= c;
+                capped = cap_s;
+                w = w_s;
+                obj = w * fmin(u, c);
+                dobj = gate ? w * r_s * A_s * dlog : 0.0;
+            }
+            double klv = 0.0, kld = 0.0;
+            if (with_kl) kl_terms(cfg.kl, (double)lp_ref[t] - (double)logp[t], klv, kld);
+            l_acc -= om * (obj - beta * klv);
+            coef[t] = (float)(-(om_obj * dobj - om * beta * kld));
+            w_acc += w;
             n_clip += gate ? 0.0 : 1.0;
             n_cap += capped ? 1.0 : 0.0;
+            kl_acc += klv;
         }
     }
     l_acc = wave_sum(l_acc);
     w_acc = wave_sum(w_acc);
     n_clip = wave_sum(n_clip);
     n_cap = wave_sum(n_cap);
+    kl_acc = wave_sum(kl_acc);
     if (lane == 0) {
         red_d[0][wave] = l_acc;
         red_d[1][wave] = w_acc;
         red_d[2][wave] = n_clip;
         red_d[3][wave] = n_cap;
+        red_d[4][wave] = kl_acc;
     }
     __syncthreads();
     if (tid == 0) {
-        double L = 0.0, W = 0.0, NC = 0.0, NK = 0.0;
-        for (int i = 0; i < kCoefWaves; ++i) {
-            L += red_d[0][i];
-            W += red_d[1][i];
-            NC += red_d[2][i];
-            NK += red_d[3][i];
-        }
-        loss[0] = L;
+        double acc[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+        for (int i = 0; i < kCoefWaves; ++i)
+            for (int j = 0; j < 5; ++j) acc[j] += red_d[j][i];
+        loss[0] = acc[0];
         if (stats) {
-            stats[0] = (float)(NC * inv_n);
-            stats[1] = (float)(W * inv_n);
-            stats[2] = (float)(NK * inv_n);
-            stats[3] = (float)N;
+            const float out[6] = {(float)(acc[2] * inv_n), (float)(acc[1] * inv_n),
+                                  (float)(acc[3] * inv_n), (float)N, (float)(acc[4] * inv_n),
+                                  (float)K};
+            for (int j = 0; j < nstats; ++j) stats[j] = out[j];
         }
     }
 }
@@ -627,7 +731,8 @@ template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS
 __global__ void __launch_bounds__(THREADS)
 tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __restrict__ target,
                 const float* __restrict__ lse, const float* __restrict__ logp,
-                const float* __restrict__ coef, void* dlogits, int64_t ld_out) {
+                const float* __restrict__ coef, float inv_temp, uint32_t flags, void* dlogits,
+                int64_t ld_out) {
     // logits and dlogits may be the same buffer (in place): every element is
     // read and then written by the same lane, and a lane only reads elements
     // it has not yet written.
@@ -641,8 +746,10 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
     E* orow = static_cast<E*>(dlogits) + t * ld_out;
     const int64_t y_in = target[t];
     const int64_t y = (y_in >= 0 && y_in < V) ? y_in : -1;
-    const float g = coef[t];
+    // d/dz of a softmax at inverse temperature it: it * g * (onehot - p)
+    const float g = coef[t] * inv_temp;
     const float neg_g = -g;
+    const float k = inv_temp * kLog2e;
     const float lb = lse[t] * kLog2e;
     // 1 - p_y = -expm1(logp_y), accurate when p_y -> 1
     const float dy = g * -expm1f(logp[t]);
@@ -650,6 +757,17 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
     RowLayout L = row_layout<D>(row, V);
     const RowLayout Lo = row_layout<D>(orow, V);
     if (L.head != Lo.head || !Lo.vector_ok) L = RowLayout{V, 0, V, false};
+
+    if ((flags & DART_GRAD_SKIP_ZERO_ROWS) && g == 0.f) {
+        // the row's gradient is exactly zero: write it without reading the logits
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        u32x4* vo = reinterpret_cast<u32x4*>(orow + L.head);
+        for (int64_t j = tid; j < L.nvec; j += THREADS) vstore<NTS>(zero, vo + j);
+        const int64_t ns = L.head + (V - L.body_end);
+        for (int64_t q = tid; q < ns; q += THREADS)
+            store_one<D>(orow, q < L.head ? q : L.body_end + (q - L.head), 0.f);
+        return;
+    }
     const u32x4* vrow = reinterpret_cast<const u32x4*>(row + L.head);
     u32x4* vout = reinterpret_cast<u32x4*>(orow + L.head);
     const int64_t vy = (y >= L.head && y < L.body_end) ? (y - L.head) / EPV : -1;
@@ -662,7 +780,7 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
         for (int u = 0; u < UNROLL; ++u) unpack<D>(v[u], z + u * EPV);
 #pragma unroll
         for (int i = 0; i < UNROLL * EPV; ++i)
-            z[i] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[i], kLog2e, -lb));
+            z[i] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[i], k, -lb));
         if (it == it_y) {
 #pragma unroll
             for (int u = 0; u < UNROLL; ++u)
@@ -681,16 +799,16 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
         unpack<D>(vload<NTL>(vrow + j), z);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) {
-            z[e] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[e], kLog2e, -lb));
+            z[e] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[e], k, -lb));
             if (L.head + j * EPV + e == y) z[e] = dy;
         }
         vstore<NTS>(pack<D>(z), vout + j);
     }
     const int64_t nscalar = L.head + (V - L.body_end);
-    for (int64_t k = tid; k < nscalar; k += THREADS) {
-        const int64_t col = k < L.head ? k : L.body_end + (k - L.head);
+    for (int64_t q = tid; q < nscalar; q += THREADS) {
+        const int64_t col = q < L.head ? q : L.body_end + (q - L.head);
         const float x = load_one<D>(row, col);
-        const float d = col == y ? dy : neg_g * __builtin_amdgcn_exp2f(fmaf(x, kLog2e, -lb));
+        const float d = col == y ? dy : neg_g * __builtin_amdgcn_exp2f(fmaf(x, k, -lb));
         store_one<D>(orow, col, d);
     }
 }
@@ -702,6 +820,18 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
 bool bad_dtype(dart_dtype_t d) { return d != DART_F32 && d != DART_BF16; }
 
 size_t elem_size(dart_dtype_t d) { return d == DART_F32 ? 4 : 2; }
+
+// dlogits may alias logits exactly (same base, same row stride); any other
+// overlap of the two [T, ld] row ranges is rejected.
+bool bad_overlap(const void* logits, int64_t ld, const void* dlogits, int64_t ld_out, int64_t T,
+                 int64_t V, size_t es) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits);
+    const uintptr_t a1 = a0 + (uintptr_t)(((T - 1) * ld + V) * (int64_t)es);
+    const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits);
+    const uintptr_t b1 = b0 + (uintptr_t)(((T - 1) * ld_out + V) * (int64_t)es);
+    const bool alias = a0 == b0 && ld == ld_out;
+    return !alias && a0 < b1 && b0 < a1;
+}
 
 dart_status_t launch_status() {
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
@@ -729,23 +859,30 @@ int64_t dart_kept_steps(int64_t S, double rho) {
     return (int64_t)k;
 }
 
-dart_status_t dart_tok_stats(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
-                             int64_t ld, const int32_t* target, float* logp, float* entropy,
-                             float* lse, hipStream_t stream) {
+dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                                int64_t ld, const int32_t* target, float inv_temp, float* logp,
+                                float* entropy, float* lse, hipStream_t stream) {
     if (!logits || !target || !logp || !entropy || !lse) return DART_ERR_INVALID_ARG;
     if (bad_dtype(dtype) || T < 1 || V < 1 || ld < V || T > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
+    if (!(inv_temp > 0.f) || isinf(inv_temp)) return DART_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(logits) % elem_size(dtype)) return DART_ERR_INVALID_ARG;
     const dim3 grid((unsigned)T), block(kStatsThreads);
     if (dtype == DART_BF16)
         hipLaunchKernelGGL(
             (tok_stats_kernel<DART_BF16, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
-            block, 0, stream, logits, V, ld, target, logp, entropy, lse);
+            block, 0, stream, logits, V, ld, target, inv_temp, logp, entropy, lse);
     else
         hipLaunchKernelGGL(
             (tok_stats_kernel<DART_F32, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
-            block, 0, stream, logits, V, ld, target, logp, entropy, lse);
+            block, 0, stream, logits, V, ld, target, inv_temp, logp, entropy, lse);
     return launch_status();
+}
+
+dart_status_t dart_tok_stats(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                             int64_t ld, const int32_t* target, float* logp, float* entropy,
+                             float* lse, hipStream_t stream) {
+    return dart_tok_stats_ex(logits, dtype, T, V, ld, target, 1.f, logp, entropy, lse, stream);
 }
 
 dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* step_offsets,
@@ -760,6 +897,40 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     return launch_status();
 }
 
+dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* logp_old,
+                                   const float* logp_rollout, const float* logp_ref,
+                                   const float* adv, const int32_t* step_offsets, int64_t S,
+                                   const uint8_t* step_mask, const dart_loss_config_t* config,
+                                   double* loss, float* tok_coef, float* stats,
+                                   hipStream_t stream) {
+    if (!config) return DART_ERR_INVALID_ARG;
+    const dart_loss_config_t& c = *config;
+    if (c.kl < DART_KL_NONE || c.kl > DART_KL_K3 || c.aggregation < DART_AGG_TOKEN_MEAN ||
+        c.aggregation > DART_AGG_STEP_MEAN || c.ratio < DART_RATIO_TOKEN ||
+        c.ratio > DART_RATIO_STEP_PRODUCT)
+        return DART_ERR_INVALID_ARG;
+    if (c.kl != DART_KL_NONE && (!logp_ref || !(c.beta >= 0.f) || isinf(c.beta)))
+        return DART_ERR_INVALID_ARG;
+    if (!logp || !logp_old || !logp_rollout || !adv || !step_offsets || !step_mask || !loss ||
+        !tok_coef)
+        return DART_ERR_INVALID_ARG;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
+    if (!(c.eps_low >= 0.f) || !(c.eps_high >= 0.f) || !(c.C > 0.f)) return DART_ERR_INVALID_ARG;
+    LossConfig cfg;
+    cfg.eps_low = c.eps_low;
+    cfg.eps_high = c.eps_high;
+    cfg.C = c.C;
+    cfg.log_C = isinf(c.C) ? INFINITY : (float)log((double)c.C);
+    cfg.kl = c.kl;
+    cfg.beta = c.kl == DART_KL_NONE ? 0.f : c.beta;
+    cfg.agg = c.aggregation;
+    cfg.ratio = c.ratio;
+    hipLaunchKernelGGL(tis_coef_kernel<true>, dim3(1), dim3(kCoefThreads), 0, stream, T, logp,
+                       logp_old, logp_rollout, c.kl == DART_KL_NONE ? nullptr : logp_ref, adv,
+                       step_offsets, S, step_mask, cfg, tok_coef, loss, stats, 6);
+    return launch_status();
+}
+
 dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_old,
                                 const float* logp_rollout, const float* adv,
                                 const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
@@ -770,10 +941,45 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
         return DART_ERR_INVALID_ARG;
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
-    const float log_C = isinf(C) ? INFINITY : (float)log((double)C);
-    hipLaunchKernelGGL(tis_coef_kernel, dim3(1), dim3(kCoefThreads), 0, stream, T, logp, logp_old,
-                       logp_rollout, adv, step_offsets, S, step_mask, eps_low, eps_high, C, log_C,
-                       tok_coef, loss, stats);
+    LossConfig cfg;
+    cfg.eps_low = eps_low;
+    cfg.eps_high = eps_high;
+    cfg.C = C;
+    cfg.log_C = isinf(C) ? INFINITY : (float)log((double)C);
+    cfg.kl = DART_KL_NONE;
+    cfg.beta = 0.f;
+    cfg.agg = DART_AGG_TOKEN_MEAN;
+    cfg.ratio = DART_RATIO_TOKEN;
+    hipLaunchKernelGGL(tis_coef_kernel<false>, dim3(1), dim3(kCoefThreads), 0, stream, T, logp,
+                       logp_old, logp_rollout, nullptr, adv, step_offsets, S, step_mask, cfg,
+                       tok_coef, loss, stats, 4);
+    return launch_status();
+}
+
+dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
+                               int64_t ld, const int32_t* target, const float* logp,
+                               const float* lse, const float* tok_coef, float inv_temp,
+                               uint32_t flags, void* dlogits, int64_t ld_out, hipStream_t stream) {
+    if (!logits || !target || !logp || !lse || !tok_coef || !dlogits) return DART_ERR_INVALID_ARG;
+    if (bad_dtype(dtype) || T < 1 || V < 1 || ld < V || ld_out < V || T > 0x7FFFFFFFll)
+        return DART_ERR_INVALID_ARG;
+    if (!(inv_temp > 0.f) || isinf(inv_temp) || (flags & ~DART_GRAD_SKIP_ZERO_ROWS))
+        return DART_ERR_INVALID_ARG;
+    const size_t es = elem_size(dtype);
+    if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
+        return DART_ERR_INVALID_ARG;
+    if (bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
+    const dim3 grid((unsigned)T), block(kGradThreads);
+    if (dtype == DART_BF16)
+        hipLaunchKernelGGL(
+            (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
+            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
+            dlogits, ld_out);
+    else
+        hipLaunchKernelGGL(
+            (tis_grad_kernel<DART_F32, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
+            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
+            dlogits, ld_out);
     return launch_status();
 }
 
@@ -781,29 +987,8 @@ dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, i
                             int64_t ld, const int32_t* target, const float* logp,
                             const float* lse, const float* tok_coef, void* dlogits,
                             int64_t ld_out, hipStream_t stream) {
-    if (!logits || !target || !logp || !lse || !tok_coef || !dlogits) return DART_ERR_INVALID_ARG;
-    if (bad_dtype(dtype) || T < 1 || V < 1 || ld < V || ld_out < V || T > 0x7FFFFFFFll)
-        return DART_ERR_INVALID_ARG;
-    const size_t es = elem_size(dtype);
-    if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
-        return DART_ERR_INVALID_ARG;
-    // in place is allowed only as an exact alias with the same row stride
-    const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits);
-    const uintptr_t a1 = a0 + (uintptr_t)(((T - 1) * ld + V) * (int64_t)es);
-    const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits);
-    const uintptr_t b1 = b0 + (uintptr_t)(((T - 1) * ld_out + V) * (int64_t)es);
-    const bool alias = a0 == b0 && ld == ld_out;
-    if (!alias && a0 < b1 && b0 < a1) return DART_ERR_INVALID_ARG;
-    const dim3 grid((unsigned)T), block(kGradThreads);
-    if (dtype == DART_BF16)
-        hipLaunchKernelGGL(
-            (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
-            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, dlogits, ld_out);
-    else
-        hipLaunchKernelGGL(
-            (tis_grad_kernel<DART_F32, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
-            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, dlogits, ld_out);
-    return launch_status();
+    return dart_tis_grad_ex(logits, dtype, T, V, ld, target, logp, lse, tok_coef, 1.f, 0u,
+                            dlogits, ld_out, stream);
 }
 
 dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
@@ -820,14 +1005,7 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
     const size_t es = elem_size(dtype);
     if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
         return DART_ERR_INVALID_ARG;
-    if (T >= 1) {
-        const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits);
-        const uintptr_t a1 = a0 + (uintptr_t)(((T - 1) * ld + V) * (int64_t)es);
-        const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits);
-        const uintptr_t b1 = b0 + (uintptr_t)(((T - 1) * ld_out + V) * (int64_t)es);
-        const bool alias = a0 == b0 && ld == ld_out;
-        if (!alias && a0 < b1 && b0 < a1) return DART_ERR_INVALID_ARG;
-    }
+    if (T >= 1 && bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
     dart_status_t st = dart_tis_loss_fwd(T, logp, logp_old, logp_rollout, adv, step_offsets, S,
                                          step_mask, eps_low, eps_high, C, loss, tok_coef, stats,
                                          stream);

@@ -25,6 +25,7 @@ from .gen import (  # noqa: F401
     draw_uniform,
     logits_rows_numpy,
     perturbed_logprobs,
+    reference_logprobs,
     bf16_bits_to_f32,
     f32_to_bf16_bits,
 )

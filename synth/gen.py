@@ -18,7 +18,8 @@ IEEE double arithmetic, so the same table on every machine); its tails end at
 +-4.3249.
 
 Streams: 0 logits, 1 target id, 2 target spike, 3 step lengths, 4 advantages,
-5 old-policy offset, 6 rollout-policy offset, 7 row type / one-hot column.
+5 old-policy offset, 6 rollout-policy offset, 7 row type / one-hot column,
+8 reference-policy offset.
 
 Logits
 ------
@@ -53,6 +54,7 @@ STREAM_ADV = 4
 STREAM_OLD = 5
 STREAM_ROLL = 6
 STREAM_ROWTYPE = 7
+STREAM_REF = 8
 
 KIND_GAUSS = 0
 KIND_FLAT = 1
@@ -144,6 +146,7 @@ class Workload:
     adv: np.ndarray  # float32 [T]
     old_offset: np.ndarray  # float64 [T]: lp_old = logp_new + old_offset
     roll_offset: np.ndarray  # float64 [T]: lp_roll = lp_old + roll_offset
+    ref_offset: np.ndarray = None  # float64 [T]: lp_ref = logp_new + ref_offset
     description: str = ""
     extra: dict = field(default_factory=dict)
 
@@ -235,6 +238,7 @@ def _build(name, *, seed, V, dtype, lens, rho, eps_low, eps_high, C, inplace, si
         target=target.astype(np.int32), adv=adv.astype(np.float32),
         old_offset=np.asarray(old_off, dtype=np.float64),
         roll_offset=np.asarray(roll_off, dtype=np.float64),
+        ref_offset=0.05 * draw_normal(seed, STREAM_REF, t, 0),
         description=description,
     )
 
@@ -383,6 +387,12 @@ def logits_rows_numpy(wl: Workload, rows) -> np.ndarray:
     if wl.dtype == "bf16":
         return f32_to_bf16_bits(out)
     return out
+
+
+def reference_logprobs(wl: Workload, logp_new: np.ndarray):
+    """Reference-policy log-probs of the targets, float32:
+    ``lp_ref = fl32(logp_new + ref_offset)`` (offsets 0.05 N(0,1))."""
+    return (np.asarray(logp_new, dtype=np.float64) + wl.ref_offset).astype(np.float32)
 
 
 def perturbed_logprobs(wl: Workload, logp_new: np.ndarray):

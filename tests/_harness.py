@@ -4,7 +4,8 @@ side, and the comparisons at the tolerances of the specification:
 * logp, entropy (and lse, step entropy): 2e-4 absolute;
 * loss: 1e-4 relative;
 * dlogits: at most 1 bfloat16 ulp of the oracle value (and 1e-2 absolute)
-  per element, rows of clip-boundary tokens excluded;
+  per element, rows of clip-boundary tokens (ratio within 1e-4 of a clip
+  bound, where the gate may legitimately differ) excluded;
 * step mask: exactly k kept; identical to the oracle wherever the oracle's step
   entropy is more than 1e-5 away from the k-th largest; a valid top-k of the
   GPU's own step entropies with ties towards the lower index everywhere.
@@ -77,7 +78,7 @@ class OracleSide:
         rows = np.asarray(rows, dtype=np.int64)
         z = sn.logits_rows_host(wl, rows)
         g = self.res["g"] if g is None else g
-        return oracle.dlogits(z, wl.target[rows], self.lse[rows], g[rows])
+        return oracle.dlogits(z, wl.target[rows], self.lse[rows], self.logp[rows], g[rows])
 
 
 # ---------------------------------------------------------------- GPU side
@@ -192,7 +193,8 @@ def check_loss(gpu, res, boundary):
     ok = ~boundary
     g, gg = res["g"][ok], gpu["g"][ok]
     err = np.abs(gg - g)
-    assert np.all(err <= 1e-4 * np.abs(g) + 1e-12), f"tok_coef max rel err {np.max(err / np.maximum(np.abs(g), 1e-30)):.3g}"
+    floor = 1e-6 * np.abs(res["g"]).max() + 1e-30
+    assert np.all(err <= 1e-4 * np.abs(g) + floor), f"tok_coef max rel err {np.max(err / np.maximum(np.abs(g), 1e-30)):.3g}"
     N = res["stats"][3]
     assert gpu["stats"][3] == N
     if N > 0:
@@ -223,8 +225,12 @@ def check_dz(gpu_dz, ref64, dtype, row_ok=None):
         return float((diff / ulp).max())
     scale = np.abs(ref64).max(axis=1, keepdims=True) + 1e-30
     err = np.abs(gpu_dz.astype(np.float64) - ref64)
-    assert np.all(err <= 1e-5 * scale), f"dlogits f32 max scaled err {(err / scale).max():.3g}"
-    return float((err / scale).max())
+    rel = err / scale
+    if not np.all(rel <= 1e-5):
+        i, j = np.unravel_index(np.argmax(rel), rel.shape)
+        raise AssertionError(f"dlogits f32 max scaled err {rel.max():.3g} at row {i} col {j}: "
+                             f"got {gpu_dz[i, j]!r} ref {ref64[i, j]!r} row scale {scale[i, 0]!r}")
+    return float(rel.max())
 
 
 def sample_rows(wl, res, n_random=48, seed=0):

@@ -123,3 +123,42 @@ def test_python_binding_requires_built_library(monkeypatch, tmp_path):
     monkeypatch.setattr(dart, "_lib", None)
     with pytest.raises(RuntimeError, match="not built"):
         dart.load_library()
+
+
+class _Cfg:
+    pass
+
+
+def _loss_ex_args(lib, **kw):
+    import paper_2509_23866_amd as d
+
+    cfg = d.dart_loss_config_t(0.2, 0.28, 2.0, kw.pop("kl", 0), kw.pop("beta", 0.0),
+                               kw.pop("aggregation", 0), kw.pop("ratio", 0))
+    a = dict(T=4, logp=P, lp_old=P, lp_roll=P, lp_ref=0, adv=P, off=P, S=2, mask=P, cfg=cfg,
+             loss=P, coef=P, stats=0)
+    a.update(kw)
+    cfgp = None if a["cfg"] is None else ctypes.byref(a["cfg"])
+    return [a["T"], a["logp"], a["lp_old"], a["lp_roll"], a["lp_ref"], a["adv"], a["off"], a["S"],
+            a["mask"], cfgp, a["loss"], a["coef"], a["stats"], None]
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(cfg=None), dict(kl=4), dict(kl=-1), dict(aggregation=3), dict(ratio=3),
+    dict(kl=3, lp_ref=0), dict(kl=1, lp_ref=P, beta=-0.1), dict(kl=1, lp_ref=P, beta=float("inf")),
+    dict(T=0), dict(S=5), dict(logp=0), dict(coef=0),
+])
+def test_tis_loss_fwd_ex_rejects(kw):
+    lib = dart.load_library()
+    assert lib.dart_tis_loss_fwd_ex(*_loss_ex_args(lib, **kw)) == dart.DART_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("inv_temp,flags", [(0.0, 0), (-1.0, 0), (float("inf"), 0),
+                                            (float("nan"), 0), (1.0, 2), (1.0, 0x80000000)])
+def test_ex_temperature_and_flags_rejected(inv_temp, flags):
+    lib = dart.load_library()
+    assert lib.dart_tok_stats_ex(P, 1, 4, 8, 8, P, inv_temp if flags == 0 else 0.0, P, P, P,
+                                 None) == dart.DART_ERR_INVALID_ARG
+    assert lib.dart_tis_grad_ex(P, 1, 4, 8, 8, P, P, P, P, inv_temp, flags, 1 << 20, 8,
+                                None) == dart.DART_ERR_INVALID_ARG

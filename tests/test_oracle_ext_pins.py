@@ -240,7 +240,7 @@ def test_variant_gradients_finite_differences(kl, agg, ratio, it):
     beta = 0.1
     res = oracle.tis_loss_ex(logp0, lp_old, lp_roll, A, off, mask, eps_low, eps_high, C,
                              lp_ref=ref, kl=kl, beta=beta, agg=agg, ratio=ratio)
-    dz = oracle.dlogits(z32, y, lse0, res["g"], inv_temp=it)
+    dz = oracle.dlogits(z32, y, lse0, logp0, res["g"], inv_temp=it)
     rows = z32.astype(np.float64).tolist()
 
     def L_of(rows_):

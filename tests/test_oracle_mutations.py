@@ -21,7 +21,10 @@ MUTATIONS = {
     "entropy_in_bits": ("ksum_add(&h, -p * log_p)", "ksum_add(&h, -p * log_p / log(2.0))"),
     "entropy_sign": ("ksum_add(&h, -p * log_p)", "ksum_add(&h, p * log_p)"),
     "probability_unnormalised": ("const double p = e[v] / sum;", "const double p = e[v];"),
-    "logp_vs_max_not_normaliser": ("target[t]) - log_norm;", "target[t]) - m;"),
+    "logp_vs_max_not_normaliser": ("logp[t] = (inv_temp * logit_at(z, dtype, ld, t, target[t]) - m) - log_s;",
+                                   "logp[t] = (inv_temp * logit_at(z, dtype, ld, t, target[t]) - m);"),
+    "target_gradient_sign": ("out[t * V + y] = inv_temp * g[t] * -expm1(logp[t]);",
+                             "out[t * V + y] = inv_temp * g[t] * expm1(logp[t]);"),
     "step_mean_wrong_denominator": ("/ (double)(off[s + 1] - off[s]);",
                                     "/ (double)(off[s + 1] - off[s] + 1);"),
     "kept_count_floor": ("ceil(rho * (double)S - 1e-6)", "floor(rho * (double)S)"),
@@ -57,8 +60,8 @@ MUTATIONS = {
                                    "            if (ratio == RATIO_STEP_PRODUCT) {\n                lr /= (double)len;"),
     "temperature_not_in_gradient": ("out[t * V + v] = inv_temp * g[t] * (delta - p);",
                                     "out[t * V + v] = g[t] * (delta - p);"),
-    "temperature_not_in_logp": ("logp[t] = inv_temp * logit_at(z, dtype, ld, t, target[t]) - log_norm;",
-                                "logp[t] = logit_at(z, dtype, ld, t, target[t]) - log_norm;"),
+    "temperature_not_in_logp": ("logp[t] = (inv_temp * logit_at(z, dtype, ld, t, target[t]) - m) - log_s;",
+                                "logp[t] = (logit_at(z, dtype, ld, t, target[t]) - m) - log_s;"),
     "dlogits_wrong_target": ("const double delta = v == target[t] ? 1.0 : 0.0;",
                              "const double delta = v == (target[t] + 1) % V ? 1.0 : 0.0;"),
 }

@@ -354,9 +354,9 @@ def test_dlogits_rows_sum_to_zero():
     rng = np.random.default_rng(10)
     z = rng.normal(0, 3, (6, 1000)).astype(np.float32)
     y = rng.integers(0, 1000, 6).astype(np.int32)
-    _, _, lse = oracle.token_stats(z, y)
+    logp, _, lse = oracle.token_stats(z, y)
     g = rng.normal(0, 1e-3, 6)
-    dz = oracle.dlogits(z, y, lse, g)
+    dz = oracle.dlogits(z, y, lse, logp, g)
     assert np.all(np.abs(dz.sum(axis=1)) <= 1e-14 * np.abs(g) * 10)
     assert np.all(np.sign(dz[np.arange(6), y]) == np.sign(g))
 
@@ -387,7 +387,7 @@ def test_dlogits_finite_differences(seed):
     lp_old = (logp0 - np.log(r_target)).astype(np.float32)
     lp_roll = (lp_old + rng.normal(0, 0.5, T)).astype(np.float32)
     res = oracle.tis_loss(logp0, lp_old, lp_roll, A, off, mask, eps_low, eps_high, C)
-    dz = oracle.dlogits(z32, y, lse0, res["g"])
+    dz = oracle.dlogits(z32, y, lse0, logp0, res["g"])
 
     # finite differences in float64: evaluate the same definitions on float64
     # logits through the pure-Python oracle (the C oracle reads float32 storage)
@@ -453,3 +453,30 @@ def test_bf16_rounding_helper():
     assert bits[0] == 0x3F80 and bits[1] == 0x3F80 and bits[2] == 0x3F82
     assert np.array_equal(oracle.f64_to_bf16_bits(x[:5].astype(np.float32).astype(np.float64)),
                           f32_to_bf16_bits(x[:5].astype(np.float32)))
+
+
+def test_boundary_flag_marks_only_ratios_at_a_clip_bound():
+    """The gate of the gradient can differ between precisions only where the
+    ratio sits at a clip bound; ratios strictly inside or outside the range,
+    and zero advantages, are not excused from element-wise checks."""
+    r = np.array([1.0, 0.9, 1.1, 0.5, 1.9, 0.8 * (1 + 5e-5), 1.28 * (1 - 5e-5), 0.8, 1.28])
+    A = np.array([1.0, -1.0, 2.0, 1.0, -1.0, 1.0, -2.0, 0.0, 1.0], np.float32)
+    logp = np.log(r)
+    res = _one_step(logp, np.zeros(9, np.float32), np.zeros(9, np.float32), A, 0.2, 0.28, 2.0)
+    assert res["boundary"].tolist() == [False] * 5 + [True, True, False, True]
+
+
+@pytest.mark.parametrize("V,delta", [(777, 30.0), (151936, 30.0), (33, 20.0)])
+def test_near_one_hot_logp_and_gradient_relative_accuracy(V, delta):
+    """Spike at the target: log p_y = -log1p(a) and 1 - p_y = a / (1 + a),
+    a = (V-1) e^-delta, to 1e-10 *relative* accuracy (both are ~1e-11 here,
+    far below the resolution of lse ~ delta) - the gradient's row scale."""
+    z = np.zeros((1, V), np.float32)
+    z[0, 3] = delta
+    logp, H, lse = oracle.token_stats(z, [3])
+    a = (V - 1) * math.exp(-delta)
+    assert abs(logp[0] / -math.log1p(a) - 1) < 1e-10
+    g = np.array([0.25])
+    dz = oracle.dlogits(z, [3], lse, logp, g)
+    assert abs(dz[0, 3] / (0.25 * a / (1 + a)) - 1) < 1e-10
+    assert abs(dz[0, 0] / (-0.25 * math.exp(-delta) / (1 + a)) - 1) < 1e-12
