@@ -40,6 +40,8 @@ def parse_args():
                     choices=["tiny", "vlm7b", "microbatch", "longhorizon", "edge"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="0 = the process's CPU affinity (max 16)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the separately reported variants (profiling runs of the headline step)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed steps, run one plain device copy of this many MiB "
                          "(torch copy kernel) so that hardware counters can be scaled by it")
@@ -183,6 +185,35 @@ def main():
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
 
+    # separately reported variants (never the headline): the gradient pass with
+    # zero-coefficient rows written without reading them, and the statistics
+    # pass alone (the forward-only recompute of pi_old's log-probs)
+    variants = {}
+    if not wl.inplace and not args.no_variants:
+        zero_rows = float((coef == 0).float().mean().item())
+        ev_v = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            ev_v[i][0].record(stream)
+            dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream,
+                               skip_zero_rows=True)
+            ev_v[i][1].record(stream)
+        torch.cuda.synchronize(dev)
+        skip_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_v]))
+        variants["grad_skip_zero_rows"] = {
+            "zero_row_fraction": zero_rows, "grad_ms": skip_ms,
+            "hbm_bytes_per_launch": (1.0 - zero_rows) * T * V * esize + T * V * esize,
+            "achieved_GBps": ((1.0 - zero_rows) + 1.0) * T * V * esize / (skip_ms * 1e-3) / 1e9}
+    if not args.no_variants:
+        ev_s = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            ev_s[i][0].record(stream)
+            dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream)
+            ev_s[i][1].record(stream)
+        torch.cuda.synchronize(dev)
+        stats_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_s]))
+        variants["stats_only"] = {"ms": stats_ms, "logit_elements_per_s": T * V / (stats_ms * 1e-3),
+                                  "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
+
     step_ms = [e[0].elapsed_time(e[3]) for e in evs]
     k1_ms = [e[0].elapsed_time(e[1]) for e in evs]
     grad_ms = [e[2].elapsed_time(e[3]) for e in evs]
@@ -218,6 +249,7 @@ def main():
         "roofline": {"kernel": DOMINANT, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "algorithmic_bytes_per_launch": grad_bytes},
+        "variants": variants,
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
