@@ -218,6 +218,44 @@ dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T
                                const float* lse, const float* tok_coef, float inv_temp,
                                uint32_t flags, void* dlogits, int64_t ld_out, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Around the path: the advantage and several task groups per call
+ * ------------------------------------------------------------------------ */
+
+/* Step-wise GRPO advantage (Sec. 3.3). A task's step group D holds every step
+ * of its N trajectories, each step carrying its trajectory's reward R_i; over
+ * D, Rbar = mean(R) and sigma = the population standard deviation, and every
+ * token of every step of trajectory i gets A = (R_i - Rbar) / sigma (0 when
+ * sigma == 0, i.e. all rewards equal).
+ *   reward:              [n_traj] float32, one reward per trajectory.
+ *   traj_step_offsets:   [n_traj+1] int32, steps of trajectory i are
+ *                        [traj_step_offsets[i], traj_step_offsets[i+1]) (ends at S).
+ *   group_traj_offsets:  [G+1] int32, trajectories of group g are
+ *                        [group_traj_offsets[g], group_traj_offsets[g+1]) (ends at n_traj).
+ *   step_offsets:        [S+1] int32 token offsets of the steps (ends at T).
+ *   adv:                 [T] float32 output (the per-token advantage the loss takes).
+ *   group_mean, group_std: [G] float32 outputs or NULL.
+ * Offsets are preconditions (monotone, consistent ends); malformed ones give
+ * meaningless values but never an out-of-bounds access. Errors: INVALID_ARG for
+ * a null required pointer, n_traj < 1, G < 1 or G > n_traj, S < 1, S > T. */
+dart_status_t dart_grpo_advantage(const float* reward, int64_t n_traj,
+                                  const int32_t* traj_step_offsets,
+                                  const int32_t* group_traj_offsets, int64_t G,
+                                  const int32_t* step_offsets, int64_t S, int64_t T, float* adv,
+                                  float* group_mean, float* group_std, hipStream_t stream);
+
+/* dart_step_select for G task groups in one call (one workgroup per group):
+ * group g is steps [group_step_offsets[g], group_step_offsets[g+1]) and keeps
+ * dart_kept_steps(S_g, rho) of its own steps, by the same rule (the paper selects
+ * "within the group", Sec. 4.3). n_kept_steps: [G] int32 or NULL. Errors as
+ * dart_step_select; also INVALID_ARG for a null group_step_offsets, G < 1 or
+ * G > S. */
+dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
+                                     const int32_t* step_offsets, int64_t S,
+                                     const int32_t* group_step_offsets, int64_t G, double rho,
+                                     float* step_entropy, uint8_t* step_mask,
+                                     int32_t* n_kept_steps, hipStream_t stream);
+
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
  * number of steps dart_step_select keeps (the guard absorbs the representation
  * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside

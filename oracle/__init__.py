@@ -62,6 +62,8 @@ def _load():
         lib.oracle_dlogits_ex.restype = None
         lib.oracle_dlogits_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _D,
                                           _P, ctypes.c_int]
+        lib.oracle_grpo_advantage.restype = None
+        lib.oracle_grpo_advantage.argtypes = [_P, _P, _I64, _P, _I64, _P, _P, _P, _P]
         lib.oracle_token_stats.restype = None
         lib.oracle_token_stats.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
                                            ctypes.c_int]
@@ -250,6 +252,40 @@ def forward_backward(z, target, lp_old, lp_roll, adv, off, rho, eps_low, eps_hig
     dz = dlogits(z, target, lse, logp, res["g"], nthreads)
     res.update(logp=logp, H=H, lse=lse, Hs=Hs, Hs32=Hs32, mask=mask, k=k, dz=dz)
     return res
+
+
+def grpo_advantage(reward, traj_off, grp_off, off):
+    """Step-wise GRPO advantage per token (Sec. 3.3); returns (adv [T] float64,
+    group_mean [G], group_std [G])."""
+    lib = _load()
+    reward = _c(reward, np.float32)
+    traj_off = _c(traj_off, np.int32)
+    grp_off = _c(grp_off, np.int32)
+    off = _c(off, np.int32)
+    n_traj, G = reward.size, grp_off.size - 1
+    assert traj_off.size == n_traj + 1 and grp_off[-1] == n_traj
+    assert traj_off[-1] == off.size - 1
+    T = int(off[-1])
+    adv = np.zeros(T, np.float64)
+    mean = np.empty(G, np.float64)
+    std = np.empty(G, np.float64)
+    lib.oracle_grpo_advantage(reward.ctypes.data, traj_off.ctypes.data, n_traj, grp_off.ctypes.data,
+                              G, off.ctypes.data, adv.ctypes.data, mean.ctypes.data, std.ctypes.data)
+    return adv, mean, std
+
+
+def step_mask_groups(Hs32, group_step_off, rho):
+    """Top-k selection within each group of steps [group_step_off[g],
+    group_step_off[g+1]) (Sec. 4.3 applied per task group): (mask, k per group)."""
+    Hs32 = np.asarray(Hs32, np.float32)
+    mask = np.zeros(Hs32.size, np.uint8)
+    ks = []
+    for g in range(len(group_step_off) - 1):
+        a, b = int(group_step_off[g]), int(group_step_off[g + 1])
+        m, k = step_mask(Hs32[a:b], rho)
+        mask[a:b] = m
+        ks.append(k)
+    return mask, np.array(ks, np.int64)
 
 
 def f64_to_bf16_bits(x):

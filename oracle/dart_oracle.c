@@ -336,3 +336,43 @@ void oracle_dlogits(const void* z, int dtype, int64_t nrows, int64_t V, int64_t 
                     double* out, int nthreads) {
     oracle_dlogits_ex(z, dtype, nrows, V, ld, target, lse, logp, g, 1.0, out, nthreads);
 }
+
+/* Sec. 3.3, step-wise GRPO advantage. The step group D of a task holds every
+ * step of its N trajectories, each step carrying its trajectory's reward R_i.
+ * Over D: Rbar = (1/|D|) sum R, sigma^2 = (1/|D|) sum (R - Rbar)^2 (population
+ * variance, as written), and every step (i, j) gets A = (R_i - Rbar) / sigma;
+ * every token of the step carries it. R8-like guard: sigma == 0 (all rewards
+ * equal; the data manager excludes such groups) gives A = 0.
+ * Layout: trajectories [grp_off[g], grp_off[g+1]) form group g; steps
+ * [traj_off[i], traj_off[i+1]) form trajectory i; tokens [off[s], off[s+1])
+ * form step s. adv is [T]; group_mean / group_std are [G] (or NULL). */
+void oracle_grpo_advantage(const float* reward, const int32_t* traj_off, int64_t n_traj,
+                           const int32_t* grp_off, int64_t G, const int32_t* off, double* adv,
+                           double* group_mean, double* group_std) {
+    (void)n_traj;
+    for (int64_t g = 0; g < G; ++g) {
+        /* walk the steps of the group: D as a list of rewards */
+        ksum_t sum = {0.0, 0.0};
+        int64_t count = 0;
+        for (int64_t i = grp_off[g]; i < grp_off[g + 1]; ++i)
+            for (int64_t s = traj_off[i]; s < traj_off[i + 1]; ++s) {
+                ksum_add(&sum, (double)reward[i]);
+                ++count;
+            }
+        const double mean = count > 0 ? ksum_value(&sum) / (double)count : 0.0;
+        ksum_t sq = {0.0, 0.0};
+        for (int64_t i = grp_off[g]; i < grp_off[g + 1]; ++i)
+            for (int64_t s = traj_off[i]; s < traj_off[i + 1]; ++s) {
+                const double d = (double)reward[i] - mean;
+                ksum_add(&sq, d * d);
+            }
+        const double sd = count > 0 ? sqrt(ksum_value(&sq) / (double)count) : 0.0;
+        if (group_mean) group_mean[g] = mean;
+        if (group_std) group_std[g] = sd;
+        for (int64_t i = grp_off[g]; i < grp_off[g + 1]; ++i) {
+            const double a = sd > 0.0 ? ((double)reward[i] - mean) / sd : 0.0;
+            for (int64_t s = traj_off[i]; s < traj_off[i + 1]; ++s)
+                for (int64_t t = off[s]; t < off[s + 1]; ++t) adv[t] = a;
+        }
+    }
+}

@@ -34,7 +34,8 @@ DART_GRAD_SKIP_ZERO_ROWS = 1
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
-            "dart_kept_steps", "dart_status_string")
+            "dart_grpo_advantage", "dart_step_select_groups", "dart_kept_steps",
+            "dart_status_string")
 
 
 class dart_loss_config_t(ctypes.Structure):
@@ -86,6 +87,11 @@ def load_library():
         lib.dart_tis_grad_ex.restype = ctypes.c_int
         lib.dart_tis_grad_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
                                          ctypes.c_float, ctypes.c_uint32, _P, _I64, _P]
+        lib.dart_grpo_advantage.restype = ctypes.c_int
+        lib.dart_grpo_advantage.argtypes = [_P, _I64, _P, _P, _I64, _P, _I64, _I64, _P, _P, _P, _P]
+        lib.dart_step_select_groups.restype = ctypes.c_int
+        lib.dart_step_select_groups.argtypes = [_P, _I64, _P, _I64, _P, _I64, ctypes.c_double, _P,
+                                                _P, _P, _P]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
         lib.dart_status_string.restype = ctypes.c_char_p
@@ -333,6 +339,56 @@ def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None
     if rc != DART_OK:
         raise DartError(name, rc)
     return dlogits
+
+
+def dart_grpo_advantage(reward, traj_step_offsets, group_traj_offsets, step_offsets, T=None,
+                        adv=None, group_mean=None, group_std=None, stream=None):
+    """Step-wise GRPO advantage per token (float32 [T]) and per-group mean/std."""
+    torch = _torch()
+    dev = reward.device
+    n_traj = reward.numel()
+    G = group_traj_offsets.numel() - 1
+    S = step_offsets.numel() - 1
+    _check_vec("reward", reward, torch.float32, n_traj, dev)
+    _check_vec("traj_step_offsets", traj_step_offsets, torch.int32, n_traj + 1, dev)
+    _check_vec("group_traj_offsets", group_traj_offsets, torch.int32, G + 1, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    if T is None:
+        T = int(step_offsets[-1].item())
+    adv = torch.empty(T, dtype=torch.float32, device=dev) if adv is None else adv
+    group_mean = torch.empty(G, dtype=torch.float32, device=dev) if group_mean is None else group_mean
+    group_std = torch.empty(G, dtype=torch.float32, device=dev) if group_std is None else group_std
+    _check_vec("adv", adv, torch.float32, T, dev)
+    rc = load_library().dart_grpo_advantage(
+        reward.data_ptr(), n_traj, traj_step_offsets.data_ptr(), group_traj_offsets.data_ptr(), G,
+        step_offsets.data_ptr(), S, T, adv.data_ptr(), _ptr(group_mean), _ptr(group_std),
+        _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_grpo_advantage", rc)
+    return adv, group_mean, group_std
+
+
+def dart_step_select_groups(entropy, step_offsets, group_step_offsets, rho, step_entropy=None,
+                            step_mask=None, n_kept_steps=None, stream=None):
+    """Per-step entropy, mask and kept count per group (top ceil(rho S_g) of each group)."""
+    torch = _torch()
+    dev = entropy.device
+    T = entropy.numel()
+    S = step_offsets.numel() - 1
+    G = group_step_offsets.numel() - 1
+    _check_vec("entropy", entropy, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    _check_vec("group_step_offsets", group_step_offsets, torch.int32, G + 1, dev)
+    step_entropy = torch.empty(S, dtype=torch.float32, device=dev) if step_entropy is None else step_entropy
+    step_mask = torch.empty(S, dtype=torch.uint8, device=dev) if step_mask is None else step_mask
+    n_kept_steps = torch.empty(G, dtype=torch.int32, device=dev) if n_kept_steps is None else n_kept_steps
+    rc = load_library().dart_step_select_groups(
+        entropy.data_ptr(), T, step_offsets.data_ptr(), S, group_step_offsets.data_ptr(), G,
+        float(rho), step_entropy.data_ptr(), step_mask.data_ptr(), n_kept_steps.data_ptr(),
+        _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_step_select_groups", rc)
+    return step_entropy, step_mask, n_kept_steps
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

@@ -428,9 +428,21 @@ __device__ __forceinline__ uint32_t float_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// k = clamp(ceil(rho * n - 1e-6), 0, n), with the two double operations
+// rounded separately (no contraction) so that it equals the host's count.
+__device__ __forceinline__ int64_t kept_steps_dev(int64_t n, double rho) {
+    double k = ceil(__dsub_rn(__dmul_rn(rho, (double)n), 1e-6));
+    k = fmin(fmax(k, 0.0), (double)n);
+    return (int64_t)k;
+}
+
+// One workgroup per group of steps: group g is steps [grp[g], grp[g+1]) (or all
+// S steps when grp is null, with k given); it keeps the ceil(rho S_g) steps of
+// highest mean entropy among its own.
 __global__ void __launch_bounds__(kSelThreads)
 step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
-                   int64_t S, int64_t k, float* __restrict__ step_H, uint8_t* __restrict__ mask,
+                   int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
+                   float* __restrict__ step_H, uint8_t* __restrict__ mask,
                    int32_t* __restrict__ n_kept) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sel_bin;
@@ -440,10 +452,17 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    int64_t gs = 0, ge = S, k = k_all;
+    if (grp) {
+        gs = min(max((int64_t)grp[blockIdx.x], (int64_t)0), S);
+        ge = min(max((int64_t)grp[blockIdx.x + 1], gs), S);
+        k = kept_steps_dev(ge - gs, rho);
+    }
+    const int64_t Sg = ge - gs;
 
     // step means: one wave per step, lanes stride the step's tokens, fixed
     // butterfly order (identical steps give identical means)
-    for (int64_t s = wave; s < S; s += kSelWaves) {
+    for (int64_t s = gs + wave; s < ge; s += kSelWaves) {
         int64_t b, e;
         step_bounds(off, s, T, b, e);
         double sum = 0.0;
@@ -453,9 +472,9 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     }
     __syncthreads();
 
-    if (k <= 0 || k >= S) {
-        for (int64_t s = tid; s < S; s += kSelThreads) mask[s] = k > 0 ? 1 : 0;
-        if (tid == 0 && n_kept) *n_kept = (int32_t)(k > 0 ? S : 0);
+    if (k <= 0 || k >= Sg) {
+        for (int64_t s = gs + tid; s < ge; s += kSelThreads) mask[s] = k > 0 ? 1 : 0;
+        if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)(k > 0 ? Sg : 0);
         return;
     }
 
@@ -465,7 +484,7 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     for (int shift = 24; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
         __syncthreads();
-        for (int64_t s = tid; s < S; s += kSelThreads) {
+        for (int64_t s = gs + tid; s < ge; s += kSelThreads) {
             const uint32_t key = float_key(step_H[s]);
             if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
         }
@@ -511,10 +530,10 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     // keep keys above the k-th; of the keys equal to it keep the first
     // `remaining` in step order (block scan over tiles of kSelThreads steps)
     int64_t carry = 0;
-    for (int64_t base = 0; base < S; base += kSelThreads) {
+    for (int64_t base = gs; base < ge; base += kSelThreads) {
         const int64_t s = base + tid;
-        const uint32_t key = s < S ? float_key(step_H[s]) : 0u;
-        const bool eq = s < S && key == prefix;
+        const uint32_t key = s < ge ? float_key(step_H[s]) : 0u;
+        const bool eq = s < ge && key == prefix;
         const uint64_t ballot = __ballot(eq);
         const int before = __popcll(ballot & ((1ull << lane) - 1ull));
         if (lane == 0) wave_count[wave] = __popcll(ballot);
@@ -524,14 +543,86 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
             if (i < wave) wave_before += wave_count[i];
             total += wave_count[i];
         }
-        if (s < S) {
+        if (s < ge) {
             const int64_t rank = carry + wave_before + before;
             mask[s] = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
         }
         carry += total;
         __syncthreads();
     }
-    if (tid == 0 && n_kept) *n_kept = (int32_t)k;
+    if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)k;
+}
+
+// ------------------------------------------------------------------------
+// step-wise GRPO advantage (Sec. 3.3)
+// ------------------------------------------------------------------------
+
+constexpr int kAdvThreads = 256;
+
+// One workgroup per group. Over the group's steps (each step counts its
+// trajectory's reward once): mean and population standard deviation, summed
+// per trajectory with weight = its step count, in fp64, in a fixed order; then
+// every token of trajectory i gets (R_i - mean) / sd (0 when sd == 0).
+__global__ void __launch_bounds__(kAdvThreads)
+grpo_advantage_kernel(const float* __restrict__ reward, const int32_t* __restrict__ traj_off,
+                      int64_t n_traj, const int32_t* __restrict__ grp_off,
+                      const int32_t* __restrict__ off, int64_t S, int64_t T,
+                      float* __restrict__ adv, float* __restrict__ group_mean,
+                      float* __restrict__ group_std) {
+    __shared__ double red[2][kAdvThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t i0 = min(max((int64_t)grp_off[blockIdx.x], (int64_t)0), n_traj);
+    const int64_t i1 = min(max((int64_t)grp_off[blockIdx.x + 1], i0), n_traj);
+    auto steps_of = [&](int64_t i, int64_t& a, int64_t& b) {
+        a = min(max((int64_t)traj_off[i], (int64_t)0), S);
+        b = min(max((int64_t)traj_off[i + 1], a), S);
+    };
+    auto block_sum2 = [&](double& x, double& y) {
+        x = wave_sum(x);
+        y = wave_sum(y);
+        if (lane == 0) {
+            red[0][wave] = x;
+            red[1][wave] = y;
+        }
+        __syncthreads();
+        x = 0.0;
+        y = 0.0;
+        for (int i = 0; i < kAdvThreads / 64; ++i) {
+            x += red[0][i];
+            y += red[1][i];
+        }
+        __syncthreads();
+    };
+    double cnt = 0.0, sum = 0.0;
+    for (int64_t i = i0 + tid; i < i1; i += kAdvThreads) {
+        int64_t a, b;
+        steps_of(i, a, b);
+        cnt += (double)(b - a);
+        sum += (double)(b - a) * (double)reward[i];
+    }
+    block_sum2(cnt, sum);
+    const double mean = cnt > 0.0 ? sum / cnt : 0.0;
+    double sq = 0.0, unused = 0.0;
+    for (int64_t i = i0 + tid; i < i1; i += kAdvThreads) {
+        int64_t a, b;
+        steps_of(i, a, b);
+        const double d = (double)reward[i] - mean;
+        sq += (double)(b - a) * d * d;
+    }
+    block_sum2(sq, unused);
+    const double sd = cnt > 0.0 ? sqrt(sq / cnt) : 0.0;
+    if (tid == 0) {
+        if (group_mean) group_mean[blockIdx.x] = (float)mean;
+        if (group_std) group_std[blockIdx.x] = (float)sd;
+    }
+    for (int64_t i = i0; i < i1; ++i) {
+        int64_t a, b;
+        steps_of(i, a, b);
+        const float A = sd > 0.0 ? (float)(((double)reward[i] - mean) / sd) : 0.f;
+        const int64_t t0 = min(max((int64_t)off[a], (int64_t)0), T);
+        const int64_t t1 = min(max((int64_t)off[b], t0), T);
+        for (int64_t t = t0 + tid; t < t1; t += kAdvThreads) adv[t] = A;
+    }
 }
 
 // ------------------------------------------------------------------------
@@ -893,7 +984,39 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     const int64_t k = dart_kept_steps(S, rho);
     if (k < 0) return DART_ERR_INVALID_ARG;
     hipLaunchKernelGGL(step_select_kernel, dim3(1), dim3(kSelThreads), 0, stream, entropy, T,
-                       step_offsets, S, k, step_entropy, step_mask, n_kept_steps);
+                       step_offsets, S, nullptr, rho, k, step_entropy, step_mask, n_kept_steps);
+    return launch_status();
+}
+
+dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
+                                     const int32_t* step_offsets, int64_t S,
+                                     const int32_t* group_step_offsets, int64_t G, double rho,
+                                     float* step_entropy, uint8_t* step_mask,
+                                     int32_t* n_kept_steps, hipStream_t stream) {
+    if (!entropy || !step_offsets || !group_step_offsets || !step_entropy || !step_mask)
+        return DART_ERR_INVALID_ARG;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll || G < 1 || G > S || G > 0x7FFFFFFFll)
+        return DART_ERR_INVALID_ARG;
+    if (dart_kept_steps(S, rho) < 0) return DART_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(step_select_kernel, dim3((unsigned)G), dim3(kSelThreads), 0, stream,
+                       entropy, T, step_offsets, S, group_step_offsets, rho, (int64_t)0,
+                       step_entropy, step_mask, n_kept_steps);
+    return launch_status();
+}
+
+dart_status_t dart_grpo_advantage(const float* reward, int64_t n_traj,
+                                  const int32_t* traj_step_offsets,
+                                  const int32_t* group_traj_offsets, int64_t G,
+                                  const int32_t* step_offsets, int64_t S, int64_t T, float* adv,
+                                  float* group_mean, float* group_std, hipStream_t stream) {
+    if (!reward || !traj_step_offsets || !group_traj_offsets || !step_offsets || !adv)
+        return DART_ERR_INVALID_ARG;
+    if (n_traj < 1 || G < 1 || G > n_traj || S < 1 || S > T || T > 0x7FFFFFFFll ||
+        G > 0x7FFFFFFFll)
+        return DART_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(grpo_advantage_kernel, dim3((unsigned)G), dim3(kAdvThreads), 0, stream,
+                       reward, traj_step_offsets, n_traj, group_traj_offsets, step_offsets, S, T,
+                       adv, group_mean, group_std);
     return launch_status();
 }
 

@@ -162,3 +162,25 @@ def test_ex_temperature_and_flags_rejected(inv_temp, flags):
                                  None) == dart.DART_ERR_INVALID_ARG
     assert lib.dart_tis_grad_ex(P, 1, 4, 8, 8, P, P, P, P, inv_temp, flags, 1 << 20, 8,
                                 None) == dart.DART_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [dict(reward=0), dict(traj=0), dict(grp=0), dict(off=0), dict(adv=0),
+                                dict(n_traj=0), dict(G=0), dict(G=5), dict(S=0), dict(S=11)])
+def test_grpo_advantage_rejects(kw):
+    lib = dart.load_library()
+    a = dict(reward=P, n_traj=4, traj=P, grp=P, G=2, off=P, S=8, T=10, adv=P)
+    a.update(kw)
+    assert lib.dart_grpo_advantage(a["reward"], a["n_traj"], a["traj"], a["grp"], a["G"], a["off"],
+                                   a["S"], a["T"], a["adv"], None, None, None) == dart.DART_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [dict(grp=0), dict(G=0), dict(G=9), dict(rho=1.5), dict(S=0),
+                                dict(entropy=0), dict(mask=0)])
+def test_step_select_groups_rejects(kw):
+    lib = dart.load_library()
+    a = dict(entropy=P, T=10, off=P, S=8, grp=P, G=2, rho=0.5, sh=P, mask=P)
+    a.update(kw)
+    assert lib.dart_step_select_groups(a["entropy"], a["T"], a["off"], a["S"], a["grp"], a["G"],
+                                       a["rho"], a["sh"], a["mask"], None, None) == dart.DART_ERR_INVALID_ARG

@@ -58,6 +58,12 @@ MUTATIONS = {
                            "dlog = 1.0;"),
     "step_ratio_product_vs_mean": ("            if (ratio == RATIO_STEP_GEOMEAN) {\n                lr /= (double)len;",
                                    "            if (ratio == RATIO_STEP_PRODUCT) {\n                lr /= (double)len;"),
+    "grpo_sample_variance": ("const double sd = count > 0 ? sqrt(ksum_value(&sq) / (double)count) : 0.0;",
+                             "const double sd = count > 1 ? sqrt(ksum_value(&sq) / (double)(count - 1)) : 0.0;"),
+    "grpo_weights_trajectories_not_steps": ("            for (int64_t s = traj_off[i]; s < traj_off[i + 1]; ++s) {\n                ksum_add(&sum, (double)reward[i]);",
+                                            "            for (int64_t s = traj_off[i]; s < traj_off[i] + 1; ++s) {\n                ksum_add(&sum, (double)reward[i]);"),
+    "grpo_no_centering": ("const double a = sd > 0.0 ? ((double)reward[i] - mean) / sd : 0.0;",
+                          "const double a = sd > 0.0 ? (double)reward[i] / sd : 0.0;"),
     "temperature_not_in_gradient": ("out[t * V + v] = inv_temp * g[t] * (delta - p);",
                                     "out[t * V + v] = g[t] * (delta - p);"),
     "temperature_not_in_logp": ("logp[t] = (inv_temp * logit_at(z, dtype, ld, t, target[t]) - m) - log_s;",
@@ -80,6 +86,7 @@ def test_planted_mistake_is_caught(name, tmp_path):
     proc = subprocess.run(
         [sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
          os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-         os.path.join(ROOT, "tests", "test_oracle_ext_pins.py"), "-k", "not mini"],
+         os.path.join(ROOT, "tests", "test_oracle_ext_pins.py"),
+         os.path.join(ROOT, "tests", "test_oracle_grpo_pins.py"), "-k", "not mini"],
         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert proc.returncode != 0, f"mutation {name} survived the pins:\n{proc.stdout[-2000:]}"
