@@ -111,9 +111,14 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
  *                the loss kernel to the gradient kernel).
  *   stats:       [4] float32 output or NULL: clip fraction, mean TIS weight,
  *                fraction of weights at the cap, N (all over kept tokens).
+ * Workspace: the loss kernel adds per-workgroup partial sums (at most 41 KB)
+ * in a workspace that the library allocates and frees on `stream`, ordered
+ * with the kernels, from a memory pool of its own (one per device, kept until
+ * the process ends); no host synchronisation.
  * Errors: INVALID_ARG for a null required pointer, T < 1, V < 1, ld < V,
  * ld_out < V, S < 1, S > T, eps < 0 or NaN, C <= 0 or NaN, an unknown dtype,
- * or a partial overlap of dlogits with logits. */
+ * or a partial overlap of dlogits with logits; HIP when the workspace cannot
+ * be allocated or a launch fails. */
 dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
                                     int64_t ld, const int32_t* target, const float* logp,
                                     const float* lse, const float* logp_old,

@@ -4,23 +4,29 @@
 // high-entropy step selection (Sec. 4.3, indicator of Eq. 2), truncated
 // importance sampling (Sec. 4.4), clipped surrogate (Eq. 1, Eq. 2).
 //
-// Four kernels, all launched on the caller's stream:
+// Kernels of the path, all launched on the caller's stream:
 //   tok_stats_kernel    one workgroup per logits row; one streaming pass with an
 //                       online (max, normaliser, entropy) triple in fp32 per lane,
 //                       merged across lanes and waves; target logit gathered.
-//   step_select_kernel  one workgroup: per-step mean entropy (fp64 sums in a fixed
-//                       order), radix select of the k-th largest 32-bit key over
-//                       steps with LDS histograms, index-ordered tie resolution.
-//   tis_coef_kernel     one workgroup: per-token ratio, TIS weight, clip gate and
-//                       loss coefficient; loss summed in fp64 in a fixed order.
+//   step_mean_kernel    one wave per step: mean entropy, fp64 sums in a fixed order.
+//   step_select_kernel  one workgroup per group of steps: direct rank of the
+//                       step keys (small groups) or radix select of the k-th
+//                       largest 32-bit key with LDS histograms; index-ordered ties.
+//   tis_coef_kernel     many workgroups: per-token ratio, TIS weight, clip gate and
+//                       loss coefficient; partial sums of the loss in fp64
+//                       (tis_coef_step_kernel: one workgroup, step-level ratios).
+//   tis_loss_finalize_kernel  adds the partial sums in a fixed order.
 //   tis_grad_kernel     one workgroup per row; second streaming pass writing
 //                       coef * (onehot - softmax) in the logits dtype.
 // The two streaming kernels are HBM-bound (no matrix contraction anywhere):
-// 16-byte non-temporal loads, 4 loads in flight per lane, base-2 exponentials.
+// 16-byte non-temporal loads, 4 (8 in place) loads in flight per lane,
+// base-2 exponentials.
 #include <hip/hip_runtime.h>
 #include <hip/hip_bf16.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <mutex>
 
 #include "dart.h"
 
@@ -229,6 +235,7 @@ constexpr int kStatsThreads = 768;
 constexpr int kStatsUnroll = 4;
 constexpr int kGradThreads = 1024;
 constexpr int kGradUnroll = 4;
+constexpr int kGradUnrollInPlace = 8;  // in place: 8 vectors per lane (measured +3% at 46 GB)
 constexpr bool kPipe = false;
 constexpr bool kNtLoad = true;
 constexpr bool kNtStore = true;
@@ -407,6 +414,8 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelLdsKeys = 8192;  // groups up to this many steps keep their keys in LDS
+constexpr int kSelRankMax = 256;   // groups up to this many steps are ranked directly
 
 __device__ __forceinline__ double wave_sum(double x) {
 #pragma unroll
@@ -428,6 +437,23 @@ __device__ __forceinline__ uint32_t float_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Step means: one wave per step, lanes stride the step's tokens, fixed
+// butterfly order (identical steps give identical means wherever they sit).
+// Grid: ceil(S / waves per workgroup), so every step runs in parallel.
+__global__ void __launch_bounds__(kSelThreads)
+step_mean_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
+                 int64_t S, float* __restrict__ step_H) {
+    const int lane = threadIdx.x & 63;
+    const int64_t s = (int64_t)blockIdx.x * kSelWaves + (threadIdx.x >> 6);
+    if (s >= S) return;
+    int64_t b, e;
+    step_bounds(off, s, T, b, e);
+    double sum = 0.0;
+    for (int64_t i = b + lane; i < e; i += 64) sum += (double)H[i];
+    sum = wave_sum(sum);
+    if (lane == 0) step_H[s] = (float)(sum / (double)(e - b));
+}
+
 // k = clamp(ceil(rho * n - 1e-6), 0, n), with the two double operations
 // rounded separately (no contraction) so that it equals the host's count.
 __device__ __forceinline__ int64_t kept_steps_dev(int64_t n, double rho) {
@@ -438,12 +464,14 @@ __device__ __forceinline__ int64_t kept_steps_dev(int64_t n, double rho) {
 
 // One workgroup per group of steps: group g is steps [grp[g], grp[g+1]) (or all
 // S steps when grp is null, with k given); it keeps the ceil(rho S_g) steps of
-// highest mean entropy among its own.
+// highest mean entropy (step_H, from step_mean_kernel) among its own, equal
+// means lower step index first: by direct rank in small groups, else by a
+// radix select of the k-th key and a scan over the keys equal to it.
 __global__ void __launch_bounds__(kSelThreads)
-step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
-                   int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
-                   float* __restrict__ step_H, uint8_t* __restrict__ mask,
+step_select_kernel(int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
+                   const float* __restrict__ step_H, uint8_t* __restrict__ mask,
                    int32_t* __restrict__ n_kept) {
+    __shared__ uint32_t keys[kSelLdsKeys];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sel_bin;
     __shared__ int64_t sel_remaining;
@@ -460,21 +488,35 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     }
     const int64_t Sg = ge - gs;
 
-    // step means: one wave per step, lanes stride the step's tokens, fixed
-    // butterfly order (identical steps give identical means)
-    for (int64_t s = gs + wave; s < ge; s += kSelWaves) {
-        int64_t b, e;
-        step_bounds(off, s, T, b, e);
-        double sum = 0.0;
-        for (int64_t i = b + lane; i < e; i += 64) sum += (double)H[i];
-        sum = wave_sum(sum);
-        if (lane == 0) step_H[s] = (float)(sum / (double)(e - b));
-    }
-    __syncthreads();
-
     if (k <= 0 || k >= Sg) {
         for (int64_t s = gs + tid; s < ge; s += kSelThreads) mask[s] = k > 0 ? 1 : 0;
         if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)(k > 0 ? Sg : 0);
+        return;
+    }
+
+    // the group's keys, read once (LDS when they fit)
+    const bool staged = Sg <= kSelLdsKeys;
+    if (staged) {
+        for (int64_t i = tid; i < Sg; i += kSelThreads) keys[i] = float_key(step_H[gs + i]);
+        __syncthreads();
+    }
+    auto key_at = [&](int64_t i) -> uint32_t {
+        return staged ? keys[i] : float_key(step_H[gs + i]);
+    };
+
+    if (Sg <= kSelRankMax) {
+        // small group: the rank of each step among the group (higher key
+        // first, equal keys lower index first) decides directly
+        for (int64_t i = tid; i < Sg; i += kSelThreads) {
+            const uint32_t ki = keys[i];
+            int64_t rank = 0;
+            for (int64_t j = 0; j < Sg; ++j) {
+                const uint32_t kj = keys[j];
+                rank += (kj > ki || (kj == ki && j < i)) ? 1 : 0;
+            }
+            mask[gs + i] = rank < k ? 1 : 0;
+        }
+        if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)k;
         return;
     }
 
@@ -484,8 +526,8 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     for (int shift = 24; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
         __syncthreads();
-        for (int64_t s = gs + tid; s < ge; s += kSelThreads) {
-            const uint32_t key = float_key(step_H[s]);
+        for (int64_t i = tid; i < Sg; i += kSelThreads) {
+            const uint32_t key = key_at(i);
             if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
         }
         __syncthreads();
@@ -530,22 +572,22 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     // keep keys above the k-th; of the keys equal to it keep the first
     // `remaining` in step order (block scan over tiles of kSelThreads steps)
     int64_t carry = 0;
-    for (int64_t base = gs; base < ge; base += kSelThreads) {
-        const int64_t s = base + tid;
-        const uint32_t key = s < ge ? float_key(step_H[s]) : 0u;
-        const bool eq = s < ge && key == prefix;
+    for (int64_t base = 0; base < Sg; base += kSelThreads) {
+        const int64_t i = base + tid;
+        const uint32_t key = i < Sg ? key_at(i) : 0u;
+        const bool eq = i < Sg && key == prefix;
         const uint64_t ballot = __ballot(eq);
         const int before = __popcll(ballot & ((1ull << lane) - 1ull));
         if (lane == 0) wave_count[wave] = __popcll(ballot);
         __syncthreads();
         int64_t wave_before = 0, total = 0;
-        for (int i = 0; i < kSelWaves; ++i) {
-            if (i < wave) wave_before += wave_count[i];
-            total += wave_count[i];
+        for (int w = 0; w < kSelWaves; ++w) {
+            if (w < wave) wave_before += wave_count[w];
+            total += wave_count[w];
         }
-        if (s < ge) {
+        if (i < Sg) {
             const int64_t rank = carry + wave_before + before;
-            mask[s] = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
+            mask[gs + i] = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
         }
         carry += total;
         __syncthreads();
@@ -629,14 +671,49 @@ grpo_advantage_kernel(const float* __restrict__ reward, const int32_t* __restric
 // K3: per-token TIS / clip coefficient and the loss
 // ------------------------------------------------------------------------
 
-constexpr int kCoefThreads = 1024;
-constexpr int kCoefWaves = kCoefThreads / 64;
-
 struct LossConfig {
     float eps_low, eps_high, C, log_C;
     int kl, agg, ratio;
     float beta;
 };
+
+// Per token t of step s (M = 1 if the step is kept, else 0):
+//   loss term  l_t = -M om_t (w o - beta kl_t),  o = min(r A, clip(r) A)
+//   coefficient g_t = dL/dlogp_t = -M (Om w [u <= c] r A dlog - om_t beta dkl_t)
+// with om_t the aggregation weight (1/N, 1/T or 1/(K |s|)). Token ratios use
+// r = exp(logp - lp_old) and w = min(exp(lp_old - lp_roll), C) per token
+// (Om = om_t, dlog = 1); step ratios use the sum (product) or mean (geometric
+// mean) of the token log-ratios of the step and its mean advantage, shared by
+// all its tokens (Om = om |s|, dlog = 1 or 1/|s|).
+//
+// Token ratios run on many workgroups (one CU cannot keep enough loads in
+// flight to read T tokens quickly); each writes the partial sums of its
+// tokens to a small workspace, and tis_loss_finalize_kernel adds them in
+// workgroup order. Step ratios run on one workgroup, one wave per step.
+// Every sum is in fp64 and in a fixed order: per lane in token order, then a
+// fixed butterfly, then waves, then workgroups.
+
+// partial sums per workgroup, in this order
+enum { kPartLoss = 0, kPartW, kPartClip, kPartCap, kPartKl, kParts };
+
+constexpr int kCoefThreads = 256;  // workgroup of the many-workgroup launch
+constexpr int kCoefWaves = kCoefThreads / 64;
+constexpr int kCoefOneThreads = 1024;  // workgroup of the one-workgroup launch
+constexpr int kCoefBatch = 4;  // tokens per lane whose loads are in flight together
+constexpr int kCoefChunk = kCoefThreads * kCoefBatch;  // tokens per workgroup iteration
+constexpr int kCoefMaxBlocks = 1024;
+// up to this many tokens one workgroup writes the loss itself (no workspace,
+// no second kernel): below it the second launch and the workspace cost more
+// than the extra bandwidth of many workgroups saves
+constexpr int64_t kCoefOneBlockMaxT = 8192;
+constexpr int kCoefLdsSteps = 8192;  // offsets and mask of up to this many steps go to LDS
+constexpr int kStepCoefThreads = 1024;
+constexpr int kStepCoefWaves = kStepCoefThreads / 64;
+
+// workspace: kParts doubles per workgroup, then N and K
+__host__ __device__ constexpr int64_t coef_workspace_doubles(int64_t nblocks) {
+    return nblocks * kParts + 2;
+}
 
 // KL estimators of D_KL(pi_theta || pi_ref) from the sampled token, with
 // delta = log pi_ref - log pi_theta: k1 = -delta, k2 = delta^2 / 2,
@@ -658,36 +735,28 @@ __device__ __forceinline__ void kl_terms(int kl, double delta, double& value, do
     }
 }
 
-// One wave per step, lanes over the step's tokens. Per token t of step s:
-//   loss term  l_t = -M om_t (w o - beta kl_t),  o = min(r A, clip(r) A)
-//   coefficient g_t = dL/dlogp_t = -M (Om w [u <= c] r A dlog - om_t beta dkl_t)
-// with om_t the aggregation weight (1/N, 1/T or 1/(K |s|)). Token ratios use
-// r = exp(logp - lp_old) and w = min(exp(lp_old - lp_roll), C) per token
-// (Om = om_t, dlog = 1); step ratios use the sum (product) or mean (geometric
-// mean) of the token log-ratios of the step and its mean advantage, shared by
-// all its tokens (Om = om |s|, dlog = 1 or 1/|s|). The loss and the counters
-// are summed per lane in token order, then in a fixed butterfly and wave order.
-// GENERAL = false compiles the paper's default configuration only (no KL term,
-// token ratios, token mean over kept tokens).
-template <bool GENERAL>
-__global__ void __launch_bounds__(kCoefThreads)
-tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
-                const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
-                const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
-                const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
-                double* __restrict__ loss, float* __restrict__ stats, int nstats) {
-    __shared__ int64_t red_i[2][kCoefWaves];
-    __shared__ double red_d[5][kCoefWaves];
-
+// Kept tokens N and kept steps K over all S steps, block-wide; with
+// off_l/mask_l non-null the (clamped) offsets and the mask are also staged.
+template <int THREADS>
+__device__ __forceinline__ void count_kept(const int32_t* __restrict__ off,
+                                           const uint8_t* __restrict__ mask, int64_t S, int64_t T,
+                                           int32_t* off_l, uint8_t* mask_l,
+                                           int64_t (*red)[THREADS / 64], int64_t& N, int64_t& K) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-
     int64_t n_local = 0, k_local = 0;
-    for (int64_t s = tid; s < S; s += kCoefThreads) {
+#pragma unroll 4
+    for (int64_t s = tid; s < S; s += THREADS) {
         int64_t b, e;
         step_bounds(off, s, T, b, e);
-        if (mask[s]) {
+        const uint8_t m = mask[s];
+        if (off_l) {
+            off_l[s] = (int32_t)b;
+            mask_l[s] = m;
+            if (s == S - 1) off_l[S] = (int32_t)e;
+        }
+        if (m) {
             n_local += e - b;
             k_local += 1;
         }
@@ -698,23 +767,195 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
         k_local += __shfl_xor(k_local, o);
     }
     if (lane == 0) {
-        red_i[0][wave] = n_local;
-        red_i[1][wave] = k_local;
+        red[0][wave] = n_local;
+        red[1][wave] = k_local;
     }
     __syncthreads();
-    int64_t N = 0, K = 0;
-    for (int i = 0; i < kCoefWaves; ++i) {
-        N += red_i[0][i];
-        K += red_i[1][i];
+    N = 0;
+    K = 0;
+    for (int i = 0; i < THREADS / 64; ++i) {
+        N += red[0][i];
+        K += red[1][i];
+    }
+}
+
+// Sums the kParts per-lane values over the block in a fixed order (butterfly
+// within each wave, then a butterfly over the wave totals in wave 0); the
+// result is valid in thread 0.
+template <int THREADS>
+__device__ __forceinline__ void block_sum_parts(double (&acc)[kParts],
+                                                double (*red)[THREADS / 64]) {
+    constexpr int WAVES = THREADS / 64;
+    static_assert(WAVES <= 64, "one wave adds the wave totals");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < kParts; ++i) acc[i] = wave_sum(acc[i]);
+    if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < kParts; ++i) red[i][wave] = acc[i];
+    __syncthreads();
+    if (wave == 0)
+#pragma unroll
+        for (int i = 0; i < kParts; ++i) acc[i] = wave_sum(lane < WAVES ? red[i][lane] : 0.0);
+}
+
+// Loss and stats = {clip fraction, mean TIS weight, capped fraction, N, mean
+// KL, K} (the first nstats of them) from the summed parts.
+__device__ __forceinline__ void write_loss(const double (&acc)[kParts], double N, double K,
+                                           double* loss, float* stats, int nstats) {
+    const double inv_n = N > 0 ? 1.0 / N : 0.0;
+    loss[0] = acc[kPartLoss];
+    if (stats) {
+        const float out[6] = {(float)(acc[kPartClip] * inv_n), (float)(acc[kPartW] * inv_n),
+                              (float)(acc[kPartCap] * inv_n), (float)N,
+                              (float)(acc[kPartKl] * inv_n), (float)K};
+        for (int j = 0; j < nstats; ++j) stats[j] = out[j];
+    }
+}
+
+// Token ratios. Workgroup b takes chunks b, b + grid, ... of THREADS *
+// kCoefBatch tokens; lane tokens are THREADS apart within a chunk (coalesced).
+// The step of each token is found by binary search over the offsets. With
+// part != null each workgroup writes its partial sums there (workgroup 0 also
+// N and K); with part == null the grid is one workgroup, which writes the loss
+// and stats itself.
+template <bool GENERAL, int THREADS>
+__global__ void __launch_bounds__(THREADS)
+tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
+                const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
+                const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
+                const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
+                double* __restrict__ part, double* __restrict__ loss, float* __restrict__ stats,
+                int nstats) {
+    constexpr int CHUNK = THREADS * kCoefBatch;
+    __shared__ int32_t off_l[kCoefLdsSteps + 1];
+    __shared__ uint8_t mask_l[kCoefLdsSteps];
+    __shared__ int64_t red_i[2][THREADS / 64];
+    __shared__ double red_d[kParts][THREADS / 64];
+
+    const int tid = threadIdx.x;
+    const bool staged = S <= kCoefLdsSteps;
+    int64_t N, K;
+    count_kept<THREADS>(off, mask, S, T, staged ? off_l : nullptr, staged ? mask_l : nullptr,
+                        red_i, N, K);
+    if (part && blockIdx.x == 0 && tid == 0) {
+        part[(int64_t)gridDim.x * kParts] = (double)N;
+        part[(int64_t)gridDim.x * kParts + 1] = (double)K;
     }
 
     const double inv_n = N > 0 ? 1.0 / (double)N : 0.0;
     const float lo = 1.f - cfg.eps_low, hi = 1.f + cfg.eps_high;
-    const bool step_ratio = GENERAL && cfg.ratio != DART_RATIO_TOKEN;
     const bool with_kl = GENERAL && cfg.kl != DART_KL_NONE;
     const double beta = (double)cfg.beta;
-    double l_acc = 0.0, w_acc = 0.0, n_clip = 0.0, n_cap = 0.0, kl_acc = 0.0;
-    for (int64_t s = wave; s < S; s += kCoefWaves) {
+    auto off_at = [&](int64_t i) -> int64_t {
+        return staged ? (int64_t)off_l[i] : min(max((int64_t)off[i], (int64_t)0), T);
+    };
+    auto weight = [&](int64_t len) -> double {
+        if (GENERAL && cfg.agg == DART_AGG_TOKEN_MEAN_ALL) return 1.0 / (double)T;
+        if (GENERAL && cfg.agg == DART_AGG_STEP_MEAN) return 1.0 / ((double)K * (double)len);
+        return inv_n;
+    };
+    // largest power of two below S (binary search over step indices [0, S-1])
+    int64_t top = 0;
+    if (S > 1) {
+        top = 1;
+        while (top * 2 <= S - 1) top *= 2;
+    }
+
+    double acc[kParts] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    const int64_t nchunks = (T + CHUNK - 1) / CHUNK;
+    for (int64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
+        const int64_t base = c * CHUNK + tid;
+        // step of each token: the last s with off[s] <= t, all at once
+        int64_t st[kCoefBatch];
+#pragma unroll
+        for (int j = 0; j < kCoefBatch; ++j) st[j] = 0;
+        for (int64_t stride = top; stride > 0; stride >>= 1) {
+#pragma unroll
+            for (int j = 0; j < kCoefBatch; ++j) {
+                const int64_t t = base + (int64_t)j * THREADS;
+                if (st[j] + stride < S && off_at(st[j] + stride) <= t) st[j] += stride;
+            }
+        }
+        bool kept[kCoefBatch];
+        double om[kCoefBatch];
+        float A[kCoefBatch], lp[kCoefBatch], lpo[kCoefBatch], lpr[kCoefBatch], lpf[kCoefBatch];
+#pragma unroll
+        for (int j = 0; j < kCoefBatch; ++j) {
+            const int64_t t = base + (int64_t)j * THREADS;
+            kept[j] = t < T && N > 0 && (staged ? mask_l[st[j]] : mask[st[j]]) != 0;
+            om[j] = kept[j] ? weight(off_at(st[j] + 1) - off_at(st[j])) : 0.0;
+            A[j] = lp[j] = lpo[j] = lpr[j] = lpf[j] = 0.f;
+            if (kept[j]) {
+                A[j] = adv[t];
+                lp[j] = logp[t];
+                lpo[j] = lp_old[t];
+                lpr[j] = lp_roll[t];
+                if (with_kl) lpf[j] = lp_ref[t];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kCoefBatch; ++j) {
+            const int64_t t = base + (int64_t)j * THREADS;
+            if (t >= T) break;
+            if (!kept[j]) {
+                coef[t] = 0.f;
+                continue;
+            }
+            const float r = expf(lp[j] - lpo[j]);
+            const float d = lpo[j] - lpr[j];
+            const bool capped = d >= cfg.log_C;
+            const float wf = capped ? cfg.C : fminf(expf(d), cfg.C);
+            const float rc = fminf(fmaxf(r, lo), hi);
+            const float u = r * A[j];
+            const float cl = rc * A[j];
+            const bool gate = u <= cl;
+            const double w = (double)wf;
+            const double obj = w * (double)fminf(u, cl);
+            const double dobj = gate ? w * (double)A[j] * (double)r : 0.0;
+            double klv = 0.0, kld = 0.0;
+            if (with_kl) kl_terms(cfg.kl, (double)lpf[j] - (double)lp[j], klv, kld);
+            acc[kPartLoss] -= om[j] * (obj - beta * klv);
+            coef[t] = (float)(-(om[j] * dobj - om[j] * beta * kld));
+            acc[kPartW] += w;
+            acc[kPartClip] += gate ? 0.0 : 1.0;
+            acc[kPartCap] += capped ? 1.0 : 0.0;
+            acc[kPartKl] += klv;
+        }
+    }
+    block_sum_parts<THREADS>(acc, red_d);
+    if (tid != 0) return;
+    if (part)
+#pragma unroll
+        for (int i = 0; i < kParts; ++i) part[(int64_t)blockIdx.x * kParts + i] = acc[i];
+    else
+        write_loss(acc, (double)N, (double)K, loss, stats, nstats);
+}
+
+// Step ratios: one workgroup, one wave per step, the step's sums first.
+__global__ void __launch_bounds__(kStepCoefThreads)
+tis_coef_step_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
+                     const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
+                     const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
+                     const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
+                     double* __restrict__ loss, float* __restrict__ stats, int nstats) {
+    __shared__ int64_t red_i[2][kStepCoefWaves];
+    __shared__ double red_d[kParts][kStepCoefWaves];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    int64_t N, K;
+    count_kept<kStepCoefThreads>(off, mask, S, T, nullptr, nullptr, red_i, N, K);
+
+    const double inv_n = N > 0 ? 1.0 / (double)N : 0.0;
+    const float lo = 1.f - cfg.eps_low, hi = 1.f + cfg.eps_high;
+    const bool with_kl = cfg.kl != DART_KL_NONE;
+    const double beta = (double)cfg.beta;
+    double acc[kParts] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    for (int64_t s = wave; s < S; s += kStepCoefWaves) {
         int64_t b, e;
         step_bounds(off, s, T, b, e);
         const int64_t len = e - b;
@@ -724,106 +965,74 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
             continue;
         }
         double om = inv_n;
-        if (GENERAL && cfg.agg == DART_AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)T;
-        if (GENERAL && cfg.agg == DART_AGG_STEP_MEAN) om = 1.0 / ((double)K * (double)len);
-
-        double r_s = 0.0, w_s = 0.0, A_s = 0.0, dlog = 1.0, om_obj = om;
-        bool cap_s = false;
-        if (step_ratio) {
-            double slr = 0.0, slw = 0.0, sa = 0.0;
-            for (int64_t t = b + lane; t < e; t += 64) {
-                slr += (double)logp[t] - (double)lp_old[t];
-                slw += (double)lp_old[t] - (double)lp_roll[t];
-                sa += (double)adv[t];
-            }
-            slr = wave_sum(slr);
-            slw = wave_sum(slw);
-            sa = wave_sum(sa);
-            if (cfg.ratio == DART_RATIO_STEP_GEOMEAN) {
-                slr /= (double)len;
-                slw /= (double)len;
-                dlog = 1.0 / (double)len;
-            }
-            r_s = exp(slr);
-            cap_s = slw >= (double)cfg.log_C;
-            w_s = cap_s ? (double)cfg.C : fmin(exp(slw), (double)cfg.C);
-            A_s = sa / (double)len;
-            om_obj = om * (double)len;
-        }
-
+        if (cfg.agg == DART_AGG_TOKEN_MEAN_ALL) om = 1.0 / (double)T;
+        if (cfg.agg == DART_AGG_STEP_MEAN) om = 1.0 / ((double)K * (double)len);
+        double slr = 0.0, slw = 0.0, sa = 0.0, dlog = 1.0;
         for (int64_t t = b + lane; t < e; t += 64) {
-            double obj, dobj, w;
-            bool gate, capped;
-            if (!step_ratio) {
-                const float A = adv[t];
-                const float r = expf(logp[t] - lp_old[t]);
-                const float d = lp_old[t] - lp_roll[t];
-                capped = d >= cfg.log_C;
-                const float wf = capped ? cfg.C : fminf(expf(d), cfg.C);
-                const float rc = fminf(fmaxf(r, lo), hi);
-                const float u = r * A;
-                const float c = rc * A;
-                gate = u <= c;
-                w = (double)wf;
-                obj = w * (double)fminf(u, c);
-                dobj = gate ? w * (double)A * (double)r : 0.0;
-            } else {
-                const double rc = fmin(fmax(r_s, (double)lo), (double)hi);
-                const double u = r_s * A_s;
-                const double c = rc * A_s;
-                gate = u <= c;
-                capped = cap_s;
-                w = w_s;
-                obj = w * fmin(u, c);
-                dobj = gate ? w * r_s * A_s * dlog : 0.0;
-            }
+            slr += (double)logp[t] - (double)lp_old[t];
+            slw += (double)lp_old[t] - (double)lp_roll[t];
+            sa += (double)adv[t];
+        }
+        slr = wave_sum(slr);
+        slw = wave_sum(slw);
+        sa = wave_sum(sa);
+        if (cfg.ratio == DART_RATIO_STEP_GEOMEAN) {
+            slr /= (double)len;
+            slw /= (double)len;
+            dlog = 1.0 / (double)len;
+        }
+        const double r_s = exp(slr);
+        const bool capped = slw >= (double)cfg.log_C;
+        const double w = capped ? (double)cfg.C : fmin(exp(slw), (double)cfg.C);
+        const double A_s = sa / (double)len;
+        const double om_obj = om * (double)len;
+        const double rc = fmin(fmax(r_s, (double)lo), (double)hi);
+        const double u = r_s * A_s;
+        const double cl = rc * A_s;
+        const bool gate = u <= cl;
+        const double obj = w * fmin(u, cl);
+        const double dobj = gate ? w * r_s * A_s * dlog : 0.0;
+        for (int64_t t = b + lane; t < e; t += 64) {
             double klv = 0.0, kld = 0.0;
             if (with_kl) kl_terms(cfg.kl, (double)lp_ref[t] - (double)logp[t], klv, kld);
-            l_acc -= om * (obj - beta * klv);
+            acc[kPartLoss] -= om * (obj - beta * klv);
             coef[t] = (float)(-(om_obj * dobj - om * beta * kld));
-            w_acc += w;
-            n_clip += gate ? 0.0 : 1.0;
-            n_cap += capped ? 1.0 : 0.0;
-            kl_acc += klv;
+            acc[kPartW] += w;
+            acc[kPartClip] += gate ? 0.0 : 1.0;
+            acc[kPartCap] += capped ? 1.0 : 0.0;
+            acc[kPartKl] += klv;
         }
     }
-    l_acc = wave_sum(l_acc);
-    w_acc = wave_sum(w_acc);
-    n_clip = wave_sum(n_clip);
-    n_cap = wave_sum(n_cap);
-    kl_acc = wave_sum(kl_acc);
-    if (lane == 0) {
-        red_d[0][wave] = l_acc;
-        red_d[1][wave] = w_acc;
-        red_d[2][wave] = n_clip;
-        red_d[3][wave] = n_cap;
-        red_d[4][wave] = kl_acc;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        double acc[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
-        for (int i = 0; i < kCoefWaves; ++i)
-            for (int j = 0; j < 5; ++j) acc[j] += red_d[j][i];
-        loss[0] = acc[0];
-        if (stats) {
-            const float out[6] = {(float)(acc[2] * inv_n), (float)(acc[1] * inv_n),
-                                  (float)(acc[3] * inv_n), (float)N, (float)(acc[4] * inv_n),
-                                  (float)K};
-            for (int j = 0; j < nstats; ++j) stats[j] = out[j];
-        }
-    }
+    block_sum_parts<kStepCoefThreads>(acc, red_d);
+    if (tid == 0) write_loss(acc, (double)N, (double)K, loss, stats, nstats);
+}
+
+// Adds the nblocks partial sums in workgroup order and writes the loss and
+// stats.
+__global__ void __launch_bounds__(kCoefThreads)
+tis_loss_finalize_kernel(const double* __restrict__ part, int64_t nblocks,
+                         double* __restrict__ loss, float* __restrict__ stats, int nstats) {
+    __shared__ double red_d[kParts][kCoefWaves];
+    double acc[kParts] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    for (int64_t b = threadIdx.x; b < nblocks; b += kCoefThreads)
+#pragma unroll
+        for (int i = 0; i < kParts; ++i) acc[i] += part[b * kParts + i];
+    block_sum_parts<kCoefThreads>(acc, red_d);
+    if (threadIdx.x == 0)
+        write_loss(acc, part[nblocks * kParts], part[nblocks * kParts + 1], loss, stats, nstats);
 }
 
 // ------------------------------------------------------------------------
 // K4: dlogits = coef * (onehot(target) - softmax(z))
 // ------------------------------------------------------------------------
 
-template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS, bool REV = false>
-__global__ void __launch_bounds__(THREADS)
-tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __restrict__ target,
-                const float* __restrict__ lse, const float* __restrict__ logp,
-                const float* __restrict__ coef, float inv_temp, uint32_t flags, void* dlogits,
-                int64_t ld_out) {
+template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS, bool REV>
+__device__ __forceinline__ void tis_grad_row(int64_t t, const void* logits, int64_t V, int64_t ld,
+                                             const int32_t* __restrict__ target,
+                                             const float* __restrict__ lse,
+                                             const float* __restrict__ logp,
+                                             const float* __restrict__ coef, float inv_temp,
+                                             uint32_t flags, void* dlogits, int64_t ld_out) {
     // logits and dlogits may be the same buffer (in place): every element is
     // read and then written by the same lane, and a lane only reads elements
     // it has not yet written.
@@ -831,7 +1040,6 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
     constexpr int EPV = Elt<D>::kPerVec;
     constexpr int PER_IT = THREADS * UNROLL;
 
-    const int64_t t = REV ? (int64_t)gridDim.x - 1 - blockIdx.x : (int64_t)blockIdx.x;
     const int tid = threadIdx.x;
     const E* row = static_cast<const E*>(logits) + t * ld;
     E* orow = static_cast<E*>(dlogits) + t * ld_out;
@@ -904,6 +1112,22 @@ tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __rest
     }
 }
 
+// One row per workgroup (rows_per_block == 0: grid = T), or a persistent grid
+// in which workgroup b takes rows b, b + gridDim.x, ... .
+template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS, bool REV = false>
+__global__ void __launch_bounds__(THREADS)
+tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __restrict__ target,
+                const float* __restrict__ lse, const float* __restrict__ logp,
+                const float* __restrict__ coef, float inv_temp, uint32_t flags, void* dlogits,
+                int64_t ld_out, int64_t T) {
+    for (int64_t b = blockIdx.x; b < T; b += gridDim.x) {
+        const int64_t t = REV ? T - 1 - b : b;
+        tis_grad_row<D, THREADS, UNROLL, PIPE, NTL, NTS, REV>(t, logits, V, ld, target, lse, logp,
+                                                              coef, inv_temp, flags, dlogits,
+                                                              ld_out);
+    }
+}
+
 // ------------------------------------------------------------------------
 // host helpers
 // ------------------------------------------------------------------------
@@ -926,6 +1150,91 @@ bool bad_overlap(const void* logits, int64_t ld, const void* dlogits, int64_t ld
 
 dart_status_t launch_status() {
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+// Stream-ordered workspace from a memory pool of the library's own, one per
+// device, created on first use and kept (with its memory: the release
+// threshold is the maximum) until the process ends. Allocation and free are
+// ordered on the caller's stream, so calls on different streams never share
+// a workspace.
+constexpr int kMaxDevices = 64;
+
+hipError_t workspace_alloc(void** ptr, size_t bytes, hipStream_t stream) {
+    int dev = 0;
+    hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    static std::mutex mu;
+    static hipMemPool_t pools[kMaxDevices] = {};
+    hipMemPool_t pool;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        if (!pools[dev]) {
+            hipMemPoolProps props = {};
+            props.allocType = hipMemAllocationTypePinned;
+            props.handleTypes = hipMemHandleTypeNone;
+            props.location.type = hipMemLocationTypeDevice;
+            props.location.id = dev;
+            hipMemPool_t created = nullptr;
+            e = hipMemPoolCreate(&created, &props);
+            if (e != hipSuccess) return e;
+            uint64_t keep = UINT64_MAX;
+            e = hipMemPoolSetAttribute(created, hipMemPoolAttrReleaseThreshold, &keep);
+            if (e != hipSuccess) {
+                (void)hipMemPoolDestroy(created);
+                return e;
+            }
+            pools[dev] = created;
+        }
+        pool = pools[dev];
+    }
+    return hipMallocFromPoolAsync(ptr, bytes, pool, stream);
+}
+
+// K3 and the loss reduction for one configuration: token ratios on up to
+// kCoefMaxBlocks workgroups, step ratios on one.
+dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const float* lp_old,
+                              const float* lp_roll, const float* lp_ref, const float* adv,
+                              const int32_t* off, int64_t S, const uint8_t* mask,
+                              const LossConfig& cfg, float* coef, double* loss, float* stats,
+                              int nstats, hipStream_t stream) {
+    if (general && cfg.ratio != DART_RATIO_TOKEN) {
+        hipLaunchKernelGGL(tis_coef_step_kernel, dim3(1), dim3(kStepCoefThreads), 0, stream, T,
+                           logp, lp_old, lp_roll, lp_ref, adv, off, S, mask, cfg, coef, loss,
+                           stats, nstats);
+        return launch_status();
+    }
+    if (T <= kCoefOneBlockMaxT) {
+        if (general)
+            hipLaunchKernelGGL((tis_coef_kernel<true, kCoefOneThreads>), dim3(1),
+                               dim3(kCoefOneThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref,
+                               adv, off, S, mask, cfg, coef, nullptr, loss, stats, nstats);
+        else
+            hipLaunchKernelGGL((tis_coef_kernel<false, kCoefOneThreads>), dim3(1),
+                               dim3(kCoefOneThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref,
+                               adv, off, S, mask, cfg, coef, nullptr, loss, stats, nstats);
+        return launch_status();
+    }
+    const int64_t nchunks = (T + kCoefChunk - 1) / kCoefChunk;
+    const int64_t nblocks = nchunks < kCoefMaxBlocks ? nchunks : kCoefMaxBlocks;
+    double* part = nullptr;
+    if (workspace_alloc(reinterpret_cast<void**>(&part),
+                        (size_t)coef_workspace_doubles(nblocks) * sizeof(double),
+                        stream) != hipSuccess)
+        return DART_ERR_HIP;
+    if (general)
+        hipLaunchKernelGGL((tis_coef_kernel<true, kCoefThreads>), dim3((unsigned)nblocks),
+                           dim3(kCoefThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref, adv,
+                           off, S, mask, cfg, coef, part, nullptr, nullptr, 0);
+    else
+        hipLaunchKernelGGL((tis_coef_kernel<false, kCoefThreads>), dim3((unsigned)nblocks),
+                           dim3(kCoefThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref, adv,
+                           off, S, mask, cfg, coef, part, nullptr, nullptr, 0);
+    hipLaunchKernelGGL(tis_loss_finalize_kernel, dim3(1), dim3(kCoefThreads), 0, stream, part,
+                       nblocks, loss, stats, nstats);
+    dart_status_t st = launch_status();
+    if (hipFreeAsync(part, stream) != hipSuccess) st = DART_ERR_HIP;
+    return st;
 }
 
 }  // namespace
@@ -983,8 +1292,10 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     const int64_t k = dart_kept_steps(S, rho);
     if (k < 0) return DART_ERR_INVALID_ARG;
-    hipLaunchKernelGGL(step_select_kernel, dim3(1), dim3(kSelThreads), 0, stream, entropy, T,
-                       step_offsets, S, nullptr, rho, k, step_entropy, step_mask, n_kept_steps);
+    hipLaunchKernelGGL(step_mean_kernel, dim3((unsigned)((S + kSelWaves - 1) / kSelWaves)),
+                       dim3(kSelThreads), 0, stream, entropy, T, step_offsets, S, step_entropy);
+    hipLaunchKernelGGL(step_select_kernel, dim3(1), dim3(kSelThreads), 0, stream, S, nullptr, rho,
+                       k, step_entropy, step_mask, n_kept_steps);
     return launch_status();
 }
 
@@ -998,9 +1309,10 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll || G < 1 || G > S || G > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
     if (dart_kept_steps(S, rho) < 0) return DART_ERR_INVALID_ARG;
-    hipLaunchKernelGGL(step_select_kernel, dim3((unsigned)G), dim3(kSelThreads), 0, stream,
-                       entropy, T, step_offsets, S, group_step_offsets, rho, (int64_t)0,
-                       step_entropy, step_mask, n_kept_steps);
+    hipLaunchKernelGGL(step_mean_kernel, dim3((unsigned)((S + kSelWaves - 1) / kSelWaves)),
+                       dim3(kSelThreads), 0, stream, entropy, T, step_offsets, S, step_entropy);
+    hipLaunchKernelGGL(step_select_kernel, dim3((unsigned)G), dim3(kSelThreads), 0, stream, S,
+                       group_step_offsets, rho, (int64_t)0, step_entropy, step_mask, n_kept_steps);
     return launch_status();
 }
 
@@ -1048,10 +1360,9 @@ dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* lo
     cfg.beta = c.kl == DART_KL_NONE ? 0.f : c.beta;
     cfg.agg = c.aggregation;
     cfg.ratio = c.ratio;
-    hipLaunchKernelGGL(tis_coef_kernel<true>, dim3(1), dim3(kCoefThreads), 0, stream, T, logp,
-                       logp_old, logp_rollout, c.kl == DART_KL_NONE ? nullptr : logp_ref, adv,
-                       step_offsets, S, step_mask, cfg, tok_coef, loss, stats, 6);
-    return launch_status();
+    return launch_tis_coef(true, T, logp, logp_old, logp_rollout,
+                           c.kl == DART_KL_NONE ? nullptr : logp_ref, adv, step_offsets, S,
+                           step_mask, cfg, tok_coef, loss, stats, 6, stream);
 }
 
 dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_old,
@@ -1073,10 +1384,8 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
     cfg.beta = 0.f;
     cfg.agg = DART_AGG_TOKEN_MEAN;
     cfg.ratio = DART_RATIO_TOKEN;
-    hipLaunchKernelGGL(tis_coef_kernel<false>, dim3(1), dim3(kCoefThreads), 0, stream, T, logp,
-                       logp_old, logp_rollout, nullptr, adv, step_offsets, S, step_mask, cfg,
-                       tok_coef, loss, stats, 4);
-    return launch_status();
+    return launch_tis_coef(false, T, logp, logp_old, logp_rollout, nullptr, adv, step_offsets, S,
+                           step_mask, cfg, tok_coef, loss, stats, 4, stream);
 }
 
 dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
@@ -1093,16 +1402,22 @@ dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T
         return DART_ERR_INVALID_ARG;
     if (bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
     const dim3 grid((unsigned)T), block(kGradThreads);
-    if (dtype == DART_BF16)
+    const bool in_place = logits == dlogits;
+    if (dtype == DART_BF16 && !in_place)
         hipLaunchKernelGGL(
             (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
             grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
-            dlogits, ld_out);
+            dlogits, ld_out, T);
+    else if (dtype == DART_BF16)
+        hipLaunchKernelGGL(
+            (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnrollInPlace, kPipe, kNtLoad, kNtStore>),
+            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
+            dlogits, ld_out, T);
     else
         hipLaunchKernelGGL(
             (tis_grad_kernel<DART_F32, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
             grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
-            dlogits, ld_out);
+            dlogits, ld_out, T);
     return launch_status();
 }
 
