@@ -42,7 +42,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="0 = the process's CPU affinity (max 16)")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip the separately reported variants (profiling runs of the headline step)")
+                    help="skip the separately reported variants and the copy ceiling "
+                         "(profiling runs of the headline step)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed steps, run one plain device copy of this many MiB "
                          "(torch copy kernel) so that hardware counters can be scaled by it")
@@ -140,6 +141,7 @@ def main():
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     coef = torch.empty(T, dtype=torch.float32, device=dev)
     stats = torch.empty(4, dtype=torch.float32, device=dev)
+    workspace = torch.empty(dart.dart_tis_loss_workspace_bytes(T), dtype=torch.uint8, device=dev)
     dlogits = logits if wl.inplace else torch.empty((T, V), dtype=tdt, device=dev)
     eps_low, eps_high, C = float(np.float32(wl.eps_low)), float(np.float32(wl.eps_high)), float(np.float32(wl.C))
     stream = torch.cuda.current_stream(dev)
@@ -152,7 +154,7 @@ def main():
             ev[1].record(stream)
         dart.dart_step_select(ent, off, wl.rho, step_H, mask, n_kept, stream=stream)
         dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C,
-                               loss, coef, stats, stream=stream)
+                               loss, coef, stats, stream=stream, workspace=workspace)
         if ev:
             ev[2].record(stream)
         dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream)
@@ -241,6 +243,24 @@ def main():
         variants["stats_only"] = {"ms": stats_ms, "logit_elements_per_s": T * V / (stats_ms * 1e-3),
                                   "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
 
+    # empirical ceiling beside the 8 TB/s peak: a plain torch elementwise kernel
+    # reading and writing the same T x V bytes as the gradient pass
+    copy_ceiling = None
+    if not args.no_variants:
+        copy_ev = [(ev_new(), ev_new()) for _ in range(min(args.steps, 10))]
+        torch.mul(logits, 1.0, out=dlogits)  # first launch loads the kernel's code
+        for a, b in copy_ev:
+            a.record(stream)
+            torch.mul(logits, 1.0, out=dlogits)
+            b.record(stream)
+        torch.cuda.synchronize(dev)
+        copy_ms = float(np.median([a.elapsed_time(b) for a, b in copy_ev]))
+        copy_gbs = 2 * T * V * esize / (copy_ms * 1e-3) / 1e9
+        copy_ceiling = {"kernel": "torch elementwise multiply by 1 (T x V read + write)",
+                        "ms": copy_ms, "GBps": copy_gbs, "frac": copy_gbs / HBM_PEAK_GBS}
+        if pristine is not None:
+            logits.copy_(pristine)
+
     k1_ms = [e[0].elapsed_time(e[1]) for e in evs]
     mid_ms = [e[1].elapsed_time(e[2]) for e in evs]
     grad_ms = [e[2].elapsed_time(e[3]) for e in evs]
@@ -274,6 +294,7 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "algorithmic_bytes_per_launch": grad_bytes},
         "variants": variants,
+        "copy_ceiling": copy_ceiling,
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))

@@ -33,6 +33,7 @@
 #define DART_H
 
 #include <hip/hip_runtime_api.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -111,14 +112,18 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
  *                the loss kernel to the gradient kernel).
  *   stats:       [4] float32 output or NULL: clip fraction, mean TIS weight,
  *                fraction of weights at the cap, N (all over kept tokens).
- * Workspace: the loss kernel adds per-workgroup partial sums (at most 41 KB)
- * in a workspace that the library allocates and frees on `stream`, ordered
- * with the kernels, from a memory pool of its own (one per device, kept until
- * the process ends); no host synchronisation.
+ *   workspace, workspace_bytes: device memory owned by the caller, or NULL.
+ *                With a workspace of at least dart_tis_loss_workspace_bytes(T)
+ *                bytes (8-byte aligned; contents on entry do not matter) the
+ *                loss runs on many workgroups that leave partial sums there,
+ *                added in a fixed order by a second kernel. With NULL one
+ *                workgroup computes it (no workspace; slower beyond ~8k
+ *                tokens). Calls that share a workspace must be ordered (one
+ *                stream); the library allocates nothing.
  * Errors: INVALID_ARG for a null required pointer, T < 1, V < 1, ld < V,
  * ld_out < V, S < 1, S > T, eps < 0 or NaN, C <= 0 or NaN, an unknown dtype,
- * or a partial overlap of dlogits with logits; HIP when the workspace cannot
- * be allocated or a launch fails. */
+ * a partial overlap of dlogits with logits, or a workspace that is too small
+ * or misaligned; HIP when a launch fails. */
 dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
                                     int64_t ld, const int32_t* target, const float* logp,
                                     const float* lse, const float* logp_old,
@@ -126,7 +131,12 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
                                     const int32_t* step_offsets, int64_t S,
                                     const uint8_t* step_mask, float eps_low, float eps_high,
                                     float C, void* dlogits, int64_t ld_out, double* loss,
-                                    float* tok_coef, float* stats, hipStream_t stream);
+                                    float* tok_coef, float* stats, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace the loss kernels use for T tokens (at most 41,000; 0 for
+ * T < 1 or T > INT32_MAX). Host only. */
+size_t dart_tis_loss_workspace_bytes(int64_t T);
 
 /* The two halves of dart_tis_loss_fwd_bwd, for callers that want the loss
  * without the gradient, or that time the two kernels separately.
@@ -140,7 +150,8 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
                                 const float* logp_rollout, const float* adv,
                                 const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
                                 float eps_low, float eps_high, float C, double* loss,
-                                float* tok_coef, float* stats, hipStream_t stream);
+                                float* tok_coef, float* stats, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream);
 
 dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
                             int64_t ld, const int32_t* target, const float* logp,
@@ -206,14 +217,15 @@ dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t 
  * required when config->kl != DART_KL_NONE, else ignored (may be NULL).
  * stats: [6] float32 or NULL: clip fraction, mean TIS weight, fraction at the
  * cap, N, mean KL, K (over kept tokens / steps). Other arguments and errors as
- * dart_tis_loss_fwd; also INVALID_ARG for a null config, an unknown enum value,
+ * dart_tis_loss_fwd (step-level ratios run on one workgroup and leave the
+ * workspace unused); also INVALID_ARG for a null config, an unknown enum value,
  * or beta < 0 / non-finite. */
 dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* logp_old,
                                    const float* logp_rollout, const float* logp_ref,
                                    const float* adv, const int32_t* step_offsets, int64_t S,
                                    const uint8_t* step_mask, const dart_loss_config_t* config,
-                                   double* loss, float* tok_coef, float* stats,
-                                   hipStream_t stream);
+                                   double* loss, float* tok_coef, float* stats, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
 
 /* dart_tis_grad at inverse temperature inv_temp (the same value given to
  * dart_tok_stats_ex): dlogits = inv_temp * tok_coef * (onehot - softmax(inv_temp z)).

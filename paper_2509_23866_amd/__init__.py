@@ -8,8 +8,9 @@ raises — there is no CPU fallback.
 Functions carry the C names: ``dart_tok_stats``, ``dart_step_select``,
 ``dart_tis_loss_fwd_bwd`` (and its halves ``dart_tis_loss_fwd`` /
 ``dart_tis_grad``), the ``_ex`` variants (inverse temperature, the KL term,
-aggregation and ratio level, zero-row skipping), ``dart_kept_steps`` and
-``dart_status_string``. ``policy_update`` chains the device calls.
+aggregation and ratio level, zero-row skipping), ``dart_tis_loss_workspace_bytes``,
+``dart_kept_steps`` and ``dart_status_string``. ``policy_update`` chains the
+device calls.
 """
 
 from __future__ import annotations
@@ -34,8 +35,8 @@ DART_GRAD_SKIP_ZERO_ROWS = 1
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
-            "dart_grpo_advantage", "dart_step_select_groups", "dart_kept_steps",
-            "dart_status_string")
+            "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
+            "dart_kept_steps", "dart_status_string")
 
 
 class dart_loss_config_t(ctypes.Structure):
@@ -71,10 +72,14 @@ def load_library():
         lib.dart_tis_loss_fwd_bwd.restype = ctypes.c_int
         lib.dart_tis_loss_fwd_bwd.argtypes = [
             _P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P,
-            ctypes.c_float, ctypes.c_float, ctypes.c_float, _P, _I64, _P, _P, _P, _P]
+            ctypes.c_float, ctypes.c_float, ctypes.c_float, _P, _I64, _P, _P, _P, _P,
+            ctypes.c_size_t, _P]
         lib.dart_tis_loss_fwd.restype = ctypes.c_int
         lib.dart_tis_loss_fwd.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, ctypes.c_float,
-                                          ctypes.c_float, ctypes.c_float, _P, _P, _P, _P]
+                                          ctypes.c_float, ctypes.c_float, _P, _P, _P, _P,
+                                          ctypes.c_size_t, _P]
+        lib.dart_tis_loss_workspace_bytes.restype = ctypes.c_size_t
+        lib.dart_tis_loss_workspace_bytes.argtypes = [_I64]
         lib.dart_tis_grad.restype = ctypes.c_int
         lib.dart_tis_grad.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P,
                                       _I64, _P]
@@ -83,7 +88,8 @@ def load_library():
                                           _P, _P, _P, _P]
         lib.dart_tis_loss_fwd_ex.restype = ctypes.c_int
         lib.dart_tis_loss_fwd_ex.argtypes = [_I64, _P, _P, _P, _P, _P, _P, _I64, _P,
-                                             ctypes.POINTER(dart_loss_config_t), _P, _P, _P, _P]
+                                             ctypes.POINTER(dart_loss_config_t), _P, _P, _P, _P,
+                                             ctypes.c_size_t, _P]
         lib.dart_tis_grad_ex.restype = ctypes.c_int
         lib.dart_tis_grad_ex.argtypes = [_P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P,
                                          ctypes.c_float, ctypes.c_uint32, _P, _I64, _P]
@@ -123,6 +129,29 @@ def _stream_handle(stream):
 
 def _ptr(t):
     return None if t is None else t.data_ptr()
+
+
+def dart_tis_loss_workspace_bytes(T: int) -> int:
+    return int(load_library().dart_tis_loss_workspace_bytes(int(T)))
+
+
+def _workspace(workspace, T, device, stream):
+    """(pointer, bytes, tensor) for the loss workspace: "auto" allocates one
+    from torch's caching allocator (kept for the stream the call runs on),
+    None passes NULL (one-workgroup loss), a uint8 tensor is used as given."""
+    torch = _torch()
+    if workspace is None:
+        return None, 0, None
+    if isinstance(workspace, str):
+        if workspace != "auto":
+            raise ValueError('workspace must be "auto", None or a uint8 device tensor')
+        workspace = torch.empty(dart_tis_loss_workspace_bytes(T), dtype=torch.uint8, device=device)
+        if isinstance(stream, torch.cuda.Stream):
+            workspace.record_stream(stream)
+    if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8
+            or workspace.device != device or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
+    return workspace.data_ptr(), workspace.numel(), workspace
 
 
 def _check_vec(name, t, dtype, n, device):
@@ -202,10 +231,12 @@ def dart_step_select(entropy, step_offsets, rho, step_entropy=None, step_mask=No
 
 def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv, step_offsets,
                           step_mask, eps_low, eps_high, C, dlogits=None, loss=None, tok_coef=None,
-                          stats=None, with_stats=True, stream=None):
+                          stats=None, with_stats=True, stream=None, workspace="auto"):
     """Loss (float64 [1]), dlogits (dtype and shape of logits; pass ``dlogits=logits``
     for the in-place gradient), per-token coefficient (float32 [T]) and stats
-    (float32 [4]: clip fraction, mean TIS weight, capped fraction, N)."""
+    (float32 [4]: clip fraction, mean TIS weight, capped fraction, N).
+    ``workspace``: "auto" (allocated here), None (one-workgroup loss, no
+    workspace) or a uint8 device tensor of dart_tis_loss_workspace_bytes(T)."""
     torch = _torch()
     dt, T, V, ld = _logits_meta(logits)
     dev = logits.device
@@ -229,11 +260,12 @@ def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv
     _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
     if stats is not None:
         _check_vec("stats", stats, torch.float32, 4, dev)
+    ws, ws_bytes, _ws = _workspace(workspace, T, dev, stream)
     rc = load_library().dart_tis_loss_fwd_bwd(
         logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
         logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(), step_offsets.data_ptr(), S,
         step_mask.data_ptr(), float(eps_low), float(eps_high), float(C), dlogits.data_ptr(),
-        dlogits.stride(0), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats),
+        dlogits.stride(0), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes,
         _stream_handle(stream))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd_bwd", rc)
@@ -242,9 +274,9 @@ def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv
 
 def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask, eps_low,
                       eps_high, C, loss=None, tok_coef=None, stats=None, with_stats=True,
-                      stream=None):
+                      stream=None, workspace="auto"):
     """Loss (float64 [1]), per-token coefficient (float32 [T]) and stats; the
-    logits are not needed."""
+    logits are not needed. ``workspace`` as for dart_tis_loss_fwd_bwd."""
     torch = _torch()
     dev = logp.device
     T = logp.numel()
@@ -262,10 +294,12 @@ def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask
     _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
     if stats is not None:
         _check_vec("stats", stats, torch.float32, 4, dev)
+    ws, ws_bytes, _ws = _workspace(workspace, T, dev, stream)
     rc = load_library().dart_tis_loss_fwd(
         T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(),
         step_offsets.data_ptr(), S, step_mask.data_ptr(), float(eps_low), float(eps_high),
-        float(C), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), _stream_handle(stream))
+        float(C), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes,
+        _stream_handle(stream))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd", rc)
     return loss, tok_coef, stats
@@ -274,9 +308,10 @@ def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask
 def dart_tis_loss_fwd_ex(logp, logp_old, logp_rollout, adv, step_offsets, step_mask, eps_low,
                          eps_high, C, logp_ref=None, kl="none", beta=0.0, aggregation="token_mean",
                          ratio="token", loss=None, tok_coef=None, stats=None, with_stats=True,
-                         stream=None):
+                         stream=None, workspace="auto"):
     """The loss with the KL term, aggregation and ratio level selectable.
-    Returns (loss float64 [1], tok_coef float32 [T], stats float32 [6])."""
+    Returns (loss float64 [1], tok_coef float32 [T], stats float32 [6]).
+    ``workspace`` as for dart_tis_loss_fwd_bwd."""
     torch = _torch()
     dev = logp.device
     T = logp.numel()
@@ -298,11 +333,12 @@ def dart_tis_loss_fwd_ex(logp, logp_old, logp_rollout, adv, step_offsets, step_m
         _check_vec("stats", stats, torch.float32, 6, dev)
     cfg = dart_loss_config_t(float(eps_low), float(eps_high), float(C), DART_KL[kl], float(beta),
                              DART_AGG[aggregation], DART_RATIO[ratio])
+    ws, ws_bytes, _ws = _workspace(workspace, T, dev, stream)
     rc = load_library().dart_tis_loss_fwd_ex(
         T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(),
         None if DART_KL[kl] == 0 else logp_ref.data_ptr(), adv.data_ptr(),
         step_offsets.data_ptr(), S, step_mask.data_ptr(), ctypes.byref(cfg), loss.data_ptr(),
-        tok_coef.data_ptr(), _ptr(stats), _stream_handle(stream))
+        tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes, _stream_handle(stream))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd_ex", rc)
     return loss, tok_coef, stats

@@ -16,17 +16,15 @@
 //                       loss coefficient; partial sums of the loss in fp64
 //                       (tis_coef_step_kernel: one workgroup, step-level ratios).
 //   tis_loss_finalize_kernel  adds the partial sums in a fixed order.
-//   tis_grad_kernel     one workgroup per row; second streaming pass writing
-//                       coef * (onehot - softmax) in the logits dtype.
+//   tis_grad_kernel     one workgroup per 4 KB chunk of a row; second streaming
+//                       pass writing coef * (onehot - softmax) in the logits dtype.
 // The two streaming kernels are HBM-bound (no matrix contraction anywhere):
-// 16-byte non-temporal loads, 4 (8 in place) loads in flight per lane,
+// 16-byte non-temporal loads and stores, several loads in flight per lane,
 // base-2 exponentials.
 #include <hip/hip_runtime.h>
 #include <hip/hip_bf16.h>
 #include <math.h>
 #include <stdint.h>
-
-#include <mutex>
 
 #include "dart.h"
 
@@ -219,23 +217,25 @@ __device__ __forceinline__ Triple triple_wave_reduce(Triple a) {
     return a;
 }
 
-// Streaming kernels use THREADS threads per row and UNROLL 16-byte vectors per
-// lane per iteration: vector j of the aligned body is read by lane j % THREADS
-// in iteration j / (THREADS * UNROLL), so every wave reads 1 KiB contiguous per
-// load. With PIPE the iteration loop is unrolled twice over two register sets,
-// so the loads of the next iteration are issued before the current one is
-// consumed (2 * UNROLL vectors in flight per lane). NTL / NTS select
-// non-temporal loads / stores. The entry points instantiate the configuration
-// chosen by measurement on MI355X (V = 152064 bf16 rows, 4096 rows): the
-// read-only statistics pass peaks with 12 waves per row (768 threads, ~97% of a
-// plain read kernel); the read+write gradient pass with 16 waves per row (1024
-// threads, 2 rows per CU), which beats a plain copy kernel. Non-temporal loads
-// and stores win in both; register double-buffering does not.
+// The statistics pass uses THREADS threads per row and UNROLL 16-byte vectors
+// per lane per iteration: vector j of the aligned body is read by lane
+// j % THREADS in iteration j / (THREADS * UNROLL), so every wave reads 1 KiB
+// contiguous per load. With PIPE the iteration loop is unrolled twice over two
+// register sets, so the loads of the next iteration are issued before the
+// current one is consumed (2 * UNROLL vectors in flight per lane). NTL / NTS
+// select non-temporal loads / stores. The entry points instantiate the
+// configurations chosen by measurement on MI355X (V = 152064 bf16 rows): the
+// read-only statistics pass peaks with 12 waves per row (768 threads); the
+// read+write gradient pass with one-shot workgroups of 128 threads x 2
+// vectors over 4 KB chunks of a row (best of 32..1024 threads x 1..8 vectors,
+// ~15% faster than one 1024-thread workgroup per row and faster than a plain
+// elementwise copy). Non-temporal loads and stores win in both; register
+// double-buffering does not.
 constexpr int kStatsThreads = 768;
 constexpr int kStatsUnroll = 4;
-constexpr int kGradThreads = 1024;
-constexpr int kGradUnroll = 4;
-constexpr int kGradUnrollInPlace = 8;  // in place: 8 vectors per lane (measured +3% at 46 GB)
+constexpr int kGradThreads = 128;
+constexpr int kGradUnroll = 2;
+constexpr int64_t kGradMaxBlocks = 1ll << 24;
 constexpr bool kPipe = false;
 constexpr bool kNtLoad = true;
 constexpr bool kNtStore = true;
@@ -281,18 +281,14 @@ __device__ __forceinline__ RowLayout row_layout(const void* row, int64_t V) {
 
 // Runs body(v, it) over the full iterations of the aligned body, with the
 // loads of iteration it+1 in flight while iteration it is consumed when PIPE.
-// REV walks the iterations from the end of the row to its start.
-template <int THREADS, int UNROLL, bool PIPE, bool NTL, bool REV = false, class Body>
+template <int THREADS, int UNROLL, bool PIPE, bool NTL, class Body>
 __device__ __forceinline__ void stream_iterations(const u32x4* vrow, int64_t nfull, int tid,
-                                                  Body&& body_fwd) {
+                                                  Body&& body) {
     constexpr int PER_IT = THREADS * UNROLL;
-    auto map = [&](int64_t it) { return REV ? nfull - 1 - it : it; };
     auto load = [&](u32x4* v, int64_t it) {
-        const int64_t i = map(it);
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) v[u] = vload<NTL>(vrow + i * PER_IT + u * THREADS + tid);
+        for (int u = 0; u < UNROLL; ++u) v[u] = vload<NTL>(vrow + it * PER_IT + u * THREADS + tid);
     };
-    auto body = [&](const u32x4* v, int64_t it) { body_fwd(v, map(it)); };
     if constexpr (!PIPE) {
         for (int64_t it = 0; it < nfull; ++it) {
             u32x4 v[UNROLL];
@@ -702,13 +698,15 @@ constexpr int kCoefOneThreads = 1024;  // workgroup of the one-workgroup launch
 constexpr int kCoefBatch = 4;  // tokens per lane whose loads are in flight together
 constexpr int kCoefChunk = kCoefThreads * kCoefBatch;  // tokens per workgroup iteration
 constexpr int kCoefMaxBlocks = 1024;
-// up to this many tokens one workgroup writes the loss itself (no workspace,
-// no second kernel): below it the second launch and the workspace cost more
-// than the extra bandwidth of many workgroups saves
-constexpr int64_t kCoefOneBlockMaxT = 8192;
 constexpr int kCoefLdsSteps = 8192;  // offsets and mask of up to this many steps go to LDS
 constexpr int kStepCoefThreads = 1024;
 constexpr int kStepCoefWaves = kStepCoefThreads / 64;
+
+// workgroups of the many-workgroup launch for T tokens
+__host__ __device__ constexpr int64_t coef_blocks(int64_t T) {
+    return (T + kCoefChunk - 1) / kCoefChunk < kCoefMaxBlocks ? (T + kCoefChunk - 1) / kCoefChunk
+                                                                : kCoefMaxBlocks;
+}
 
 // workspace: kParts doubles per workgroup, then N and K
 __host__ __device__ constexpr int64_t coef_workspace_doubles(int64_t nblocks) {
@@ -1026,105 +1024,89 @@ tis_loss_finalize_kernel(const double* __restrict__ part, int64_t nblocks,
 // K4: dlogits = coef * (onehot(target) - softmax(z))
 // ------------------------------------------------------------------------
 
-template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS, bool REV>
-__device__ __forceinline__ void tis_grad_row(int64_t t, const void* logits, int64_t V, int64_t ld,
-                                             const int32_t* __restrict__ target,
-                                             const float* __restrict__ lse,
-                                             const float* __restrict__ logp,
-                                             const float* __restrict__ coef, float inv_temp,
-                                             uint32_t flags, void* dlogits, int64_t ld_out) {
-    // logits and dlogits may be the same buffer (in place): every element is
-    // read and then written by the same lane, and a lane only reads elements
-    // it has not yet written.
+// dlogits[t, v] = it * g_t * (onehot(y_t)[v] - exp(it * z_tv - lse_t)), it the
+// inverse temperature, written in the logits dtype (bf16 rounded to nearest
+// even). The body of each row is cut into chunks of THREADS * UNROLL 16-byte
+// vectors, and workgroup b takes chunk b % nchunk of row b / nchunk in one
+// shot (every load of the lane in flight before its first store); chunk 0 also
+// takes the row's unaligned head and tail elements. Small one-shot workgroups
+// walking along the rows keep HBM busier than long per-row loops. The target
+// element uses 1 - p_y = -expm1(logp_y), accurate when p_y -> 1. dlogits may
+// be the logits buffer itself (in place): each element is read, then written,
+// by the same lane. With DART_GRAD_SKIP_ZERO_ROWS a row whose coefficient is
+// zero is written without reading the logits.
+template <dart_dtype_t D, int THREADS, int UNROLL, bool NTL, bool NTS>
+__global__ void __launch_bounds__(THREADS)
+tis_grad_kernel(const void* logits, int64_t V, int64_t ld,
+                      const int32_t* __restrict__ target, const float* __restrict__ lse,
+                      const float* __restrict__ logp, const float* __restrict__ coef,
+                      float inv_temp, uint32_t flags, void* dlogits, int64_t ld_out, int64_t T,
+                      int64_t nchunk) {
     using E = typename Elt<D>::T;
     constexpr int EPV = Elt<D>::kPerVec;
-    constexpr int PER_IT = THREADS * UNROLL;
-
+    constexpr int PER = THREADS * UNROLL;
     const int tid = threadIdx.x;
-    const E* row = static_cast<const E*>(logits) + t * ld;
-    E* orow = static_cast<E*>(dlogits) + t * ld_out;
-    const int64_t y_in = target[t];
-    const int64_t y = (y_in >= 0 && y_in < V) ? y_in : -1;
-    // d/dz of a softmax at inverse temperature it: it * g * (onehot - p)
-    const float g = coef[t] * inv_temp;
-    const float neg_g = -g;
-    const float k = inv_temp * kLog2e;
-    const float lb = lse[t] * kLog2e;
-    // 1 - p_y = -expm1(logp_y), accurate when p_y -> 1
-    const float dy = g * -expm1f(logp[t]);
+    const int64_t nblocks = T * nchunk;
+    for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+        const int64_t t = b / nchunk;
+        const int64_t c = b - t * nchunk;
+        const E* row = static_cast<const E*>(logits) + t * ld;
+        E* orow = static_cast<E*>(dlogits) + t * ld_out;
+        const int64_t y_in = target[t];
+        const int64_t y = (y_in >= 0 && y_in < V) ? y_in : -1;
+        const float g = coef[t] * inv_temp;
+        const float neg_g = -g;
+        const float k = inv_temp * kLog2e;
+        const float lb = lse[t] * kLog2e;
+        const float dy = g * -expm1f(logp[t]);
+        RowLayout L = row_layout<D>(row, V);
+        const RowLayout Lo = row_layout<D>(orow, V);
+        if (L.head != Lo.head || !Lo.vector_ok) L = RowLayout{V, 0, V, false};
+        const bool zero_row = (flags & DART_GRAD_SKIP_ZERO_ROWS) && g == 0.f;
 
-    RowLayout L = row_layout<D>(row, V);
-    const RowLayout Lo = row_layout<D>(orow, V);
-    if (L.head != Lo.head || !Lo.vector_ok) L = RowLayout{V, 0, V, false};
-
-    if ((flags & DART_GRAD_SKIP_ZERO_ROWS) && g == 0.f) {
-        // the row's gradient is exactly zero: write it without reading the logits
-        const u32x4 zero = {0u, 0u, 0u, 0u};
-        u32x4* vo = reinterpret_cast<u32x4*>(orow + L.head);
-        for (int64_t j = tid; j < L.nvec; j += THREADS) vstore<NTS>(zero, vo + j);
-        const int64_t ns = L.head + (V - L.body_end);
-        for (int64_t q = tid; q < ns; q += THREADS)
-            store_one<D>(orow, q < L.head ? q : L.body_end + (q - L.head), 0.f);
-        return;
-    }
-    const u32x4* vrow = reinterpret_cast<const u32x4*>(row + L.head);
-    u32x4* vout = reinterpret_cast<u32x4*>(orow + L.head);
-    const int64_t vy = (y >= L.head && y < L.body_end) ? (y - L.head) / EPV : -1;
-    const int64_t it_y = vy >= 0 ? vy / PER_IT : -1;
-    const int64_t nfull = L.nvec / PER_IT;
-
-    stream_iterations<THREADS, UNROLL, PIPE, NTL, REV>(vrow, nfull, tid, [&](const u32x4* v, int64_t it) {
-        float z[UNROLL * EPV];
+        const u32x4* vrow = reinterpret_cast<const u32x4*>(row + L.head);
+        u32x4* vout = reinterpret_cast<u32x4*>(orow + L.head);
+        const int64_t base = c * PER + tid;
+        if (zero_row) {
+            const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) unpack<D>(v[u], z + u * EPV);
+            for (int u = 0; u < UNROLL; ++u) {
+                const int64_t j = base + (int64_t)u * THREADS;
+                if (j < L.nvec) vstore<NTS>(zero, vout + j);
+            }
+        } else {
+            u32x4 v[UNROLL];
 #pragma unroll
-        for (int i = 0; i < UNROLL * EPV; ++i)
-            z[i] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[i], k, -lb));
-        if (it == it_y) {
+            for (int u = 0; u < UNROLL; ++u) {
+                const int64_t j = base + (int64_t)u * THREADS;
+                if (j < L.nvec) v[u] = vload<NTL>(vrow + j);
+            }
 #pragma unroll
-            for (int u = 0; u < UNROLL; ++u)
+            for (int u = 0; u < UNROLL; ++u) {
+                const int64_t j = base + (int64_t)u * THREADS;
+                if (j >= L.nvec) continue;
+                float z[EPV];
+                unpack<D>(v[u], z);
 #pragma unroll
                 for (int e = 0; e < EPV; ++e) {
-                    const int64_t col = L.head + (it * PER_IT + u * THREADS + tid) * EPV + e;
-                    if (col == y) z[u * EPV + e] = dy;
+                    z[e] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[e], k, -lb));
+                    if (L.head + j * EPV + e == y) z[e] = dy;
                 }
+                vstore<NTS>(pack<D>(z), vout + j);
+            }
         }
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
-            vstore<NTS>(pack<D>(z + u * EPV), vout + it * PER_IT + u * THREADS + tid);
-    });
-    for (int64_t j = nfull * PER_IT + tid; j < L.nvec; j += THREADS) {
-        float z[EPV];
-        unpack<D>(vload<NTL>(vrow + j), z);
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) {
-            z[e] = neg_g * __builtin_amdgcn_exp2f(fmaf(z[e], k, -lb));
-            if (L.head + j * EPV + e == y) z[e] = dy;
+        if (c == 0) {
+            const int64_t nscalar = L.head + (V - L.body_end);
+            for (int64_t q = tid; q < nscalar; q += THREADS) {
+                const int64_t col = q < L.head ? q : L.body_end + (q - L.head);
+                float d = 0.f;
+                if (!zero_row) {
+                    const float x = load_one<D>(row, col);
+                    d = col == y ? dy : neg_g * __builtin_amdgcn_exp2f(fmaf(x, k, -lb));
+                }
+                store_one<D>(orow, col, d);
+            }
         }
-        vstore<NTS>(pack<D>(z), vout + j);
-    }
-    const int64_t nscalar = L.head + (V - L.body_end);
-    for (int64_t q = tid; q < nscalar; q += THREADS) {
-        const int64_t col = q < L.head ? q : L.body_end + (q - L.head);
-        const float x = load_one<D>(row, col);
-        const float d = col == y ? dy : neg_g * __builtin_amdgcn_exp2f(fmaf(x, k, -lb));
-        store_one<D>(orow, col, d);
-    }
-}
-
-// One row per workgroup (rows_per_block == 0: grid = T), or a persistent grid
-// in which workgroup b takes rows b, b + gridDim.x, ... .
-template <dart_dtype_t D, int THREADS, int UNROLL, bool PIPE, bool NTL, bool NTS, bool REV = false>
-__global__ void __launch_bounds__(THREADS)
-tis_grad_kernel(const void* logits, int64_t V, int64_t ld, const int32_t* __restrict__ target,
-                const float* __restrict__ lse, const float* __restrict__ logp,
-                const float* __restrict__ coef, float inv_temp, uint32_t flags, void* dlogits,
-                int64_t ld_out, int64_t T) {
-    for (int64_t b = blockIdx.x; b < T; b += gridDim.x) {
-        const int64_t t = REV ? T - 1 - b : b;
-        tis_grad_row<D, THREADS, UNROLL, PIPE, NTL, NTS, REV>(t, logits, V, ld, target, lse, logp,
-                                                              coef, inv_temp, flags, dlogits,
-                                                              ld_out);
     }
 }
 
@@ -1152,59 +1134,21 @@ dart_status_t launch_status() {
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
-// Stream-ordered workspace from a memory pool of the library's own, one per
-// device, created on first use and kept (with its memory: the release
-// threshold is the maximum) until the process ends. Allocation and free are
-// ordered on the caller's stream, so calls on different streams never share
-// a workspace.
-constexpr int kMaxDevices = 64;
-
-hipError_t workspace_alloc(void** ptr, size_t bytes, hipStream_t stream) {
-    int dev = 0;
-    hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-    static std::mutex mu;
-    static hipMemPool_t pools[kMaxDevices] = {};
-    hipMemPool_t pool;
-    {
-        std::lock_guard<std::mutex> lock(mu);
-        if (!pools[dev]) {
-            hipMemPoolProps props = {};
-            props.allocType = hipMemAllocationTypePinned;
-            props.handleTypes = hipMemHandleTypeNone;
-            props.location.type = hipMemLocationTypeDevice;
-            props.location.id = dev;
-            hipMemPool_t created = nullptr;
-            e = hipMemPoolCreate(&created, &props);
-            if (e != hipSuccess) return e;
-            uint64_t keep = UINT64_MAX;
-            e = hipMemPoolSetAttribute(created, hipMemPoolAttrReleaseThreshold, &keep);
-            if (e != hipSuccess) {
-                (void)hipMemPoolDestroy(created);
-                return e;
-            }
-            pools[dev] = created;
-        }
-        pool = pools[dev];
-    }
-    return hipMallocFromPoolAsync(ptr, bytes, pool, stream);
-}
-
-// K3 and the loss reduction for one configuration: token ratios on up to
-// kCoefMaxBlocks workgroups, step ratios on one.
+// K3 and the loss reduction for one configuration: step ratios on one
+// workgroup; token ratios on up to kCoefMaxBlocks workgroups plus the
+// finalize kernel when a workspace is given, else on one workgroup.
 dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const float* lp_old,
                               const float* lp_roll, const float* lp_ref, const float* adv,
                               const int32_t* off, int64_t S, const uint8_t* mask,
                               const LossConfig& cfg, float* coef, double* loss, float* stats,
-                              int nstats, hipStream_t stream) {
+                              int nstats, void* workspace, hipStream_t stream) {
     if (general && cfg.ratio != DART_RATIO_TOKEN) {
         hipLaunchKernelGGL(tis_coef_step_kernel, dim3(1), dim3(kStepCoefThreads), 0, stream, T,
                            logp, lp_old, lp_roll, lp_ref, adv, off, S, mask, cfg, coef, loss,
                            stats, nstats);
         return launch_status();
     }
-    if (T <= kCoefOneBlockMaxT) {
+    if (!workspace) {
         if (general)
             hipLaunchKernelGGL((tis_coef_kernel<true, kCoefOneThreads>), dim3(1),
                                dim3(kCoefOneThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref,
@@ -1215,13 +1159,8 @@ dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const 
                                adv, off, S, mask, cfg, coef, nullptr, loss, stats, nstats);
         return launch_status();
     }
-    const int64_t nchunks = (T + kCoefChunk - 1) / kCoefChunk;
-    const int64_t nblocks = nchunks < kCoefMaxBlocks ? nchunks : kCoefMaxBlocks;
-    double* part = nullptr;
-    if (workspace_alloc(reinterpret_cast<void**>(&part),
-                        (size_t)coef_workspace_doubles(nblocks) * sizeof(double),
-                        stream) != hipSuccess)
-        return DART_ERR_HIP;
+    const int64_t nblocks = coef_blocks(T);
+    double* part = static_cast<double*>(workspace);
     if (general)
         hipLaunchKernelGGL((tis_coef_kernel<true, kCoefThreads>), dim3((unsigned)nblocks),
                            dim3(kCoefThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref, adv,
@@ -1232,9 +1171,14 @@ dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const 
                            off, S, mask, cfg, coef, part, nullptr, nullptr, 0);
     hipLaunchKernelGGL(tis_loss_finalize_kernel, dim3(1), dim3(kCoefThreads), 0, stream, part,
                        nblocks, loss, stats, nstats);
-    dart_status_t st = launch_status();
-    if (hipFreeAsync(part, stream) != hipSuccess) st = DART_ERR_HIP;
-    return st;
+    return launch_status();
+}
+
+// A workspace is either absent or large enough and 8-byte aligned.
+bool bad_workspace(const void* workspace, size_t bytes, int64_t T) {
+    if (!workspace) return false;
+    return bytes < (size_t)coef_workspace_doubles(coef_blocks(T)) * sizeof(double) ||
+           reinterpret_cast<uintptr_t>(workspace) % sizeof(double) != 0;
 }
 
 }  // namespace
@@ -1257,6 +1201,11 @@ int64_t dart_kept_steps(int64_t S, double rho) {
     if (k < 0.0) k = 0.0;
     if (k > (double)S) k = (double)S;
     return (int64_t)k;
+}
+
+size_t dart_tis_loss_workspace_bytes(int64_t T) {
+    if (T < 1 || T > 0x7FFFFFFFll) return 0;
+    return (size_t)coef_workspace_doubles(coef_blocks(T)) * sizeof(double);
 }
 
 dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
@@ -1336,8 +1285,8 @@ dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* lo
                                    const float* logp_rollout, const float* logp_ref,
                                    const float* adv, const int32_t* step_offsets, int64_t S,
                                    const uint8_t* step_mask, const dart_loss_config_t* config,
-                                   double* loss, float* tok_coef, float* stats,
-                                   hipStream_t stream) {
+                                   double* loss, float* tok_coef, float* stats, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
     if (!config) return DART_ERR_INVALID_ARG;
     const dart_loss_config_t& c = *config;
     if (c.kl < DART_KL_NONE || c.kl > DART_KL_K3 || c.aggregation < DART_AGG_TOKEN_MEAN ||
@@ -1351,6 +1300,7 @@ dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* lo
         return DART_ERR_INVALID_ARG;
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     if (!(c.eps_low >= 0.f) || !(c.eps_high >= 0.f) || !(c.C > 0.f)) return DART_ERR_INVALID_ARG;
+    if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
     LossConfig cfg;
     cfg.eps_low = c.eps_low;
     cfg.eps_high = c.eps_high;
@@ -1362,19 +1312,21 @@ dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* lo
     cfg.ratio = c.ratio;
     return launch_tis_coef(true, T, logp, logp_old, logp_rollout,
                            c.kl == DART_KL_NONE ? nullptr : logp_ref, adv, step_offsets, S,
-                           step_mask, cfg, tok_coef, loss, stats, 6, stream);
+                           step_mask, cfg, tok_coef, loss, stats, 6, workspace, stream);
 }
 
 dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_old,
                                 const float* logp_rollout, const float* adv,
                                 const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
                                 float eps_low, float eps_high, float C, double* loss,
-                                float* tok_coef, float* stats, hipStream_t stream) {
+                                float* tok_coef, float* stats, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
     if (!logp || !logp_old || !logp_rollout || !adv || !step_offsets || !step_mask || !loss ||
         !tok_coef)
         return DART_ERR_INVALID_ARG;
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
+    if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
     LossConfig cfg;
     cfg.eps_low = eps_low;
     cfg.eps_high = eps_high;
@@ -1385,7 +1337,7 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
     cfg.agg = DART_AGG_TOKEN_MEAN;
     cfg.ratio = DART_RATIO_TOKEN;
     return launch_tis_coef(false, T, logp, logp_old, logp_rollout, nullptr, adv, step_offsets, S,
-                           step_mask, cfg, tok_coef, loss, stats, 4, stream);
+                           step_mask, cfg, tok_coef, loss, stats, 4, workspace, stream);
 }
 
 dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,
@@ -1401,23 +1353,21 @@ dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T
     if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
         return DART_ERR_INVALID_ARG;
     if (bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
-    const dim3 grid((unsigned)T), block(kGradThreads);
-    const bool in_place = logits == dlogits;
-    if (dtype == DART_BF16 && !in_place)
-        hipLaunchKernelGGL(
-            (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
-            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
-            dlogits, ld_out, T);
-    else if (dtype == DART_BF16)
-        hipLaunchKernelGGL(
-            (tis_grad_kernel<DART_BF16, kGradThreads, kGradUnrollInPlace, kPipe, kNtLoad, kNtStore>),
-            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
-            dlogits, ld_out, T);
+    // chunks of kGradThreads * kGradUnroll vectors per row; a grid of at most
+    // kGradMaxBlocks workgroups strides over the T * nchunk chunks
+    const int64_t per = (int64_t)kGradThreads * kGradUnroll;
+    const int64_t nvec = V / (int64_t)(16 / es);
+    const int64_t nchunk = nvec > 0 ? (nvec + per - 1) / per : 1;
+    const int64_t nblocks = T * nchunk < kGradMaxBlocks ? T * nchunk : kGradMaxBlocks;
+    const dim3 grid((unsigned)nblocks), block(kGradThreads);
+    if (dtype == DART_BF16)
+        hipLaunchKernelGGL((tis_grad_kernel<DART_BF16, kGradThreads, kGradUnroll, kNtLoad, kNtStore>),
+                           grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef,
+                           inv_temp, flags, dlogits, ld_out, T, nchunk);
     else
-        hipLaunchKernelGGL(
-            (tis_grad_kernel<DART_F32, kGradThreads, kGradUnroll, kPipe, kNtLoad, kNtStore>),
-            grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef, inv_temp, flags,
-            dlogits, ld_out, T);
+        hipLaunchKernelGGL((tis_grad_kernel<DART_F32, kGradThreads, kGradUnroll, kNtLoad, kNtStore>),
+                           grid, block, 0, stream, logits, V, ld, target, lse, logp, tok_coef,
+                           inv_temp, flags, dlogits, ld_out, T, nchunk);
     return launch_status();
 }
 
@@ -1436,7 +1386,8 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
                                     const int32_t* step_offsets, int64_t S,
                                     const uint8_t* step_mask, float eps_low, float eps_high,
                                     float C, void* dlogits, int64_t ld_out, double* loss,
-                                    float* tok_coef, float* stats, hipStream_t stream) {
+                                    float* tok_coef, float* stats, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
     // validate both halves before enqueuing either
     if (!logits || !target || !lse || !dlogits) return DART_ERR_INVALID_ARG;
     if (bad_dtype(dtype) || V < 1 || ld < V || ld_out < V) return DART_ERR_INVALID_ARG;
@@ -1446,7 +1397,7 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
     if (T >= 1 && bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
     dart_status_t st = dart_tis_loss_fwd(T, logp, logp_old, logp_rollout, adv, step_offsets, S,
                                          step_mask, eps_low, eps_high, C, loss, tok_coef, stats,
-                                         stream);
+                                         workspace, workspace_bytes, stream);
     if (st != DART_OK) return st;
     return dart_tis_grad(logits, dtype, T, V, ld, target, logp, lse, tok_coef, dlogits, ld_out,
                          stream);

@@ -97,7 +97,7 @@ def test_step_select_rejects(T, S, rho, null):
 def _tis_args(**kw):
     a = dict(logits=P, dtype=1, T=4, V=8, ld=8, target=P, logp=P, lse=P, lp_old=P, lp_roll=P,
              adv=P, off=P, S=2, mask=P, eps_low=0.2, eps_high=0.2, C=2.0, dlogits=1 << 20,
-             ld_out=8, loss=P, coef=P, stats=0)
+             ld_out=8, loss=P, coef=P, stats=0, workspace=0, workspace_bytes=0)
     a.update(kw)
     return list(a.values())
 
@@ -111,10 +111,22 @@ def _tis_args(**kw):
     dict(C=float("nan")), dict(dlogits=P + 2),  # partial overlap with logits
     dict(dlogits=P, ld_out=9),  # same base, different stride
     dict(dlogits=(1 << 20) + 1),  # bf16 output not 2-byte aligned
+    dict(workspace=1 << 24, workspace_bytes=55),  # one byte short for T = 4
+    dict(workspace=(1 << 24) + 4, workspace_bytes=1 << 16),  # not 8-byte aligned
 ])
 def test_tis_loss_rejects(kw):
     lib = dart.load_library()
     assert lib.dart_tis_loss_fwd_bwd(*_tis_args(**kw), None) == dart.DART_ERR_INVALID_ARG
+
+
+def test_workspace_bytes():
+    """kParts = 5 doubles per workgroup of 1024 tokens (at most 1024
+    workgroups), then N and K."""
+    lib = dart.load_library()
+    f = lib.dart_tis_loss_workspace_bytes
+    assert f(0) == 0 and f(-3) == 0 and f(1 << 31) == 0
+    assert f(1) == 56 and f(1024) == 56 and f(1025) == 96
+    assert f(1024 * 1024) == (1024 * 5 + 2) * 8 and f((1 << 31) - 1) == (1024 * 5 + 2) * 8
 
 
 def test_python_binding_requires_built_library(monkeypatch, tmp_path):
@@ -135,11 +147,12 @@ def _loss_ex_args(lib, **kw):
     cfg = d.dart_loss_config_t(0.2, 0.28, 2.0, kw.pop("kl", 0), kw.pop("beta", 0.0),
                                kw.pop("aggregation", 0), kw.pop("ratio", 0))
     a = dict(T=4, logp=P, lp_old=P, lp_roll=P, lp_ref=0, adv=P, off=P, S=2, mask=P, cfg=cfg,
-             loss=P, coef=P, stats=0)
+             loss=P, coef=P, stats=0, workspace=0, workspace_bytes=0)
     a.update(kw)
     cfgp = None if a["cfg"] is None else ctypes.byref(a["cfg"])
     return [a["T"], a["logp"], a["lp_old"], a["lp_roll"], a["lp_ref"], a["adv"], a["off"], a["S"],
-            a["mask"], cfgp, a["loss"], a["coef"], a["stats"], None]
+            a["mask"], cfgp, a["loss"], a["coef"], a["stats"], a["workspace"],
+            a["workspace_bytes"], None]
 
 
 @pytest.mark.skipif("_gpu_visible()")
@@ -147,6 +160,7 @@ def _loss_ex_args(lib, **kw):
     dict(cfg=None), dict(kl=4), dict(kl=-1), dict(aggregation=3), dict(ratio=3),
     dict(kl=3, lp_ref=0), dict(kl=1, lp_ref=P, beta=-0.1), dict(kl=1, lp_ref=P, beta=float("inf")),
     dict(T=0), dict(S=5), dict(logp=0), dict(coef=0),
+    dict(workspace=1 << 24, workspace_bytes=8),
 ])
 def test_tis_loss_fwd_ex_rejects(kw):
     lib = dart.load_library()

@@ -68,8 +68,9 @@ def _check(ref, loss, coef, stats, nstats, exact_zeros=False):
         assert st[5] == ref["stats"][5]
 
 
+@pytest.mark.parametrize("ws", ["auto", None], ids=["workspace", "one_workgroup"])
 @pytest.mark.parametrize("name", [n for n, _ in LAYOUTS])
-def test_default_loss_on_layouts(name):
+def test_default_loss_on_layouts(name, ws):
     import paper_2509_23866_amd as dart
 
     rng = np.random.default_rng(_seed(name))
@@ -80,15 +81,16 @@ def test_default_loss_on_layouts(name):
                           x["off"], x["mask"], eps_low, eps_high, C)
     loss, coef, stats = dart.dart_tis_loss_fwd(
         _cuda(x["logp"]), _cuda(x["lp_old"]), _cuda(x["lp_roll"]), _cuda(x["adv"]),
-        _cuda(x["off"]), _cuda(x["mask"]), eps_low, eps_high, C)
+        _cuda(x["off"]), _cuda(x["mask"]), eps_low, eps_high, C, workspace=ws)
     _check(ref, loss, coef, stats, 4, exact_zeros=True)
 
 
+@pytest.mark.parametrize("ws", ["auto", None], ids=["workspace", "one_workgroup"])
 @pytest.mark.parametrize("name", ["ones_9000", "mixed_8193", "ragged_20000"])
 @pytest.mark.parametrize("kl,agg,ratio", [("k3", "step_mean", "token"),
                                           ("k2", "token_mean_all", "token"),
                                           ("none", "step_mean", "step_geomean")])
-def test_general_loss_on_layouts(name, kl, agg, ratio):
+def test_general_loss_on_layouts(name, kl, agg, ratio, ws):
     import paper_2509_23866_amd as dart
 
     rng = np.random.default_rng(_seed(name, kl, agg, ratio))
@@ -101,8 +103,29 @@ def test_general_loss_on_layouts(name, kl, agg, ratio):
     loss, coef, stats = dart.dart_tis_loss_fwd_ex(
         _cuda(x["logp"]), _cuda(x["lp_old"]), _cuda(x["lp_roll"]), _cuda(x["adv"]),
         _cuda(x["off"]), _cuda(x["mask"]), eps_low, eps_high, C, logp_ref=_cuda(x["lp_ref"]),
-        kl=kl, beta=0.05, aggregation=agg, ratio=ratio)
+        kl=kl, beta=0.05, aggregation=agg, ratio=ratio, workspace=ws)
     _check(ref, loss, coef, stats, 6)
+
+
+@pytest.mark.parametrize("name", ["under_one_wave", "mixed_8193", "ragged_20000"])
+def test_workspace_and_one_workgroup_agree(name):
+    """The two launch shapes compute each coefficient by the same arithmetic
+    (bit-identical) and differ only in the order the loss is summed."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    rng = np.random.default_rng(_seed(name, "paths"))
+    x = _inputs(rng, dict(LAYOUTS)[name](rng))
+    args = [_cuda(x[k]) for k in ("logp", "lp_old", "lp_roll", "adv", "off", "mask")]
+    ws = torch.full((dart.dart_tis_loss_workspace_bytes(x["logp"].size),), 0xA5, dtype=torch.uint8,
+                    device="cuda")  # contents on entry do not matter
+    la, ca, sa = dart.dart_tis_loss_fwd(*args, 0.2, 0.28, 2.0, workspace=ws)
+    lb, cb, sb = dart.dart_tis_loss_fwd(*args, 0.2, 0.28, 2.0, workspace=None)
+    assert np.array_equal(ca.cpu().numpy().view(np.uint32), cb.cpu().numpy().view(np.uint32))
+    assert sa[3].item() == sb[3].item()
+    La, Lb = la.item(), lb.item()
+    assert abs(La - Lb) <= 1e-12 * max(abs(La), 1e-300)
 
 
 @pytest.mark.parametrize("S,rho", [(255, 0.5), (256, 0.3), (257, 0.3), (8192, 0.5),
