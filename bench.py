@@ -191,9 +191,13 @@ def main():
         for i in range(args.steps):
             step()
         e1.record(stream)
+        t_enq = time.perf_counter() - t0
         torch.cuda.synchronize(dev)
         wall = time.perf_counter() - t0
-        ms_per_step = max(e0.elapsed_time(e1), wall * 1e3) / args.steps
+        ev_ms = e0.elapsed_time(e1)
+        ms_per_step = max(ev_ms, wall * 1e3) / args.steps
+        timing = {"events_ms_per_step": ev_ms / args.steps, "wall_ms_per_step": wall * 1e3 / args.steps,
+                  "host_enqueue_ms_per_step": t_enq * 1e3 / args.steps}
     else:
         es = [(ev_new(), ev_new()) for _ in range(args.steps)]
         for i in range(args.steps):
@@ -203,6 +207,7 @@ def main():
             es[i][1].record(stream)
         torch.cuda.synchronize(dev)
         ms_per_step = float(np.mean([a.elapsed_time(b) for a, b in es]))
+        timing = {"events_ms_per_step": ms_per_step}
 
     # ---- kernel durations: K more steps with HIP events around each kernel
     # on the launch stream (the events add idle gaps between kernels, which is
@@ -295,6 +300,7 @@ def main():
                      "algorithmic_bytes_per_launch": grad_bytes},
         "variants": variants,
         "copy_ceiling": copy_ceiling,
+        "timing": timing,
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))

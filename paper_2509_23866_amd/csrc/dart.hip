@@ -26,6 +26,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "dart.h"
 
 namespace {
@@ -411,12 +413,49 @@ tok_stats_kernel(const void* __restrict__ logits, int64_t V, int64_t ld,
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelLdsKeys = 8192;  // groups up to this many steps keep their keys in LDS
+constexpr int kSelLdsTokens = 16384;  // one group of up to this many tokens: means fused in
 constexpr int kSelRankMax = 256;   // groups up to this many steps are ranked directly
 
+// Wave sums in a fixed order on the DPP network (no LDS round trips): pairs
+// (quad_perm 1,0,3,2), quads (quad_perm 2,3,0,1), half-rows (row_half_mirror),
+// rows of 16 (row_mirror), then rows 0+1 and 2+3 (row_bcast15 into rows 1, 3)
+// and all four (row_bcast31 into rows 2, 3); lane 63 holds the total, which
+// every lane receives. The whole wave must be active. A 64-bit value moves as
+// two 32-bit halves under the same control.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, ROW_MASK, 0xf, false);
+    const int hi =
+        __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, ROW_MASK, 0xf, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t lane63_u64(uint64_t x) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+template <class Add>
+__device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t x, Add add) {
+    x = add(x, dpp_u64<0xB1>(x));
+    x = add(x, dpp_u64<0x4E>(x));
+    x = add(x, dpp_u64<0x141>(x));
+    x = add(x, dpp_u64<0x140>(x));
+    x = add(x, dpp_u64<0x142, 0xa>(x));
+    x = add(x, dpp_u64<0x143, 0xc>(x));
+    return lane63_u64(x);
+}
+
 __device__ __forceinline__ double wave_sum(double x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
-    return x;
+    const uint64_t r = wave_reduce_u64(__double_as_longlong(x), [](uint64_t a, uint64_t b) {
+        return (uint64_t)__double_as_longlong(__longlong_as_double(a) + __longlong_as_double(b));
+    });
+    return __longlong_as_double(r);
+}
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t x) {
+    return (int64_t)wave_reduce_u64((uint64_t)x, [](uint64_t a, uint64_t b) { return a + b; });
 }
 
 // Token range of step s, clamped to [0, T] so that malformed offsets (a broken
@@ -463,9 +502,15 @@ __device__ __forceinline__ int64_t kept_steps_dev(int64_t n, double rho) {
 // highest mean entropy (step_H, from step_mean_kernel) among its own, equal
 // means lower step index first: by direct rank in small groups, else by a
 // radix select of the k-th key and a scan over the keys equal to it.
+// FUSED (one group, T <= kSelLdsTokens, S <= kSelLdsKeys): the workgroup first
+// computes the step means itself, from the token entropies and offsets staged
+// in LDS, in the order of step_mean_kernel (so with bit-identical results),
+// and writes them to step_H.
+template <bool FUSED>
 __global__ void __launch_bounds__(kSelThreads)
-step_select_kernel(int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
-                   const float* __restrict__ step_H, uint8_t* __restrict__ mask,
+step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
+                   int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
+                   float* __restrict__ step_H, uint8_t* __restrict__ mask,
                    int32_t* __restrict__ n_kept) {
     __shared__ uint32_t keys[kSelLdsKeys];
     __shared__ uint32_t hist[256];
@@ -476,6 +521,31 @@ step_select_kernel(int64_t S, const int32_t* __restrict__ grp, double rho, int64
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    if constexpr (FUSED) {
+        __shared__ float H_l[kSelLdsTokens];
+        __shared__ int32_t off_l[kSelLdsKeys + 1];
+#pragma unroll 4
+        for (int64_t i = tid; i < T; i += kSelThreads) H_l[i] = H[i];
+        for (int64_t s = tid; s < S; s += kSelThreads) {
+            int64_t b, e;
+            step_bounds(off, s, T, b, e);
+            off_l[s] = (int32_t)b;
+            if (s == S - 1) off_l[S] = (int32_t)e;
+        }
+        __syncthreads();
+        for (int64_t s = wave; s < S; s += kSelWaves) {
+            const int64_t b = off_l[s], e = max((int64_t)off_l[s + 1], b);
+            double sum = 0.0;
+            for (int64_t i = b + lane; i < e; i += 64) sum += (double)H_l[i];
+            sum = wave_sum(sum);
+            const float m = (float)(sum / (double)(e - b));
+            if (lane == 0) {
+                step_H[s] = m;
+                keys[s] = float_key(m);
+            }
+        }
+        __syncthreads();
+    }
     int64_t gs = 0, ge = S, k = k_all;
     if (grp) {
         gs = min(max((int64_t)grp[blockIdx.x], (int64_t)0), S);
@@ -492,7 +562,7 @@ step_select_kernel(int64_t S, const int32_t* __restrict__ grp, double rho, int64
 
     // the group's keys, read once (LDS when they fit)
     const bool staged = Sg <= kSelLdsKeys;
-    if (staged) {
+    if (staged && !FUSED) {
         for (int64_t i = tid; i < Sg; i += kSelThreads) keys[i] = float_key(step_H[gs + i]);
         __syncthreads();
     }
@@ -698,6 +768,9 @@ constexpr int kCoefOneThreads = 1024;  // workgroup of the one-workgroup launch
 constexpr int kCoefBatch = 4;  // tokens per lane whose loads are in flight together
 constexpr int kCoefChunk = kCoefThreads * kCoefBatch;  // tokens per workgroup iteration
 constexpr int kCoefMaxBlocks = 1024;
+// up to this many tokens the one-workgroup launch is used even with a
+// workspace: one launch instead of two (the finalize kernel)
+constexpr int64_t kCoefOneBlockMaxT = 4096;
 constexpr int kCoefLdsSteps = 8192;  // offsets and mask of up to this many steps go to LDS
 constexpr int kStepCoefThreads = 1024;
 constexpr int kStepCoefWaves = kStepCoefThreads / 64;
@@ -759,11 +832,8 @@ __device__ __forceinline__ void count_kept(const int32_t* __restrict__ off,
             k_local += 1;
         }
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        n_local += __shfl_xor(n_local, o);
-        k_local += __shfl_xor(k_local, o);
-    }
+    n_local = wave_sum_i64(n_local);
+    k_local = wave_sum_i64(k_local);
     if (lane == 0) {
         red[0][wave] = n_local;
         red[1][wave] = k_local;
@@ -834,6 +904,27 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
     __shared__ double red_d[kParts][THREADS / 64];
 
     const int tid = threadIdx.x;
+    const bool with_kl = GENERAL && cfg.kl != DART_KL_NONE;
+    const int64_t nchunks = (T + CHUNK - 1) / CHUNK;
+    // the lane's tokens of a chunk: loaded before they are needed (the first
+    // chunk's loads are in flight while the kept counts are taken)
+    float A[kCoefBatch], lp[kCoefBatch], lpo[kCoefBatch], lpr[kCoefBatch], lpf[kCoefBatch];
+    auto load_chunk = [&](int64_t c) {
+#pragma unroll
+        for (int j = 0; j < kCoefBatch; ++j) {
+            const int64_t t = c * CHUNK + tid + (int64_t)j * THREADS;
+            A[j] = lp[j] = lpo[j] = lpr[j] = lpf[j] = 0.f;
+            if (t < T) {
+                A[j] = adv[t];
+                lp[j] = logp[t];
+                lpo[j] = lp_old[t];
+                lpr[j] = lp_roll[t];
+                if (with_kl) lpf[j] = lp_ref[t];
+            }
+        }
+    };
+    if ((int64_t)blockIdx.x < nchunks) load_chunk(blockIdx.x);
+
     const bool staged = S <= kCoefLdsSteps;
     int64_t N, K;
     count_kept<THREADS>(off, mask, S, T, staged ? off_l : nullptr, staged ? mask_l : nullptr,
@@ -845,11 +936,7 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
 
     const double inv_n = N > 0 ? 1.0 / (double)N : 0.0;
     const float lo = 1.f - cfg.eps_low, hi = 1.f + cfg.eps_high;
-    const bool with_kl = GENERAL && cfg.kl != DART_KL_NONE;
     const double beta = (double)cfg.beta;
-    auto off_at = [&](int64_t i) -> int64_t {
-        return staged ? (int64_t)off_l[i] : min(max((int64_t)off[i], (int64_t)0), T);
-    };
     auto weight = [&](int64_t len) -> double {
         if (GENERAL && cfg.agg == DART_AGG_TOKEN_MEAN_ALL) return 1.0 / (double)T;
         if (GENERAL && cfg.agg == DART_AGG_STEP_MEAN) return 1.0 / ((double)K * (double)len);
@@ -863,66 +950,70 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
     }
 
     double acc[kParts] = {0.0, 0.0, 0.0, 0.0, 0.0};
-    const int64_t nchunks = (T + CHUNK - 1) / CHUNK;
-    for (int64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
-        const int64_t base = c * CHUNK + tid;
-        // step of each token: the last s with off[s] <= t, all at once
-        int64_t st[kCoefBatch];
+    // the token loop, compiled twice: offsets and mask in LDS or in global
+    // memory (a run-time choice per access would serialise the probes)
+    auto token_loop = [&](auto staged_tag) {
+        constexpr bool STAGED = decltype(staged_tag)::value;
+        auto off_at = [&](int64_t i) -> int64_t {
+            if constexpr (STAGED)
+                return (int64_t)off_l[i];
+            else
+                return min(max((int64_t)off[i], (int64_t)0), T);
+        };
+        for (int64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
+            if (c != (int64_t)blockIdx.x) load_chunk(c);
+            const int64_t base = c * CHUNK + tid;
+            // step of each token: the last s with off[s] <= t, the lane's tokens
+            // searched together (every probe of a round issued before any is used)
+            int64_t st[kCoefBatch];
 #pragma unroll
-        for (int j = 0; j < kCoefBatch; ++j) st[j] = 0;
-        for (int64_t stride = top; stride > 0; stride >>= 1) {
+            for (int j = 0; j < kCoefBatch; ++j) st[j] = 0;
+            for (int64_t stride = top; stride > 0; stride >>= 1) {
+                int64_t probe[kCoefBatch];
+#pragma unroll
+                for (int j = 0; j < kCoefBatch; ++j) probe[j] = off_at(min(st[j] + stride, S - 1));
+#pragma unroll
+                for (int j = 0; j < kCoefBatch; ++j) {
+                    const int64_t t = base + (int64_t)j * THREADS;
+                    st[j] = (st[j] + stride < S && probe[j] <= t) ? st[j] + stride : st[j];
+                }
+            }
 #pragma unroll
             for (int j = 0; j < kCoefBatch; ++j) {
                 const int64_t t = base + (int64_t)j * THREADS;
-                if (st[j] + stride < S && off_at(st[j] + stride) <= t) st[j] += stride;
+                if (t >= T) break;
+                const bool kept = N > 0 && (STAGED ? mask_l[st[j]] : mask[st[j]]) != 0;
+                if (!kept) {
+                    coef[t] = 0.f;
+                    continue;
+                }
+                const double om = weight(off_at(st[j] + 1) - off_at(st[j]));
+                const float r = expf(lp[j] - lpo[j]);
+                const float d = lpo[j] - lpr[j];
+                const bool capped = d >= cfg.log_C;
+                const float wf = capped ? cfg.C : fminf(expf(d), cfg.C);
+                const float rc = fminf(fmaxf(r, lo), hi);
+                const float u = r * A[j];
+                const float cl = rc * A[j];
+                const bool gate = u <= cl;
+                const double w = (double)wf;
+                const double obj = w * (double)fminf(u, cl);
+                const double dobj = gate ? w * (double)A[j] * (double)r : 0.0;
+                double klv = 0.0, kld = 0.0;
+                if (with_kl) kl_terms(cfg.kl, (double)lpf[j] - (double)lp[j], klv, kld);
+                acc[kPartLoss] -= om * (obj - beta * klv);
+                coef[t] = (float)(-(om * dobj - om * beta * kld));
+                acc[kPartW] += w;
+                acc[kPartClip] += gate ? 0.0 : 1.0;
+                acc[kPartCap] += capped ? 1.0 : 0.0;
+                acc[kPartKl] += klv;
             }
         }
-        bool kept[kCoefBatch];
-        double om[kCoefBatch];
-        float A[kCoefBatch], lp[kCoefBatch], lpo[kCoefBatch], lpr[kCoefBatch], lpf[kCoefBatch];
-#pragma unroll
-        for (int j = 0; j < kCoefBatch; ++j) {
-            const int64_t t = base + (int64_t)j * THREADS;
-            kept[j] = t < T && N > 0 && (staged ? mask_l[st[j]] : mask[st[j]]) != 0;
-            om[j] = kept[j] ? weight(off_at(st[j] + 1) - off_at(st[j])) : 0.0;
-            A[j] = lp[j] = lpo[j] = lpr[j] = lpf[j] = 0.f;
-            if (kept[j]) {
-                A[j] = adv[t];
-                lp[j] = logp[t];
-                lpo[j] = lp_old[t];
-                lpr[j] = lp_roll[t];
-                if (with_kl) lpf[j] = lp_ref[t];
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kCoefBatch; ++j) {
-            const int64_t t = base + (int64_t)j * THREADS;
-            if (t >= T) break;
-            if (!kept[j]) {
-                coef[t] = 0.f;
-                continue;
-            }
-            const float r = expf(lp[j] - lpo[j]);
-            const float d = lpo[j] - lpr[j];
-            const bool capped = d >= cfg.log_C;
-            const float wf = capped ? cfg.C : fminf(expf(d), cfg.C);
-            const float rc = fminf(fmaxf(r, lo), hi);
-            const float u = r * A[j];
-            const float cl = rc * A[j];
-            const bool gate = u <= cl;
-            const double w = (double)wf;
-            const double obj = w * (double)fminf(u, cl);
-            const double dobj = gate ? w * (double)A[j] * (double)r : 0.0;
-            double klv = 0.0, kld = 0.0;
-            if (with_kl) kl_terms(cfg.kl, (double)lpf[j] - (double)lp[j], klv, kld);
-            acc[kPartLoss] -= om[j] * (obj - beta * klv);
-            coef[t] = (float)(-(om[j] * dobj - om[j] * beta * kld));
-            acc[kPartW] += w;
-            acc[kPartClip] += gate ? 0.0 : 1.0;
-            acc[kPartCap] += capped ? 1.0 : 0.0;
-            acc[kPartKl] += klv;
-        }
-    }
+    };
+    if (staged)
+        token_loop(std::true_type{});
+    else
+        token_loop(std::false_type{});
     block_sum_parts<THREADS>(acc, red_d);
     if (tid != 0) return;
     if (part)
@@ -1136,7 +1227,8 @@ dart_status_t launch_status() {
 
 // K3 and the loss reduction for one configuration: step ratios on one
 // workgroup; token ratios on up to kCoefMaxBlocks workgroups plus the
-// finalize kernel when a workspace is given, else on one workgroup.
+// finalize kernel when a workspace is given and T > kCoefOneBlockMaxT, else
+// on one workgroup.
 dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const float* lp_old,
                               const float* lp_roll, const float* lp_ref, const float* adv,
                               const int32_t* off, int64_t S, const uint8_t* mask,
@@ -1148,7 +1240,7 @@ dart_status_t launch_tis_coef(bool general, int64_t T, const float* logp, const 
                            stats, nstats);
         return launch_status();
     }
-    if (!workspace) {
+    if (!workspace || T <= kCoefOneBlockMaxT) {
         if (general)
             hipLaunchKernelGGL((tis_coef_kernel<true, kCoefOneThreads>), dim3(1),
                                dim3(kCoefOneThreads), 0, stream, T, logp, lp_old, lp_roll, lp_ref,
@@ -1241,10 +1333,16 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     const int64_t k = dart_kept_steps(S, rho);
     if (k < 0) return DART_ERR_INVALID_ARG;
+    if (T <= kSelLdsTokens && S <= kSelLdsKeys) {
+        hipLaunchKernelGGL(step_select_kernel<true>, dim3(1), dim3(kSelThreads), 0, stream,
+                           entropy, T, step_offsets, S, nullptr, rho, k, step_entropy, step_mask,
+                           n_kept_steps);
+        return launch_status();
+    }
     hipLaunchKernelGGL(step_mean_kernel, dim3((unsigned)((S + kSelWaves - 1) / kSelWaves)),
                        dim3(kSelThreads), 0, stream, entropy, T, step_offsets, S, step_entropy);
-    hipLaunchKernelGGL(step_select_kernel, dim3(1), dim3(kSelThreads), 0, stream, S, nullptr, rho,
-                       k, step_entropy, step_mask, n_kept_steps);
+    hipLaunchKernelGGL(step_select_kernel<false>, dim3(1), dim3(kSelThreads), 0, stream, entropy,
+                       T, step_offsets, S, nullptr, rho, k, step_entropy, step_mask, n_kept_steps);
     return launch_status();
 }
 
@@ -1260,8 +1358,9 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
     if (dart_kept_steps(S, rho) < 0) return DART_ERR_INVALID_ARG;
     hipLaunchKernelGGL(step_mean_kernel, dim3((unsigned)((S + kSelWaves - 1) / kSelWaves)),
                        dim3(kSelThreads), 0, stream, entropy, T, step_offsets, S, step_entropy);
-    hipLaunchKernelGGL(step_select_kernel, dim3((unsigned)G), dim3(kSelThreads), 0, stream, S,
-                       group_step_offsets, rho, (int64_t)0, step_entropy, step_mask, n_kept_steps);
+    hipLaunchKernelGGL(step_select_kernel<false>, dim3((unsigned)G), dim3(kSelThreads), 0, stream,
+                       entropy, T, step_offsets, S, group_step_offsets, rho, (int64_t)0,
+                       step_entropy, step_mask, n_kept_steps);
     return launch_status();
 }
 
