@@ -273,6 +273,38 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
                                      float* step_entropy, uint8_t* step_mask,
                                      int32_t* n_kept_steps, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * The LM head fused in: statistics without materialised logits
+ * ------------------------------------------------------------------------ */
+
+/* dart_tok_stats for the logits z = h W^T of the LM head, computed tile by tile
+ * on the matrix cores and reduced to the same per-row statistics (Sec. 4.3,
+ * Eq. 1) without writing the [T, V] logits anywhere. h: the final hidden
+ * states of the T tokens, W: the LM-head weight of the policy.
+ *   hidden:     [T, ld_h] bfloat16, row-major (row t = h_t); ld_h >= d.
+ *   weight:     [V, ld_w] bfloat16, row-major (row v = W_v, torch.nn.Linear's
+ *               [out_features, in_features] layout); ld_w >= d.
+ *   d:          hidden size, a multiple of 8; ld_h and ld_w multiples of 8;
+ *               hidden, weight and workspace 16-byte aligned.
+ *   target, logp, entropy, lse: as for dart_tok_stats.
+ *   workspace:  device memory of at least dart_lmhead_stats_workspace_bytes(T, V)
+ *               bytes, owned by the caller (per-row partial statistics of every
+ *               256-column slice of the vocabulary, T * ceil(V/256) * 16 + T * 4
+ *               bytes); contents on entry do not matter.
+ * z is accumulated in fp32 from the bf16 inputs. Errors: INVALID_ARG for a null
+ * pointer, T < 1, V < 1, d < 8, a violated multiple-of-8 or alignment rule, or a
+ * workspace that is too small; UNSUPPORTED when ceil(T/256) * ceil(V/256)
+ * exceeds INT32_MAX; HIP when a launch fails. */
+dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                    const void* weight, int64_t V, int64_t ld_w,
+                                    const int32_t* target, float* logp, float* entropy,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/* Bytes of workspace dart_lmhead_tok_stats needs (0 for T or V outside
+ * [1, INT32_MAX]). Host only. */
+size_t dart_lmhead_stats_workspace_bytes(int64_t T, int64_t V);
+
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
  * number of steps dart_step_select keeps (the guard absorbs the representation
  * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside

@@ -96,7 +96,8 @@ def _c(a, dtype):
 
 
 def _logits_arg(z):
-    """float32 array -> dtype 0; uint16 (bfloat16 bit patterns) -> dtype 1."""
+    """float32 array -> dtype 0; uint16 (bfloat16 bit patterns) -> dtype 1;
+    float64 -> dtype 2."""
     z = np.asarray(z)
     if z.ndim != 2 or z.strides[1] != z.itemsize:
         raise ValueError("logits must be a 2-D array with contiguous rows")
@@ -104,7 +105,9 @@ def _logits_arg(z):
         return z, 0
     if z.dtype == np.uint16:
         return z, 1
-    raise TypeError("logits must be float32 or bfloat16 bit patterns (uint16)")
+    if z.dtype == np.float64:
+        return z, 2
+    raise TypeError("logits must be float32, float64 or bfloat16 bit patterns (uint16)")
 
 
 def token_stats(z, target, nthreads=None, inv_temp=1.0):
@@ -286,6 +289,36 @@ def step_mask_groups(Hs32, group_step_off, rho):
         mask[a:b] = m
         ks.append(k)
     return mask, np.array(ks, np.int64)
+
+
+def bf16_bits_to_f64(bits):
+    """bfloat16 bit patterns (uint16) widened exactly to float64."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def lmhead_logits(h_bits, w_bits):
+    """z = h W^T in float64 from the bf16 hidden states h [T, d] and the LM-head
+    weight W [V, d] (torch.nn.Linear's layout): the logits the LM head produces
+    before any rounding, as one library matrix product of the exact inputs."""
+    return np.ascontiguousarray(bf16_bits_to_f64(h_bits) @ bf16_bits_to_f64(w_bits).T)
+
+
+def lmhead_token_stats(h_bits, w_bits, target, nthreads=None):
+    """(logp, H, lse) of softmax(h W^T) per row, in float64 (Sec. 4.3, Eq. 1 on
+    the logits of the LM head)."""
+    return token_stats(lmhead_logits(h_bits, w_bits), target, nthreads=nthreads)
+
+
+def lmhead_grads(h_bits, w_bits, target, lse, logp, g, nthreads=None):
+    """Gradients of the loss through the LM head, given the per-token
+    coefficient g = dL/dlogp: dz = g (onehot - p) [T, V] (the logits gradient),
+    dh = dz W [T, d] and dW = dz^T h [V, d], all in float64."""
+    z = lmhead_logits(h_bits, w_bits)
+    dz = dlogits(z, target, lse, logp, g, nthreads=nthreads)
+    h = bf16_bits_to_f64(h_bits)
+    w = bf16_bits_to_f64(w_bits)
+    return dz, dz @ w, dz.T @ h
 
 
 def f64_to_bf16_bits(x):

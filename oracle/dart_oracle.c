@@ -47,9 +47,11 @@ static inline void ksum_add(ksum_t* k, double x) {
 static inline double ksum_value(const ksum_t* k) { return k->sum + k->comp; }
 
 /* Logit element (t, v) widened exactly to double. dtype 0 = float32,
- * dtype 1 = bfloat16 stored as its 16-bit pattern. */
+ * dtype 1 = bfloat16 stored as its 16-bit pattern, dtype 2 = float64 (logits
+ * the oracle formed itself, e.g. from an LM head in double). */
 static double logit_at(const void* z, int dtype, int64_t ld, int64_t t, int64_t v) {
     if (dtype == 0) return (double)((const float*)z)[t * ld + v];
+    if (dtype == 2) return ((const double*)z)[t * ld + v];
     uint32_t bits = (uint32_t)((const uint16_t*)z)[t * ld + v] << 16;
     float f;
     memcpy(&f, &bits, 4);

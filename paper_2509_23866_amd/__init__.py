@@ -36,7 +36,8 @@ DART_GRAD_SKIP_ZERO_ROWS = 1
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
-            "dart_kept_steps", "dart_status_string")
+            "dart_lmhead_tok_stats", "dart_lmhead_stats_workspace_bytes", "dart_kept_steps",
+            "dart_status_string")
 
 
 class dart_loss_config_t(ctypes.Structure):
@@ -98,6 +99,11 @@ def load_library():
         lib.dart_step_select_groups.restype = ctypes.c_int
         lib.dart_step_select_groups.argtypes = [_P, _I64, _P, _I64, _P, _I64, ctypes.c_double, _P,
                                                 _P, _P, _P]
+        lib.dart_lmhead_tok_stats.restype = ctypes.c_int
+        lib.dart_lmhead_tok_stats.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
+                                              _P, ctypes.c_size_t, _P]
+        lib.dart_lmhead_stats_workspace_bytes.restype = ctypes.c_size_t
+        lib.dart_lmhead_stats_workspace_bytes.argtypes = [_I64, _I64]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
         lib.dart_status_string.restype = ctypes.c_char_p
@@ -425,6 +431,60 @@ def dart_step_select_groups(entropy, step_offsets, group_step_offsets, rho, step
     if rc != DART_OK:
         raise DartError("dart_step_select_groups", rc)
     return step_entropy, step_mask, n_kept_steps
+
+
+def dart_lmhead_stats_workspace_bytes(T: int, V: int) -> int:
+    return int(load_library().dart_lmhead_stats_workspace_bytes(int(T), int(V)))
+
+
+def _matrix_bf16(name, t, device=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.bfloat16 or t.dim() != 2:
+        raise TypeError(f"{name} must be a 2-D bfloat16 tensor")
+    if t.stride(1) != 1 or t.stride(0) % 8 or t.data_ptr() % 16 or not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU with contiguous rows, a row stride that is a "
+                         "multiple of 8 and a 16-byte aligned base")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} must be on {device}")
+
+
+def dart_lmhead_tok_stats(hidden, weight, target, logp=None, entropy=None, lse=None,
+                          workspace="auto", stream=None):
+    """(logp, entropy, lse) float32 [T] of softmax(hidden @ weight^T) without
+    materialising the logits: hidden [T, d] and weight [V, d] bfloat16 (d a
+    multiple of 8). ``workspace``: "auto" (allocated here) or a uint8 device
+    tensor of dart_lmhead_stats_workspace_bytes(T, V) bytes."""
+    torch = _torch()
+    _matrix_bf16("hidden", hidden)
+    dev = hidden.device
+    _matrix_bf16("weight", weight, dev)
+    T, d = hidden.shape
+    V = weight.shape[0]
+    if weight.shape[1] != d:
+        raise ValueError("hidden and weight must have the same inner size d")
+    _check_vec("target", target, torch.int32, T, dev)
+    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
+    entropy = torch.empty(T, dtype=torch.float32, device=dev) if entropy is None else entropy
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    for n, v in (("logp", logp), ("entropy", entropy), ("lse", lse)):
+        _check_vec(n, v, torch.float32, T, dev)
+    if isinstance(workspace, str):
+        if workspace != "auto":
+            raise ValueError('workspace must be "auto" or a uint8 device tensor')
+        workspace = torch.empty(dart_lmhead_stats_workspace_bytes(T, V), dtype=torch.uint8,
+                                device=dev)
+        if isinstance(stream, torch.cuda.Stream):
+            workspace.record_stream(stream)
+    if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8
+            or workspace.device != dev or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
+    rc = load_library().dart_lmhead_tok_stats(
+        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+        target.data_ptr(), logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
+        workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_lmhead_tok_stats", rc)
+    return logp, entropy, lse
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

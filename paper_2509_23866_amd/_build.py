@@ -7,7 +7,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "dart.hip")
+SRCS = [os.path.join(HERE, "csrc", "dart.hip"), os.path.join(HERE, "csrc", "lmhead.hip")]
 LIB = os.path.join(HERE, "libdart.so")
 INCLUDE = os.path.join(ROOT, "include")
 
@@ -19,7 +19,7 @@ HIPCC_FLAGS = [
 
 
 def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
-    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, SRC, "-o", out]
+    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, *SRCS, "-o", out]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

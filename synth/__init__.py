@@ -28,4 +28,8 @@ from .gen import (  # noqa: F401
     reference_logprobs,
     bf16_bits_to_f32,
     f32_to_bf16_bits,
+    gaussian_bits,
+    lmhead_problem,
+    lmhead_custom,
+    LmHeadProblem,
 )

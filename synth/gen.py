@@ -55,6 +55,8 @@ STREAM_OLD = 5
 STREAM_ROLL = 6
 STREAM_ROWTYPE = 7
 STREAM_REF = 8
+STREAM_HIDDEN = 9   # LM-head inputs: hidden states h [T, d]
+STREAM_WEIGHT = 10  # LM-head weight W [V, d]
 
 KIND_GAUSS = 0
 KIND_FLAT = 1
@@ -98,6 +100,23 @@ def counter_hash(seed: int, stream: int, row, col) -> np.ndarray:
 
 def draw_normal(seed: int, stream: int, row, col) -> np.ndarray:
     return normal_table()[(counter_hash(seed, stream, row, col) >> _U64(48)).astype(np.int64)]
+
+
+def stream_key(seed: int, stream: int) -> int:
+    """The key whose XOR with (row << 28 | col) addresses stream ``stream``:
+    counter_hash(seed, stream, row, col) == splitmix64(stream_key ^ (row << 28 | col))."""
+    return base_key(seed) ^ (stream << 56)
+
+
+def gaussian_bits(seed: int, stream: int, rows: int, cols: int, sigma: float,
+                  row0: int = 0) -> np.ndarray:
+    """bf16 bit patterns [rows, cols] of the matrix whose element (r, c) is
+    sigma * Q[hash(seed, stream, row0 + r, c) >> 48] in double, rounded to
+    float32 and then to bf16 (nearest even): the LM-head inputs."""
+    r = np.arange(row0, row0 + rows, dtype=np.uint64)[:, None]
+    c = np.arange(cols, dtype=np.uint64)[None, :]
+    vals = sigma * draw_normal(seed, stream, r, c)
+    return f32_to_bf16_bits(vals.astype(np.float32))
 
 
 def draw_uniform(seed: int, stream: int, row, col) -> np.ndarray:
@@ -317,6 +336,44 @@ def _edge():
         description="T=16384 in 256 steps of 64, V=151936 bf16; Gaussian, flat and "
                     "near-one-hot rows, exact-tie step blocks, ratios U(0.5,1.5), "
                     "lp_old-lp_roll U(-3,3)")
+
+
+class LmHeadProblem:
+    """An LM-head workload: the step structure, targets, advantages and
+    log-prob offsets of a logits workload, with the logits replaced by
+    h W^T: h [T, d] ~ N(0, sigma_h^2), W [V, d] ~ N(0, sigma_w^2), bf16, so
+    that z ~ N(0, d sigma_h^2 sigma_w^2)."""
+
+    def __init__(self, wl: "Workload", d: int, sigma_h: float, sigma_w: float, description: str):
+        self.wl, self.d, self.sigma_h, self.sigma_w = wl, d, sigma_h, sigma_w
+        self.name = "lmhead_" + wl.name
+        self.description = description
+
+    def hidden_bits(self, rows=None):
+        wl = self.wl
+        if rows is None:
+            return gaussian_bits(wl.seed, STREAM_HIDDEN, wl.T, self.d, self.sigma_h)
+        return np.concatenate([gaussian_bits(wl.seed, STREAM_HIDDEN, 1, self.d, self.sigma_h, int(r))
+                               for r in rows]) if len(rows) else np.zeros((0, self.d), np.uint16)
+
+    def weight_bits(self):
+        return gaussian_bits(self.wl.seed, STREAM_WEIGHT, self.wl.V, self.d, self.sigma_w)
+
+
+def lmhead_problem(name: str, d: int | None = None) -> LmHeadProblem:
+    """The LM-head version of a named logits workload: d = 3584 (the 7B VLM's
+    hidden size) unless given; sigma_h = 1, sigma_w = 3 / sqrt(d) so that the
+    logits have the N(0, 3^2) spread of the logits workloads."""
+    wl = make_workload(name)
+    d = 3584 if d is None else d
+    return LmHeadProblem(wl, d, 1.0, 3.0 / math.sqrt(d),
+                         f"h [T={wl.T}, d={d}] N(0,1), W [V={wl.V}, d] N(0, 9/d), bf16; "
+                         f"steps, targets and advantages of {wl.name}")
+
+
+def lmhead_custom(lens, V, d, seed, **kw) -> LmHeadProblem:
+    wl = custom_workload(lens=lens, V=V, dtype="bf16", seed=seed, **kw)
+    return LmHeadProblem(wl, d, 1.0, 3.0 / math.sqrt(d), f"custom T={wl.T}, d={d}, V={V}")
 
 
 WORKLOADS = {

@@ -80,6 +80,25 @@ def logits_rows_host(wl: gen.Workload, rows, out: np.ndarray | None = None, nthr
     return out
 
 
+def gaussian_bits_host(seed: int, stream_id: int, rows: int, cols: int, sigma: float,
+                       nthreads: int | None = None) -> np.ndarray:
+    """gen.gaussian_bits (bit-exact) via the C twin, for matrices too large for
+    numpy's temporaries (the 152064 x 3584 LM-head weight)."""
+    lib = _load_host()
+    out = np.empty((rows, cols), dtype=np.uint16)
+    idx = np.arange(rows, dtype=np.int64)
+    kind = np.zeros(rows, np.int32)
+    src_row = np.arange(rows, dtype=np.int32)
+    spike_col = np.full(rows, -1, np.int32)
+    spike_val = np.zeros(rows, np.float64)
+    q = gen.normal_table()
+    lib.synth_logits_host(out.ctypes.data, 1, rows, idx.ctypes.data, cols, cols,
+                          gen.stream_key(seed, stream_id), float(sigma), kind.ctypes.data,
+                          src_row.ctypes.data, spike_col.ctypes.data, spike_val.ctypes.data,
+                          q.ctypes.data, nthreads or default_threads())
+    return out
+
+
 def _load_dev():
     global _dev
     if _dev is None:
@@ -107,6 +126,31 @@ class DeviceRecipe:
         self.spike_col = torch.from_numpy(wl.spike_col).to(device)
         self.spike_val = torch.from_numpy(wl.spike_val).to(device)
         self.Q = torch.from_numpy(np.array(gen.normal_table())).to(device)
+
+
+def fill_gaussian_device(out, seed: int, stream_id: int, sigma: float, stream=None) -> None:
+    """Fill the bf16 device tensor ``out`` [rows, cols] with gen.gaussian_bits
+    (seed, stream_id, rows, cols, sigma), bit for bit, with the logits kernel:
+    every row Gaussian, no spike, the stream folded into the key."""
+    import torch
+
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be a 2-D bfloat16 tensor with contiguous rows")
+    rows, cols = out.shape
+    dev = out.device
+    kind = torch.zeros(rows, dtype=torch.int32, device=dev)
+    src_row = torch.arange(rows, dtype=torch.int32, device=dev)
+    spike_col = torch.full((rows,), -1, dtype=torch.int32, device=dev)
+    spike_val = torch.zeros(rows, dtype=torch.float64, device=dev)
+    Q = torch.from_numpy(np.array(gen.normal_table())).to(dev)
+    if stream is None:
+        stream = torch.cuda.current_stream().cuda_stream
+    rc = _load_dev().synth_logits_device(
+        out.data_ptr(), 1, rows, cols, out.stride(0), gen.stream_key(seed, stream_id), float(sigma),
+        kind.data_ptr(), src_row.data_ptr(), spike_col.data_ptr(), spike_val.data_ptr(),
+        Q.data_ptr(), stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_logits_device failed with code {rc}")
 
 
 def fill_logits_device(recipe: DeviceRecipe, out, stream=None) -> None:

@@ -198,3 +198,31 @@ def test_step_select_groups_rejects(kw):
     a.update(kw)
     assert lib.dart_step_select_groups(a["entropy"], a["T"], a["off"], a["S"], a["grp"], a["G"],
                                        a["rho"], a["sh"], a["mask"], None, None) == dart.DART_ERR_INVALID_ARG
+
+
+def _lm_args(**kw):
+    a = dict(hidden=1 << 20, T=4, d=16, ld_h=16, weight=1 << 21, V=300, ld_w=16, target=P,
+             logp=P, H=P, lse=P, workspace=1 << 22, ws_bytes=1 << 20)
+    a.update(kw)
+    return list(a.values()) + [None]
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(hidden=0), dict(weight=0), dict(target=0), dict(logp=0), dict(H=0), dict(lse=0),
+    dict(workspace=0), dict(T=0), dict(V=0), dict(d=4, ld_h=4, ld_w=4), dict(d=12, ld_h=16, ld_w=16),
+    dict(ld_h=12), dict(ld_w=20), dict(ld_h=8), dict(hidden=(1 << 20) + 8),
+    dict(weight=(1 << 21) + 2), dict(workspace=(1 << 22) + 4), dict(ws_bytes=4 * 2 * 16 + 15),
+])
+def test_lmhead_stats_rejects(kw):
+    lib = dart.load_library()
+    assert lib.dart_lmhead_tok_stats(*_lm_args(**kw)) == dart.DART_ERR_INVALID_ARG
+
+
+def test_lmhead_workspace_bytes():
+    """One 16-byte partial triple per row and 256-column slice, plus the
+    target logit per row."""
+    f = dart.load_library().dart_lmhead_stats_workspace_bytes
+    assert f(0, 10) == 0 and f(10, 0) == 0 and f(1 << 31, 5) == 0
+    assert f(4, 300) == 4 * 2 * 16 + 16
+    assert f(4096, 152064) == 4096 * 594 * 16 + 4096 * 4

@@ -100,3 +100,15 @@ def test_perturbation_model_std():
     lp_old, lp_roll = synth.perturbed_logprobs(w, np.full(w.T, -3.0))
     assert lp_old.dtype == np.float32 and lp_roll.dtype == np.float32
     assert np.allclose(lp_old, -3.0 + w.old_offset, atol=1e-6)
+
+
+def test_gaussian_matrix_twins():
+    """The LM-head inputs: numpy definition and the C twin agree bit for bit;
+    rows generated from an offset equal the same rows of the whole matrix."""
+    import synth.native as sn
+
+    a = synth.gaussian_bits(7, synth.gen.STREAM_WEIGHT, 53, 40, 0.3)
+    assert np.array_equal(a, sn.gaussian_bits_host(7, synth.gen.STREAM_WEIGHT, 53, 40, 0.3))
+    assert np.array_equal(a[17:20], synth.gaussian_bits(7, synth.gen.STREAM_WEIGHT, 3, 40, 0.3, row0=17))
+    vals = synth.bf16_bits_to_f32(synth.gaussian_bits(1, synth.gen.STREAM_HIDDEN, 200, 256, 1.0))
+    assert abs(vals.std() - 1.0) < 0.02 and abs(vals.mean()) < 0.02
