@@ -305,6 +305,64 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
  * [1, INT32_MAX]). Host only. */
 size_t dart_lmhead_stats_workspace_bytes(int64_t T, int64_t V);
 
+/* The gradient pass of the fused head, part one: dlogits of the logits
+ * z = h W^T, recomputed tile by tile on the matrix cores exactly as
+ * dart_lmhead_tok_stats forms them, then
+ *   dlogits[t, v] = tok_coef[t] * (onehot(target[t])[v] - exp(z_tv - lse[t]))
+ * (the chain rule through Eq. 1's log-softmax; the target element is
+ * tok_coef[t] * -expm1(logp[t]), accurate when p_y is near 1), written in
+ * bfloat16 (round to nearest even).
+ *   hidden, weight, d, ld_h, ld_w, target: as for dart_lmhead_tok_stats.
+ *   lse, logp:  [T] float32, the outputs of dart_lmhead_tok_stats for these rows.
+ *   tok_coef:   [T] float32, dloss/dlogp_t from a loss forward (dart_tis_loss_fwd
+ *               or dart_tis_loss_fwd_ex).
+ *   dlogits:    [T, ld_out] bfloat16 output, row-major; ld_out >= V and a
+ *               multiple of 8; 16-byte aligned. Columns [V, ld_out) are not
+ *               written.
+ * Errors: as for dart_lmhead_tok_stats (INVALID_ARG also for a bad ld_out or
+ * dlogits alignment). */
+dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                  const void* weight, int64_t V, int64_t ld_w,
+                                  const int32_t* target, const float* lse, const float* logp,
+                                  const float* tok_coef, void* dlogits, int64_t ld_out,
+                                  hipStream_t stream);
+
+/* The gradient pass of the fused head, whole: the gradients of the loss with
+ * respect to the hidden states and the LM-head weight,
+ *   dhidden = dlogits W        [T, d]
+ *   dweight = dlogits^T h      [V, d]
+ * with dlogits as dart_lmhead_dlogits defines it. The rows are taken
+ * chunk_rows at a time: the chunk's dlogits go to the workspace in bfloat16,
+ * then two GEMMs of the ROCm BLAS library (bf16 inputs, fp32 accumulation and
+ * output) form the chunk's rows of dhidden and add its share to dweight, so the
+ * [T, V] dlogits never exist whole.
+ *   dhidden:    [T, ld_dh] float32 output, row-major; ld_dh >= d.
+ *   dweight:    [V, ld_dw] float32 output, row-major; ld_dw >= d; overwritten
+ *               (not accumulated into).
+ *   chunk_rows: rows per chunk, >= 1 (values above T are taken as T).
+ *   workspace:  device memory of at least
+ *               dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
+ *               bytes, 16-byte aligned, owned by the caller; contents on entry
+ *               do not matter.
+ * The first call on a device creates that device's BLAS handle (the library
+ * allocates its own memory then); the handle lives until the process ends and
+ * calls into this function are serialised on it. Errors: as for
+ * dart_lmhead_dlogits, INVALID_ARG also for a null output, bad ld_dh/ld_dw,
+ * chunk_rows < 1 or a workspace that is too small; UNSUPPORTED for a leading
+ * dimension above INT32_MAX (the BLAS library's limit); HIP when the BLAS
+ * library reports an error. */
+dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                   const void* weight, int64_t V, int64_t ld_w,
+                                   const int32_t* target, const float* lse, const float* logp,
+                                   const float* tok_coef, float* dhidden, int64_t ld_dh,
+                                   float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace dart_lmhead_backward needs for chunks of chunk_rows rows:
+ * chunk_rows * ceil8(V) * 2 (0 for arguments outside [1, INT32_MAX]). Host
+ * only. */
+size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V);
+
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
  * number of steps dart_step_select keeps (the guard absorbs the representation
  * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside

@@ -36,7 +36,8 @@ DART_GRAD_SKIP_ZERO_ROWS = 1
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
-            "dart_lmhead_tok_stats", "dart_lmhead_stats_workspace_bytes", "dart_kept_steps",
+            "dart_lmhead_tok_stats", "dart_lmhead_stats_workspace_bytes", "dart_lmhead_dlogits",
+            "dart_lmhead_backward", "dart_lmhead_backward_workspace_bytes", "dart_kept_steps",
             "dart_status_string")
 
 
@@ -104,6 +105,14 @@ def load_library():
                                               _P, ctypes.c_size_t, _P]
         lib.dart_lmhead_stats_workspace_bytes.restype = ctypes.c_size_t
         lib.dart_lmhead_stats_workspace_bytes.argtypes = [_I64, _I64]
+        lib.dart_lmhead_dlogits.restype = ctypes.c_int
+        lib.dart_lmhead_dlogits.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
+                                            _P, _I64, _P]
+        lib.dart_lmhead_backward.restype = ctypes.c_int
+        lib.dart_lmhead_backward.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
+                                             _P, _I64, _P, _I64, _I64, _P, ctypes.c_size_t, _P]
+        lib.dart_lmhead_backward_workspace_bytes.restype = ctypes.c_size_t
+        lib.dart_lmhead_backward_workspace_bytes.argtypes = [_I64, _I64]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
         lib.dart_status_string.restype = ctypes.c_char_p
@@ -485,6 +494,78 @@ def dart_lmhead_tok_stats(hidden, weight, target, logp=None, entropy=None, lse=N
     if rc != DART_OK:
         raise DartError("dart_lmhead_tok_stats", rc)
     return logp, entropy, lse
+
+
+def dart_lmhead_backward_workspace_bytes(chunk_rows: int, V: int) -> int:
+    return int(load_library().dart_lmhead_backward_workspace_bytes(int(chunk_rows), int(V)))
+
+
+def _lmhead_common(hidden, weight, target, lse, logp, tok_coef):
+    torch = _torch()
+    _matrix_bf16("hidden", hidden)
+    dev = hidden.device
+    _matrix_bf16("weight", weight, dev)
+    T, d = hidden.shape
+    if weight.shape[1] != d:
+        raise ValueError("hidden and weight must have the same inner size d")
+    _check_vec("target", target, torch.int32, T, dev)
+    for n, v in (("lse", lse), ("logp", logp), ("tok_coef", tok_coef)):
+        _check_vec(n, v, torch.float32, T, dev)
+    return dev, T, d, weight.shape[0]
+
+
+def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=None, stream=None):
+    """bfloat16 [T, V] dlogits = tok_coef (onehot - softmax(hidden @ weight^T)), the
+    logits recomputed on the matrix cores; lse and logp from dart_lmhead_tok_stats."""
+    torch = _torch()
+    dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
+    if dlogits is None:
+        dlogits = torch.empty((T, V), dtype=torch.bfloat16, device=dev)
+    _matrix_bf16("dlogits", dlogits, dev)
+    if tuple(dlogits.shape) != (T, V):
+        raise ValueError(f"dlogits must have shape ({T}, {V})")
+    rc = load_library().dart_lmhead_dlogits(
+        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+        target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
+        dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_lmhead_dlogits", rc)
+    return dlogits
+
+
+def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows=1024,
+                         dhidden=None, dweight=None, workspace="auto", stream=None):
+    """(dhidden float32 [T, d], dweight float32 [V, d]) of the loss through the LM
+    head, dlogits formed chunk_rows rows at a time in ``workspace`` ("auto" or a
+    uint8 device tensor of dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
+    bytes)."""
+    torch = _torch()
+    dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
+    chunk_rows = max(1, min(int(chunk_rows), T))
+    dhidden = torch.empty((T, d), dtype=torch.float32, device=dev) if dhidden is None else dhidden
+    dweight = torch.empty((V, d), dtype=torch.float32, device=dev) if dweight is None else dweight
+    for n, m, shape in (("dhidden", dhidden, (T, d)), ("dweight", dweight, (V, d))):
+        if (not isinstance(m, torch.Tensor) or m.dtype != torch.float32 or m.device != dev
+                or tuple(m.shape) != shape or m.stride(1) != 1):
+            raise ValueError(f"{n} must be a float32 {shape} tensor on {dev} with contiguous rows")
+    if isinstance(workspace, str):
+        if workspace != "auto":
+            raise ValueError('workspace must be "auto" or a uint8 device tensor')
+        workspace = torch.empty(dart_lmhead_backward_workspace_bytes(chunk_rows, V),
+                                dtype=torch.uint8, device=dev)
+        if isinstance(stream, torch.cuda.Stream):
+            workspace.record_stream(stream)
+    if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8
+            or workspace.device != dev or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
+    rc = load_library().dart_lmhead_backward(
+        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+        target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
+        dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0), chunk_rows,
+        workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    if rc != DART_OK:
+        raise DartError("dart_lmhead_backward", rc)
+    return dhidden, dweight
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

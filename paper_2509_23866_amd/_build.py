@@ -19,7 +19,8 @@ HIPCC_FLAGS = [
 
 
 def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
-    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, *SRCS, "-o", out]
+    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, *SRCS, "-o", out,
+           "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -18,7 +18,10 @@
 //                        and lse exactly as tok_stats_kernel defines them.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <rocblas/rocblas.h>
 #include <stdint.h>
+
+#include <mutex>
 
 #include "dart.h"
 
@@ -85,6 +88,18 @@ struct Triple {
     float m, s, w;  // reference, sum of e^{z-m}, sum of e^{z-m} (z-m), natural units
 };
 
+// float -> bf16 bits, round to nearest even (NaN kept a quiet NaN)
+__device__ __forceinline__ uint16_t bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)bf16_bits(lo) | ((uint32_t)bf16_bits(hi) << 16);
+}
+
 // Exact merge of two partial triples; an empty triple has s == 0.
 __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
     if (b.s == 0.f) return a;
@@ -111,6 +126,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
                                           int64_t K, int64_t m0, int64_t n0,
                                           typename C::Smem& sm,
                                           f32x16 (&acc)[C::TM][C::TN]) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the gfx950 builtins below have no host form
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = (wave / C::WN) * (C::BM / C::WM), wc = (wave % C::WN) * (C::BN / C::WN);
 #pragma unroll
@@ -205,6 +221,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
         }
     }
     __syncthreads();
+#endif
 }
 
 // Logical tile of workgroup b: the hardware places workgroup b on XCD b % 8,
@@ -288,6 +305,71 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
     }
 }
 
+// dlogits = g_t (onehot(y_t) - exp(z - lse_t)) for rows [0, M) of the chunk
+// (h and out already offset to the chunk's first row), written in bf16
+// (nearest even) to out [M, ld_out]: the gradient pass of the logits path
+// with the logits formed on the fly. The target element is
+// g_t * -expm1(logp_t), accurate when p_y -> 1. The fp32 tile is staged
+// through LDS so that each row leaves as 16-byte vectors.
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
+                      const uint16_t* __restrict__ w, int64_t V, int64_t ldw, int64_t d,
+                      const int32_t* __restrict__ target, const float* __restrict__ lse,
+                      const float* __restrict__ logp, const float* __restrict__ coef,
+                      uint16_t* __restrict__ out, int64_t ld_out, int64_t nmt, int64_t nvt) {
+    __shared__ typename C::Smem sm;
+    int64_t mt, vt;
+    tile_of_block(nmt, nvt, mt, vt);
+    const int64_t m0 = mt * C::BM, n0 = vt * C::BN;
+    f32x16 acc[C::TM][C::TN];
+    gemm_tile<C>(h, M, ldh, w, V, ldw, d, m0, n0, sm, acc);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = (wave / C::WN) * (C::BM / C::WM), wc = (wave % C::WN) * (C::BN / C::WN);
+    constexpr int CHUNKS = C::BN / 8;  // 16-byte output chunks per tile row
+    for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
+        if (e0) __syncthreads();
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = wr + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
+                    if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
+                }
+        __syncthreads();
+        for (int e = tid; e < C::EPI * CHUNKS; e += C::THREADS) {
+            const int r = e / CHUNKS, ch = e % CHUNKS;
+            const int64_t t = m0 + e0 + r;
+            const int64_t col0 = n0 + ch * 8;
+            if (t >= M || col0 >= V) continue;
+            const float g = coef[t], lb = lse[t];
+            const int64_t y = target[t];
+            const float dy = g * -expm1f(logp[t]);
+            float dz[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int64_t col = col0 + q;
+                const float x = sm.c[r][ch * 8 + q];
+                dz[q] = col == y ? dy : -g * expf(x - lb);
+            }
+            uint16_t* dst = out + t * ld_out + col0;
+            if (col0 + 8 <= V) {
+                u32x4 pk;
+                pk.x = pack_bf16x2(dz[0], dz[1]);
+                pk.y = pack_bf16x2(dz[2], dz[3]);
+                pk.z = pack_bf16x2(dz[4], dz[5]);
+                pk.w = pack_bf16x2(dz[6], dz[7]);
+                __builtin_nontemporal_store(pk, reinterpret_cast<u32x4*>(dst));
+            } else {
+                for (int q = 0; q < 8 && col0 + q < V; ++q) dst[q] = bf16_bits(dz[q]);
+            }
+        }
+    }
+}
+
 // One wave per row: the row's nvt triples merged lane-strided in index order,
 // then across lanes by a butterfly; the target logit is added last, as in
 // tok_stats_kernel: lse = M + log S, H = log S - W / S, and logp from
@@ -336,6 +418,48 @@ lmhead_merge_kernel(const float4* __restrict__ part, const float* __restrict__ z
 
 int64_t vocab_tiles(int64_t V) { return (V + LmCfg::BN - 1) / LmCfg::BN; }
 
+// Host-side argument rules shared by the LM-head entry points.
+bool bad_lmhead_args(const void* hidden, int64_t T, int64_t d, int64_t ld_h, const void* weight,
+                     int64_t V, int64_t ld_w) {
+    if (!hidden || !weight) return true;
+    if (T < 1 || V < 1 || d < 8 || T > 0x7FFFFFFFll || V > 0x7FFFFFFFll || d > 0x7FFFFFFFll)
+        return true;
+    if (d % 8 || ld_h < d || ld_w < d || ld_h % 8 || ld_w % 8) return true;
+    return reinterpret_cast<uintptr_t>(hidden) % 16 || reinterpret_cast<uintptr_t>(weight) % 16;
+}
+
+dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, int64_t ld_h,
+                             const uint16_t* weight, int64_t V, int64_t ld_w,
+                             const int32_t* target, const float* lse, const float* logp,
+                             const float* coef, uint16_t* out, int64_t ld_out,
+                             hipStream_t stream) {
+    const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
+    if (nmt * nvt > 0x7FFFFFFFll) return DART_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
+                       dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
+                       target, lse, logp, coef, out, ld_out, nmt, nvt);
+    return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+// One rocBLAS handle per device, created on first use and kept until the
+// process ends; calls that use it are serialised by the mutex (the handle's
+// stream is set per call).
+constexpr int kMaxDevices = 64;
+std::mutex g_blas_mu;
+rocblas_handle g_blas[kMaxDevices] = {};
+
+// A handle belongs to the device current when it is created.
+rocblas_handle blas_handle(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    if (g_blas[dev]) return g_blas[dev];
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return nullptr;
+    if (rocblas_create_handle(&g_blas[dev]) != rocblas_status_success) g_blas[dev] = nullptr;
+    if (cur != dev) (void)hipSetDevice(cur);
+    return g_blas[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -350,12 +474,8 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
                                     const int32_t* target, float* logp, float* entropy,
                                     float* lse, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream) {
-    if (!hidden || !weight || !target || !logp || !entropy || !lse || !workspace)
-        return DART_ERR_INVALID_ARG;
-    if (T < 1 || V < 1 || d < 8 || T > 0x7FFFFFFFll || V > 0x7FFFFFFFll || d > 0x7FFFFFFFll)
-        return DART_ERR_INVALID_ARG;
-    if (d % 8 || ld_h < d || ld_w < d || ld_h % 8 || ld_w % 8) return DART_ERR_INVALID_ARG;
-    if (reinterpret_cast<uintptr_t>(hidden) % 16 || reinterpret_cast<uintptr_t>(weight) % 16 ||
+    if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!target || !logp || !entropy || !lse || !workspace ||
         reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
     if (workspace_bytes < dart_lmhead_stats_workspace_bytes(T, V)) return DART_ERR_INVALID_ARG;
@@ -371,6 +491,83 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
     hipLaunchKernelGGL(lmhead_merge_kernel, dim3((unsigned)((T + kMergeWaves - 1) / kMergeWaves)),
                        dim3(kMergeWaves * 64), 0, stream, part, z_y, T, nvt, V, target, logp,
                        entropy, lse);
+    return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                  const void* weight, int64_t V, int64_t ld_w,
+                                  const int32_t* target, const float* lse, const float* logp,
+                                  const float* tok_coef, void* dlogits, int64_t ld_out,
+                                  hipStream_t stream) {
+    if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!target || !lse || !logp || !tok_coef || !dlogits || ld_out < V || ld_out % 8 ||
+        reinterpret_cast<uintptr_t>(dlogits) % 16)
+        return DART_ERR_INVALID_ARG;
+    return launch_dlogits(static_cast<const uint16_t*>(hidden), T, d, ld_h,
+                          static_cast<const uint16_t*>(weight), V, ld_w, target, lse, logp,
+                          tok_coef, static_cast<uint16_t*>(dlogits), ld_out, stream);
+}
+
+size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
+    if (chunk_rows < 1 || V < 1 || chunk_rows > 0x7FFFFFFFll || V > 0x7FFFFFFFll) return 0;
+    return (size_t)chunk_rows * (size_t)((V + 7) / 8 * 8) * 2;
+}
+
+dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                   const void* weight, int64_t V, int64_t ld_w,
+                                   const int32_t* target, const float* lse, const float* logp,
+                                   const float* tok_coef, float* dhidden, int64_t ld_dh,
+                                   float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
+        return DART_ERR_INVALID_ARG;
+    if (ld_dh < d || ld_dw < d || chunk_rows < 1 ||
+        reinterpret_cast<uintptr_t>(workspace) % 16)
+        return DART_ERR_INVALID_ARG;
+    // the BLAS library takes 32-bit sizes and leading dimensions
+    const int64_t kI32 = 0x7FFFFFFFll;
+    if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
+    if (chunk_rows > T) chunk_rows = T;
+    if (workspace_bytes < dart_lmhead_backward_workspace_bytes(chunk_rows, V))
+        return DART_ERR_INVALID_ARG;
+    int dev = 0;
+    if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess)
+        return DART_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_blas_mu);
+    rocblas_handle blas = blas_handle(dev);
+    if (!blas || rocblas_set_stream(blas, stream) != rocblas_status_success) return DART_ERR_HIP;
+    const int64_t ld_dz = (V + 7) / 8 * 8;
+    uint16_t* dz = static_cast<uint16_t*>(workspace);
+    const uint16_t* h = static_cast<const uint16_t*>(hidden);
+    const uint16_t* w = static_cast<const uint16_t*>(weight);
+    const float one = 1.f, zero = 0.f;
+    for (int64_t r0 = 0; r0 < T; r0 += chunk_rows) {
+        const int64_t rows = T - r0 < chunk_rows ? T - r0 : chunk_rows;
+        dart_status_t st = launch_dlogits(h + r0 * ld_h, rows, d, ld_h, w, V, ld_w, target + r0,
+                                          lse + r0, logp + r0, tok_coef + r0, dz, ld_dz, stream);
+        if (st != DART_OK) return st;
+        // rocBLAS is column-major: a row-major [R, C] matrix with row stride ld
+        // is its column-major [C, R] transpose with leading dimension ld.
+        // dh[rows, d] = dz[rows, V] W[V, d]   <=>   dh^T = W^T dz^T
+        if (rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)d,
+                            (rocblas_int)rows, (rocblas_int)V, &one, w, rocblas_datatype_bf16_r,
+                            (rocblas_int)ld_w, dz, rocblas_datatype_bf16_r, (rocblas_int)ld_dz,
+                            &zero, dhidden + r0 * ld_dh, rocblas_datatype_f32_r,
+                            (rocblas_int)ld_dh, dhidden + r0 * ld_dh, rocblas_datatype_f32_r,
+                            (rocblas_int)ld_dh, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
+                            0, 0) != rocblas_status_success)
+            return DART_ERR_HIP;
+        // dW[V, d] (+)= dz^T[V, rows] h[rows, d]   <=>   dW^T = h^T dz
+        if (rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
+                            (rocblas_int)d, (rocblas_int)V, (rocblas_int)rows, &one, h + r0 * ld_h,
+                            rocblas_datatype_bf16_r, (rocblas_int)ld_h, dz,
+                            rocblas_datatype_bf16_r, (rocblas_int)ld_dz, r0 == 0 ? &zero : &one,
+                            dweight, rocblas_datatype_f32_r, (rocblas_int)ld_dw, dweight,
+                            rocblas_datatype_f32_r, (rocblas_int)ld_dw, rocblas_datatype_f32_r,
+                            rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
+            return DART_ERR_HIP;
+    }
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 

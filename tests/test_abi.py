@@ -226,3 +226,49 @@ def test_lmhead_workspace_bytes():
     assert f(0, 10) == 0 and f(10, 0) == 0 and f(1 << 31, 5) == 0
     assert f(4, 300) == 4 * 2 * 16 + 16
     assert f(4096, 152064) == 4096 * 594 * 16 + 4096 * 4
+
+
+def _lm_grad_args(**kw):
+    a = dict(hidden=1 << 20, T=4, d=16, ld_h=16, weight=1 << 21, V=300, ld_w=16, target=P,
+             lse=P, logp=P, coef=P, out=1 << 23, ld_out=304)
+    a.update(kw)
+    return list(a.values()) + [None]
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(hidden=0), dict(weight=0), dict(target=0), dict(lse=0), dict(logp=0), dict(coef=0),
+    dict(out=0), dict(T=0), dict(V=0), dict(d=12, ld_h=16, ld_w=16), dict(ld_w=12),
+    dict(ld_out=296), dict(ld_out=302), dict(out=(1 << 23) + 8), dict(hidden=(1 << 20) + 2),
+])
+def test_lmhead_dlogits_rejects(kw):
+    lib = dart.load_library()
+    assert lib.dart_lmhead_dlogits(*_lm_grad_args(**kw)) == dart.DART_ERR_INVALID_ARG
+
+
+def _lm_bwd_args(**kw):
+    a = dict(hidden=1 << 20, T=4, d=16, ld_h=16, weight=1 << 21, V=300, ld_w=16, target=P,
+             lse=P, logp=P, coef=P, dh=1 << 23, ld_dh=16, dw=1 << 24, ld_dw=16, chunk=2,
+             workspace=1 << 22, ws_bytes=2 * 304 * 2)
+    a.update(kw)
+    return list(a.values()) + [None]
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(hidden=0), dict(weight=0), dict(target=0), dict(lse=0), dict(logp=0), dict(coef=0),
+    dict(dh=0), dict(dw=0), dict(workspace=0), dict(T=0), dict(V=0), dict(d=4, ld_h=4, ld_w=4),
+    dict(ld_dh=15), dict(ld_dw=8), dict(chunk=0), dict(ws_bytes=2 * 304 * 2 - 1),
+    dict(chunk=9, ws_bytes=4 * 304 * 2 - 2), dict(workspace=(1 << 22) + 8),
+])
+def test_lmhead_backward_rejects(kw):
+    lib = dart.load_library()
+    assert lib.dart_lmhead_backward(*_lm_bwd_args(**kw)) == dart.DART_ERR_INVALID_ARG
+
+
+def test_lmhead_backward_workspace_bytes():
+    """One bfloat16 dlogits chunk with rows padded to a multiple of 8 columns."""
+    f = dart.load_library().dart_lmhead_backward_workspace_bytes
+    assert f(0, 10) == 0 and f(10, 0) == 0 and f(1 << 31, 5) == 0
+    assert f(2, 300) == 2 * 304 * 2 and f(3, 8) == 3 * 8 * 2
+    assert f(1024, 152064) == 1024 * 152064 * 2
