@@ -99,6 +99,72 @@ def cpu_baseline(wl, threads):
             "sample": f"whole workload ({wl.T} rows x {wl.V}), float64 C oracle, OpenMP over rows"}
 
 
+def lmhead_variant(wl, dev, stream, target, coef, n):
+    """The LM head fused in (never the headline): statistics and gradients of
+    the logits h W^T formed on the matrix cores, at this workload's T and V and
+    the 7B VLM's hidden size, with the headline step's own loss coefficients;
+    beside it the library GEMM that materialises the same logits. Per-launch
+    HIP events on the bench stream; medians of n launches after one warm-up."""
+    import numpy as np
+    import torch
+
+    import paper_2509_23866_amd as dart
+    import synth
+    import synth.native as sn
+    from synth.gen import STREAM_HIDDEN, STREAM_WEIGHT
+
+    prob = synth.lmhead_problem(wl.name)
+    T, V, d = wl.T, wl.V, prob.d
+    bf = torch.bfloat16
+    h = torch.empty((T, d), dtype=bf, device=dev)
+    w = torch.empty((V, d), dtype=bf, device=dev)
+    sn.fill_gaussian_device(h, wl.seed, STREAM_HIDDEN, prob.sigma_h)
+    sn.fill_gaussian_device(w, wl.seed, STREAM_WEIGHT, prob.sigma_w)
+    logp, ent, lse = (torch.empty(T, dtype=torch.float32, device=dev) for _ in range(3))
+    ws = torch.empty(dart.dart_lmhead_stats_workspace_bytes(T, V), dtype=torch.uint8, device=dev)
+    zbuf = torch.empty((T, V), dtype=bf, device=dev)
+    dh = torch.empty((T, d), dtype=torch.float32, device=dev)
+    dw = torch.empty((V, d), dtype=torch.float32, device=dev)
+    wsb = torch.empty(dart.dart_lmhead_backward_workspace_bytes(T, V), dtype=torch.uint8, device=dev)
+
+    def timed(f):
+        f()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n)]
+        for a, b in ev:
+            a.record(stream)
+            f()
+            b.record(stream)
+        torch.cuda.synchronize(dev)
+        return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+    stats_ms = timed(lambda: dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, workspace=ws,
+                                                        stream=stream))
+    dl_ms = timed(lambda: dart.dart_lmhead_dlogits(h, w, target, lse, logp, coef, dlogits=zbuf,
+                                                   stream=stream))
+    bwd_ms = timed(lambda: dart.dart_lmhead_backward(h, w, target, lse, logp, coef, chunk_rows=T,
+                                                     dhidden=dh, dweight=dw, workspace=wsb,
+                                                     stream=stream))
+    gemm_ms = timed(lambda: torch.matmul(h, w.t(), out=zbuf))
+    tstats_ms = timed(lambda: dart.dart_tok_stats(zbuf, target, logp, ent, lse, stream=stream))
+    flop = 2.0 * T * V * d
+    peak = 2500.0  # dense bf16 MFMA, TFLOP/s
+
+    def tf(ms, k=1):
+        return k * flop / (ms * 1e-3) / 1e12
+
+    return {
+        "shape": {"T": T, "d": d, "V": V}, "flop_per_gemm": flop, "peak_TFLOPs": peak,
+        "stats_kernels_ms": stats_ms, "stats_TFLOPs": tf(stats_ms),
+        "stats_mfma_frac": tf(stats_ms) / peak,
+        "dlogits_ms": dl_ms, "dlogits_TFLOPs": tf(dl_ms), "dlogits_mfma_frac": tf(dl_ms) / peak,
+        "backward_ms": bwd_ms, "backward_chunk_rows": T, "backward_TFLOPs": tf(bwd_ms, 3),
+        "library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
+        "unfused_stats_ms": gemm_ms + tstats_ms,
+        "logits_bytes_not_materialised": T * V * 2,
+    }
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -247,6 +313,10 @@ def main():
         stats_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_s]))
         variants["stats_only"] = {"ms": stats_ms, "logit_elements_per_s": T * V / (stats_ms * 1e-3),
                                   "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
+
+    if not args.no_variants and T <= 16384:
+        variants["lmhead_fused"] = lmhead_variant(wl, dev, stream, target, coef,
+                                                  min(args.steps, 10))
 
     # empirical ceiling beside the 8 TB/s peak: a plain torch elementwise kernel
     # reading and writing the same T x V bytes as the gradient pass
