@@ -22,6 +22,7 @@
 #include <stdint.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "dart.h"
 
@@ -54,27 +55,52 @@ __device__ __forceinline__ void lds_ring_barrier() {
 // slices of 64 through an NS-buffer LDS ring filled by direct global->LDS
 // loads (no staging registers), WM x WN waves each owning a (BM/WM) x (BN/WN)
 // block of 32 x 32 MFMA tiles.
-template <int BM_, int BN_, int WM_, int WN_, int NS_>
+// A K slice of BK bf16 per tile row is BK/8 chunks of 16 B. Chunk c of row r
+// sits in LDS slot c ^ swz(r). gfx950's LDS serves 16-byte-per-lane reads 16
+// lanes at a time across 64 four-byte banks (16 bank quads); a row of CH
+// chunks covers CH quads, so 16 / CH consecutive rows tile the banks once and
+// the swizzle shifts each such run of rows: the 16 rows that one read cycle
+// takes (same chunk c) land in 16 distinct quads. With the plain c ^ (r % 8)
+// of a 32-bank LDS, the bank-conflict counter showed half of all LDS cycles
+// in two-way conflicts.
+template <int CH>
+__device__ __forceinline__ int swz(int r) { return (r / (16 / CH)) % CH; }
+
+template <int BM_, int BN_, int WM_, int WN_, int NS_, int BK_ = 64>
 struct Cfg {
-    static constexpr int BM = BM_, BN = BN_, BK = 64, WM = WM_, WN = WN_, NS = NS_;
+    static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_, NS = NS_;
+    static_assert(NS == 2, "the K loop alternates two LDS buffers");
+    static constexpr int CH = BK / 8;          // 16-byte chunks per row and slice
+    static constexpr int LROWS = 64 / CH;      // rows one load instruction fills
+    static constexpr int KSTEPS = BK / 16;     // MFMA k-steps per slice
     static constexpr int THREADS = 64 * WM * WN, WAVES = WM * WN;
     static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;  // MFMA tiles per wave
-    static constexpr int IA = BM / 8 / WAVES, IB = BN / 8 / WAVES;  // load instructions per slice
-    static constexpr int CROW = BN + 1;  // LDS row of the fp32 result tile
-    // the epilogue stages EPI rows of the fp32 tile at a time through LDS
-    static constexpr int EPI = (BM * CROW * 4 <= 159 * 1024) ? BM : BM / 2;
+    // a wave's TM row blocks of 32 sit RS = WM * 32 rows apart, so that each
+    // epilogue pass over EPI = RS rows takes one block from every wave
+    static constexpr int RS = BM / TM;
+    static constexpr int IA = BM / LROWS / WAVES, IB = BN / LROWS / WAVES;  // loads per slice
+    // LDS row of the fp32 result tile: BN + 16 floats, so that consecutive
+    // rows start one bank quad apart: the 16 lanes of one 16-byte read cycle
+    // (4 rows x 4 adjacent 16-byte pieces) fall in 16 distinct quads
+    static constexpr int CROW = BN + 16;
+    // the epilogue stages EPI rows of the fp32 tile at a time through LDS:
+    // one 32-row block of every wave
+    static constexpr int EPI = RS;
+    static_assert(BK == 32 || BK == 64, "slice depth");
     static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "tile shape");
-    static_assert(IA * 8 * WAVES == BM && IB * 8 * WAVES == BN, "rows per wave");
+    static_assert(IA * LROWS * WAVES == BM && IB * LROWS * WAVES == BN, "rows per wave");
     static_assert(THREADS % EPI == 0 || EPI % THREADS == 0, "epilogue rows");
     struct alignas(16) Smem {
         union {
             struct {
-                // slice buffers: 64 bf16 (8 chunks of 16 B) per row, chunk c of
-                // row r stored in slot c ^ (r % 8)
-                uint16_t a[NS][BM][64];
-                uint16_t b[NS][BN][64];
+                // slice buffers: BK bf16 per row, chunk c of row r in slot c ^ swz(r)
+                uint16_t a[NS][BM][BK];
+                uint16_t b[NS][BN][BK];
             } in;
-            float c[EPI][CROW];
+            struct {
+                float c[EPI][CROW];
+                float4 rowp[EPI];  // per-row constants of the gradient epilogue
+            };
         };
     };
 };
@@ -82,6 +108,7 @@ struct Cfg {
 // tiles, 4 or 8 waves, 2-4 ring buffers and register-staged loads: 256 x 256
 // with 8 waves as 4 x 2 (64 x 128 per wave) and 2 buffers is the fastest.
 using LmCfg = Cfg<256, 256, 4, 2, 2>;
+static_assert(sizeof(LmCfg::Smem) <= 160 * 1024, "LDS per workgroup");
 constexpr int kMergeWaves = 4;
 
 struct Triple {
@@ -113,13 +140,13 @@ __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
     return r;
 }
 
-// acc = this wave's block of the tile A[m0:m0+BM, :] B[n0:n0+BN, :]^T (A [M, K]
+// acc = this wave's part of the tile A[m0:m0+BM, :] B[n0:n0+BN, :]^T (A [M, K]
 // and B [N, K] row-major bf16, rows 16-byte aligned, K % 8 == 0). Rows past M
 // or N read clamped copies of the last row (their results are not used); K
-// past the end is zeroed in LDS. Layout of acc[i][j]: value v of lane l is row
-// i*32 + (v/4)*8 + (l/32)*4 + v%4, column j*32 + l%32 of the wave's block,
-// which starts at row (wave / WN) * BM/WM, column (wave % WN) * BN/WN. Ends
-// on a barrier with no loads in flight, so the caller may reuse the LDS.
+// past the end is zeroed in LDS. Layout of acc[i][j]: value v of lane l is
+// tile row (wave / WN) * 32 + i * RS + (v/4)*8 + (l/32)*4 + v%4, column
+// (wave % WN) * BN/WN + j*32 + l%32. Ends on a barrier with no loads in
+// flight, so the caller may reuse the LDS.
 template <class C>
 __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_t M, int64_t lda,
                                           const uint16_t* __restrict__ B, int64_t N, int64_t ldb,
@@ -127,8 +154,9 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
                                           typename C::Smem& sm,
                                           f32x16 (&acc)[C::TM][C::TN]) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the gfx950 builtins below have no host form
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = (wave / C::WN) * (C::BM / C::WM), wc = (wave % C::WN) * (C::BN / C::WN);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: addresses in SGPRs
+    const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
 #pragma unroll
     for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -136,81 +164,123 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    // one load instruction fills 8 rows x 8 slots (1 KB): lane l writes slot
-    // l % 8 of row r0 + l / 8, i.e. chunk (l % 8) ^ (row % 8) of that row
-    const int lrow = lane >> 3, lslot = lane & 7;
+    // One load instruction fills LROWS rows x CH slots (1 KB): lane l writes
+    // slot l % CH of row r0 + l / CH, i.e. chunk (l % CH) ^ swz(row) of that
+    // row. Each lane's source offsets within the tile are fixed for the whole
+    // K loop (rows past M or N clamped to the last row), so a full slice's
+    // load is a uniform base plus a per-lane 32-bit offset.
+    constexpr int CH = C::CH, BK = C::BK, PER = C::IA + C::IB;
+    const int lrow = lane / CH, lslot = lane % CH;
+    const char* a_tile = reinterpret_cast<const char*>(A + m0 * lda);
+    const char* b_tile = reinterpret_cast<const char*>(B + n0 * ldb);
+    uint32_t aoff[C::IA], boff[C::IB];
+#pragma unroll
+    for (int q = 0; q < C::IA; ++q) {
+        const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+        aoff[q] = (uint32_t)(((min(m0 + r, M - 1) - m0) * lda + (lslot ^ swz<CH>(r)) * 8) * 2);
+    }
+#pragma unroll
+    for (int q = 0; q < C::IB; ++q) {
+        const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+        boff[q] = (uint32_t)(((min(n0 + r, N - 1) - n0) * ldb + (lslot ^ swz<CH>(r)) * 8) * 2);
+    }
+    auto lds_a = [&](int buf, int q) { return &sm.in.a[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
+    auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
+    const int64_t nk = (K + BK - 1) / BK;
+    // slice kt into buffer buf; a slice that ends past K clamps each chunk's
+    // column to K - 8 (those chunks are zeroed after landing)
     auto issue = [&](int64_t kt, int buf) {
+        if ((kt + 1) * BK <= K) {
+            const int64_t kb = kt * BK * 2;
 #pragma unroll
-        for (int q = 0; q < C::IA; ++q) {
-            const int r0 = (q * C::WAVES + wave) * 8, r = r0 + lrow;
-            const int c = lslot ^ (r & 7);
-            const int64_t row = min(m0 + r, M - 1), k = min(kt * 64 + c * 8, K - 8);
-            __builtin_amdgcn_global_load_lds(A + row * lda + k, &sm.in.a[buf][r0][0], 16, 0, 0);
-        }
+            for (int q = 0; q < C::IA; ++q)
+                __builtin_amdgcn_global_load_lds(a_tile + kb + aoff[q], lds_a(buf, q), 16, 0, 0);
 #pragma unroll
-        for (int q = 0; q < C::IB; ++q) {
-            const int r0 = (q * C::WAVES + wave) * 8, r = r0 + lrow;
-            const int c = lslot ^ (r & 7);
-            const int64_t row = min(n0 + r, N - 1), k = min(kt * 64 + c * 8, K - 8);
-            __builtin_amdgcn_global_load_lds(B + row * ldb + k, &sm.in.b[buf][r0][0], 16, 0, 0);
+            for (int q = 0; q < C::IB; ++q)
+                __builtin_amdgcn_global_load_lds(b_tile + kb + boff[q], lds_b(buf, q), 16, 0, 0);
+        } else {
+#pragma unroll
+            for (int q = 0; q < C::IA; ++q) {
+                const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+                const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, K - 8);
+                __builtin_amdgcn_global_load_lds(A + min(m0 + r, M - 1) * lda + k, lds_a(buf, q), 16, 0, 0);
+            }
+#pragma unroll
+            for (int q = 0; q < C::IB; ++q) {
+                const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+                const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, K - 8);
+                __builtin_amdgcn_global_load_lds(B + min(n0 + r, N - 1) * ldb + k, lds_b(buf, q), 16, 0, 0);
+            }
         }
     };
-    auto operand = [&](const uint16_t (*tile)[64], int r, int c) {
-        return __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(&tile[r][(c ^ (r & 7)) * 8]));
+    // a partial last slice: zero the chunks past K (they hold clamped copies)
+    auto zero_tail = [&](int64_t kt, int buf) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        for (int e = tid; e < (C::BM + C::BN) * CH; e += C::THREADS) {
+            const int r = e / CH, c = e % CH;
+            if (kt * BK + c * 8 < K) continue;
+            if (r < C::BM)
+                *reinterpret_cast<u32x4*>(&sm.in.a[buf][r][(c ^ swz<CH>(r)) * 8]) = z;
+            else
+                *reinterpret_cast<u32x4*>(
+                    &sm.in.b[buf][r - C::BM][(c ^ swz<CH>(r - C::BM)) * 8]) = z;
+        }
     };
 
-    const int64_t nk = (K + 63) / 64;
-    constexpr int PER = C::IA + C::IB;  // loads per wave and slice
+    // MFMA operands: lane l reads row (l % 32) of each 32-row block, chunk
+    // 2 ks + l / 32. The rows' swizzle depends only on l % 32 (blocks start at
+    // multiples of 32), so one byte offset per k-step serves every block, the
+    // block and the buffer entering as immediate offsets.
+    uint32_t rda[C::KSTEPS], rdb[C::KSTEPS];
 #pragma unroll
-    for (int s = 0; s < C::NS - 1; ++s)
-        if (s < nk) issue(s, s);
-    for (int64_t kt = 0; kt < nk; ++kt) {
-        // slice kt has landed (up to NS-2 newer slices stay in flight)
-        if (kt + C::NS - 2 < nk)
-            wait_vmcnt<(C::NS - 2) * PER>();
-        else
-            wait_vmcnt<0>();
+    for (int ks = 0; ks < C::KSTEPS; ++ks) {
+        const int c = ks * 2 + (lane >> 5), ra = wr + (lane & 31), rb = wc + (lane & 31);
+        rda[ks] = (uint32_t)(ra * BK + (c ^ swz<CH>(ra)) * 8) * 2;
+        rdb[ks] = (uint32_t)(rb * BK + (c ^ swz<CH>(rb)) * 8) * 2;
+    }
+    bf16x8 af[2][C::TM], bfr[2][C::TN];
+    auto read_step = [&](auto bufc, int ks, int set) {
+        constexpr int buf = decltype(bufc)::value;
+        const char* ba = reinterpret_cast<const char*>(&sm.in.a[buf][0][0]);
+        const char* bb = reinterpret_cast<const char*>(&sm.in.b[buf][0][0]);
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+            af[set][i] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(ba + rda[ks] + i * C::RS * BK * 2));
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+            bfr[set][j] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(bb + rdb[ks] + j * 32 * BK * 2));
+    };
+    auto mfmas = [&](int set) {
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][i], bfr[set][j],
+                                                                    acc[i][j], 0, 0, 0);
+    };
+
+    // two LDS buffers: slice kt+1 loads while slice kt is multiplied
+    auto slice = [&](auto bufc, int64_t kt) {
+        constexpr int buf = decltype(bufc)::value;
+        // slice kt has landed for this wave; the barrier makes it so for all,
+        // and every wave has finished reading the other buffer (slice kt-1)
+        wait_vmcnt<0>();
         lds_ring_barrier();
-        const int buf = (int)(kt % C::NS);
-        if ((K & 63) && kt == nk - 1) {
-            // a partial last slice: zero the chunks past K (they hold clamped copies)
-            const u32x4 z = {0u, 0u, 0u, 0u};
-            for (int e = tid; e < (C::BM + C::BN) * 8; e += C::THREADS) {
-                const int r = e >> 3, c = e & 7;
-                if (kt * 64 + c * 8 < K) continue;
-                if (r < C::BM)
-                    *reinterpret_cast<u32x4*>(&sm.in.a[buf][r][(c ^ (r & 7)) * 8]) = z;
-                else
-                    *reinterpret_cast<u32x4*>(
-                        &sm.in.b[buf][r - C::BM][(c ^ ((r - C::BM) & 7)) * 8]) = z;
-            }
+        if ((K % BK) && kt == nk - 1) {
+            zero_tail(kt, buf);
             lds_ring_barrier();
         }
-        // the buffer refilled here was last read in iteration kt-1, before the barrier
-        if (kt + C::NS - 1 < nk) issue(kt + C::NS - 1, (int)((kt + C::NS - 1) % C::NS));
-
+        if (kt + 1 < nk) issue(kt + 1, buf ^ 1);
         // the operands of k-step ks+1 are read while the MFMAs of k-step ks issue
-        bf16x8 af[2][C::TM], bfr[2][C::TN];
-        auto read_step = [&](int ks, int set) {
-            const int c = ks * 2 + (lane >> 5);
+        read_step(bufc, 0, 0);
 #pragma unroll
-            for (int i = 0; i < C::TM; ++i) af[set][i] = operand(sm.in.a[buf], wr + i * 32 + (lane & 31), c);
-#pragma unroll
-            for (int j = 0; j < C::TN; ++j) bfr[set][j] = operand(sm.in.b[buf], wc + j * 32 + (lane & 31), c);
-        };
-        read_step(0, 0);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
             const int cs = ks & 1;
-            if (ks < 3) read_step(ks + 1, cs ^ 1);
-#pragma unroll
-            for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < C::TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cs][i], bfr[cs][j],
-                                                                        acc[i][j], 0, 0, 0);
-            if (ks < 3) {
+            if (ks < C::KSTEPS - 1) read_step(bufc, ks + 1, cs ^ 1);
+            mfmas(cs);
+            if (ks < C::KSTEPS - 1) {
                 // interleave: one LDS read, then a share of the MFMAs
 #pragma unroll
                 for (int g = 0; g < C::TM + C::TN; ++g) {
@@ -219,6 +289,11 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
                 }
             }
         }
+    };
+    issue(0, 0);
+    for (int64_t kt = 0; kt < nk; kt += 2) {
+        slice(std::integral_constant<int, 0>{}, kt);
+        if (kt + 1 < nk) slice(std::integral_constant<int, 1>{}, kt + 1);
     }
     __syncthreads();
 #endif
@@ -252,7 +327,8 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
     gemm_tile<C>(h, T, ldh, w, V, ldw, d, m0, n0, sm, acc);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = (wave / C::WN) * (C::BM / C::WM), wc = (wave % C::WN) * (C::BN / C::WN);
+    const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
+#pragma unroll
     for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
         if (e0) __syncthreads();
         // rows [e0, e0 + EPI) of the tile to LDS
@@ -262,46 +338,66 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
             for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int row = wr + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
+                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
                     if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
                 }
         __syncthreads();
-        // P threads per row, BN / P columns each: maximum, then the sums; the
-        // P partial triples merged in lane order
-        constexpr int P = C::THREADS >= C::EPI ? C::THREADS / C::EPI : 1;
-        constexpr int NC = C::BN / P;
-        for (int r = tid / P; r < C::EPI; r += C::THREADS / P) {
-            const int part_id = tid % P;
-            const int64_t t = m0 + e0 + r;
-            const int64_t y = t < T ? (int64_t)target[t] : -1;
-            const int c0 = part_id * NC;
-            int ncol = (int)min((int64_t)NC, V - (n0 + c0));
-            if (ncol < 0) ncol = 0;
-            const int yc = (int)(y - n0 - c0);  // the target's column here, if 0 <= yc < ncol
-            float mx = -INFINITY;
-            for (int c = 0; c < ncol; ++c)
-                if (c != yc) mx = fmaxf(mx, sm.c[r][c0 + c]);
-            Triple mine = {mx, 0.f, 0.f};
-            if (mx > -INFINITY) {
-                for (int c = 0; c < ncol; ++c) {
-                    if (c == yc) continue;
-                    const float x = sm.c[r][c0 + c] - mx;
-                    const float e = expf(x);
-                    mine.s += e;
-                    mine.w = fmaf(e, x, mine.w);
-                }
-            }
+        // P threads per row; thread p takes the 16-byte pieces p, p + P, ...
+        // of the row (columns 16 c + 4 p + u) into registers: maximum over the
+        // row's columns other than the target, then the sums in base-2 units
+        // against it; the P partial triples merged in lane order
+        constexpr int P = C::THREADS / C::EPI, NX = C::BN / P;
+        static_assert(C::THREADS == C::EPI * P && P == 4, "four threads per epilogue row");
+        const int r = tid / P, p = tid % P;
+        const int64_t t = m0 + e0 + r;
+        const int64_t yrel = (t < T ? (int64_t)target[t] : -1) - n0;
+        // columns below vlim exist; the target sits at column y32 (-1: not here)
+        const int vlim = (int)min(V - n0, (int64_t)C::BN);
+        const int y32 = yrel >= 0 && yrel < vlim ? (int)yrel : -1;
+        float x[NX];
 #pragma unroll
-            for (int off = 1; off < P; off <<= 1) {
-                Triple o;
-                o.m = __shfl_xor(mine.m, off);
-                o.s = __shfl_xor(mine.s, off);
-                o.w = __shfl_xor(mine.w, off);
-                mine = (part_id & off) ? merge(o, mine) : merge(mine, o);
-            }
-            if (t < T && part_id == 0) part[t * nvt + vt] = make_float4(mine.m, mine.s, mine.w, 0.f);
-            if (t < T && yc >= 0 && yc < ncol) z_y[t] = sm.c[r][c0 + yc];
+        for (int c4 = 0; c4 < NX / 4; ++c4) {
+            const float4 q = *reinterpret_cast<const float4*>(&sm.c[r][16 * c4 + 4 * p]);
+            x[4 * c4] = q.x;
+            x[4 * c4 + 1] = q.y;
+            x[4 * c4 + 2] = q.z;
+            x[4 * c4 + 3] = q.w;
         }
+        // columns past V and the target's column drop out as -inf
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NX; ++i) {
+            const int col = 16 * (i >> 2) + 4 * p + (i & 3);
+            x[i] = col < vlim && col != y32 ? x[i] : -INFINITY;
+            mx = fmaxf(mx, x[i]);
+        }
+        Triple mine = {mx, 0.f, 0.f};
+        if (mx > -INFINITY) {
+            // e = 2^xl with xl = (x - mx) log2(e) floored at -200, where 2^xl is
+            // already 0 in fp32, so that dropped columns add 0 to both sums
+            constexpr float kLog2e = 1.4426950408889634f;
+            const float ml = mx * kLog2e;
+            float s2 = 0.f, w2 = 0.f;
+#pragma unroll
+            for (int i = 0; i < NX; ++i) {
+                const float xl = fmaxf(fmaf(x[i], kLog2e, -ml), -200.f);
+                const float e = __builtin_amdgcn_exp2f(xl);
+                s2 += e;
+                w2 = fmaf(e, xl, w2);
+            }
+            mine.s = s2;
+            mine.w = w2 * 0.6931471805599453f;
+        }
+#pragma unroll
+        for (int off = 1; off < P; off <<= 1) {
+            Triple o;
+            o.m = __shfl_xor(mine.m, off);
+            o.s = __shfl_xor(mine.s, off);
+            o.w = __shfl_xor(mine.w, off);
+            mine = (p & off) ? merge(o, mine) : merge(mine, o);
+        }
+        if (t < T && p == 0) part[t * nvt + vt] = make_float4(mine.m, mine.s, mine.w, 0.f);
+        if (t < T && y32 >= 0 && ((y32 >> 2) & (P - 1)) == p) z_y[t] = sm.c[r][y32];
     }
 }
 
@@ -326,8 +422,9 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
     gemm_tile<C>(h, M, ldh, w, V, ldw, d, m0, n0, sm, acc);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = (wave / C::WN) * (C::BM / C::WM), wc = (wave % C::WN) * (C::BN / C::WN);
+    const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
     constexpr int CHUNKS = C::BN / 8;  // 16-byte output chunks per tile row
+#pragma unroll
     for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
         if (e0) __syncthreads();
 #pragma unroll
@@ -336,24 +433,43 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
             for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int row = wr + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
+                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
                     if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
                 }
+        // per-row constants: -g, -lse log2(e), the target's gradient
+        // g (-expm1(logp)) (accurate when p_y -> 1), the target's column here
+        if (tid < C::EPI) {
+            const int64_t t = m0 + e0 + tid;
+            float4 rp = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
+            if (t < M) {
+                const float g = coef[t];
+                const int64_t yrel = (int64_t)target[t] - n0;
+                rp = make_float4(-g, -lse[t] * 1.4426950408889634f, g * -expm1f(logp[t]),
+                                 __int_as_float(yrel >= 0 && yrel < C::BN ? (int)yrel : -1));
+            }
+            sm.rowp[tid] = rp;
+        }
         __syncthreads();
         for (int e = tid; e < C::EPI * CHUNKS; e += C::THREADS) {
             const int r = e / CHUNKS, ch = e % CHUNKS;
             const int64_t t = m0 + e0 + r;
             const int64_t col0 = n0 + ch * 8;
             if (t >= M || col0 >= V) continue;
-            const float g = coef[t], lb = lse[t];
-            const int64_t y = target[t];
-            const float dy = g * -expm1f(logp[t]);
+            const float4 rp = sm.rowp[r];
+            const int yc = __float_as_int(rp.w) - ch * 8;  // the target's index in this chunk
+            // the chunk's two 16-byte halves, read in an order that alternates
+            // every 8 chunks so that the 16 lanes of one LDS read cycle hit 16
+            // distinct bank quads
+            const int sw = (ch >> 3) & 1;
+            const float4 a = *reinterpret_cast<const float4*>(&sm.c[r][ch * 8 + 4 * sw]);
+            const float4 b = *reinterpret_cast<const float4*>(&sm.c[r][ch * 8 + 4 - 4 * sw]);
+            const float4 lo = sw ? b : a, hi = sw ? a : b;
+            const float xs[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
             float dz[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
-                const int64_t col = col0 + q;
-                const float x = sm.c[r][ch * 8 + q];
-                dz[q] = col == y ? dy : -g * expf(x - lb);
+                const float e2 = __builtin_amdgcn_exp2f(fmaf(xs[q], 1.4426950408889634f, rp.y));
+                dz[q] = q == yc ? rp.z : rp.x * e2;
             }
             uint16_t* dst = out + t * ld_out + col0;
             if (col0 + 8 <= V) {
