@@ -1,21 +1,27 @@
-// libdart, LM-head part: the token statistics of the policy-update hot path
-// computed straight from the LM head's inputs, so that the [T, V] logits are
-// never written to memory.
+// libdart, LM-head part: the token statistics and the gradient of the
+// policy-update hot path computed straight from the LM head's inputs, so that
+// the [T, V] logits are never written to memory.
 //
 // Paper: DART, arXiv 2509.23866. The statistics are those of Sec. 4.3 (token
 // entropy, the target's log-prob of Eq. 1) for logits z = h W^T, where h [T, d]
 // are the final hidden states of the T action tokens and W [V, d] the LM-head
-// weight of the policy (the 7B VLM of Sec. 5.1: d = 3584, V = 152064).
+// weight of the policy (the 7B VLM of Sec. 5.1); the gradient is the chain
+// rule of Eq. 2's loss through them.
 //
-//   lmhead_stats_kernel  one 256 x 256 tile of z per workgroup on MFMA
-//                        (v_mfma_f32_32x32x16_bf16, fp32 accumulation), K = d in
-//                        slices of 64 loaded straight into an LDS ring; the tile
-//                        is reduced in the epilogue to one (max, normaliser,
-//                        entropy) triple per row over its 256 columns (the
-//                        target column kept apart) and written to a workspace.
-//   lmhead_merge_kernel  one wave per row: merges the row's V / 256 triples in
-//                        a fixed order, adds the target logit, writes logp, H
-//                        and lse exactly as tok_stats_kernel defines them.
+//   lmhead_stats_kernel   one 256 x 256 tile of z per workgroup on MFMA
+//                         (v_mfma_f32_32x32x16_bf16, fp32 accumulation), K = d
+//                         in slices of 64 loaded straight into two LDS buffers;
+//                         the tile is reduced in the epilogue to one (max,
+//                         normaliser, entropy) triple per row over its 256
+//                         columns (the target column kept apart), written to a
+//                         workspace.
+//   lmhead_merge_kernel   one wave per row: merges the row's V / 256 triples in
+//                         a fixed order, adds the target logit, writes logp, H
+//                         and lse exactly as tok_stats_kernel defines them.
+//   lmhead_dlogits_kernel the same tile, its epilogue writing
+//                         dz = g (onehot - softmax) in bf16.
+// dart_lmhead_backward adds dh = dz W and dW = dz^T h per chunk of rows with
+// the ROCm BLAS library.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <rocblas/rocblas.h>
@@ -105,8 +111,9 @@ struct Cfg {
     };
 };
 // Measured on MI355X at T = 4096, d = 3584, V = 152064 among 128/256-square
-// tiles, 4 or 8 waves, 2-4 ring buffers and register-staged loads: 256 x 256
-// with 8 waves as 4 x 2 (64 x 128 per wave) and 2 buffers is the fastest.
+// tiles, 4 or 8 waves, 2-4 buffers, 32- or 64-wide slices and register-staged
+// loads: 256 x 256 with 8 waves as 4 x 2 (64 x 128 per wave) and two 64-wide
+// buffers is the fastest.
 using LmCfg = Cfg<256, 256, 4, 2, 2>;
 static_assert(sizeof(LmCfg::Smem) <= 160 * 1024, "LDS per workgroup");
 constexpr int kMergeWaves = 4;
@@ -354,39 +361,45 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
         // columns below vlim exist; the target sits at column y32 (-1: not here)
         const int vlim = (int)min(V - n0, (int64_t)C::BN);
         const int y32 = yrel >= 0 && yrel < vlim ? (int)yrel : -1;
-        float x[NX];
+        // the thread's 64 columns in two halves of 32 registers, each folded
+        // into a triple (maximum, then the sums in base-2 units against it)
+        // and merged; columns past V and the target's column drop out as -inf
+        constexpr int NH = NX / 2;
+        Triple mine = {-INFINITY, 0.f, 0.f};
 #pragma unroll
-        for (int c4 = 0; c4 < NX / 4; ++c4) {
-            const float4 q = *reinterpret_cast<const float4*>(&sm.c[r][16 * c4 + 4 * p]);
-            x[4 * c4] = q.x;
-            x[4 * c4 + 1] = q.y;
-            x[4 * c4 + 2] = q.z;
-            x[4 * c4 + 3] = q.w;
-        }
-        // columns past V and the target's column drop out as -inf
-        float mx = -INFINITY;
+        for (int hh = 0; hh < 2; ++hh) {
+            float x[NH];
+            float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < NX; ++i) {
-            const int col = 16 * (i >> 2) + 4 * p + (i & 3);
-            x[i] = col < vlim && col != y32 ? x[i] : -INFINITY;
-            mx = fmaxf(mx, x[i]);
-        }
-        Triple mine = {mx, 0.f, 0.f};
-        if (mx > -INFINITY) {
-            // e = 2^xl with xl = (x - mx) log2(e) floored at -200, where 2^xl is
-            // already 0 in fp32, so that dropped columns add 0 to both sums
-            constexpr float kLog2e = 1.4426950408889634f;
-            const float ml = mx * kLog2e;
-            float s2 = 0.f, w2 = 0.f;
+            for (int c4 = 0; c4 < NH / 4; ++c4) {
+                const int cc = hh * (NH / 4) + c4;
+                const float4 q = *reinterpret_cast<const float4*>(&sm.c[r][16 * cc + 4 * p]);
+                const float qv[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-            for (int i = 0; i < NX; ++i) {
-                const float xl = fmaxf(fmaf(x[i], kLog2e, -ml), -200.f);
-                const float e = __builtin_amdgcn_exp2f(xl);
-                s2 += e;
-                w2 = fmaf(e, xl, w2);
+                for (int u = 0; u < 4; ++u) {
+                    const int col = 16 * cc + 4 * p + u;
+                    x[4 * c4 + u] = col < vlim && col != y32 ? qv[u] : -INFINITY;
+                    mx = fmaxf(mx, x[4 * c4 + u]);
+                }
             }
-            mine.s = s2;
-            mine.w = w2 * 0.6931471805599453f;
+            Triple part_h = {mx, 0.f, 0.f};
+            if (mx > -INFINITY) {
+                // e = 2^xl with xl = (x - mx) log2(e) floored at -200, where 2^xl
+                // is already 0 in fp32, so that dropped columns add 0
+                constexpr float kLog2e = 1.4426950408889634f;
+                const float ml = mx * kLog2e;
+                float s2 = 0.f, w2 = 0.f;
+#pragma unroll
+                for (int i = 0; i < NH; ++i) {
+                    const float xl = fmaxf(fmaf(x[i], kLog2e, -ml), -200.f);
+                    const float e = __builtin_amdgcn_exp2f(xl);
+                    s2 += e;
+                    w2 = fmaf(e, xl, w2);
+                }
+                part_h.s = s2;
+                part_h.w = w2 * 0.6931471805599453f;
+            }
+            mine = merge(mine, part_h);
         }
 #pragma unroll
         for (int off = 1; off < P; off <<= 1) {
