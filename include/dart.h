@@ -294,7 +294,7 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
  * z is accumulated in fp32 from the bf16 inputs. Errors: INVALID_ARG for a null
  * pointer, T < 1, V < 1, d < 8, a violated multiple-of-8 or alignment rule, or a
  * workspace that is too small; UNSUPPORTED when ceil(T/256) * ceil(V/256)
- * exceeds INT32_MAX; HIP when a launch fails. */
+ * exceeds INT32_MAX or ld_h or ld_w exceeds 2^22; HIP when a launch fails. */
 dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                     const void* weight, int64_t V, int64_t ld_w,
                                     const int32_t* target, float* logp, float* entropy,

@@ -548,6 +548,10 @@ lmhead_merge_kernel(const float4* __restrict__ part, const float* __restrict__ z
 int64_t vocab_tiles(int64_t V) { return (V + LmCfg::BN - 1) / LmCfg::BN; }
 
 // Host-side argument rules shared by the LM-head entry points.
+// The MFMA tile addresses its rows by 32-bit byte offsets from the tile's first
+// row: (BM - 1) rows of ld elements must stay below 2^31 bytes.
+constexpr int64_t kMaxLd = int64_t(1) << 22;
+
 bool bad_lmhead_args(const void* hidden, int64_t T, int64_t d, int64_t ld_h, const void* weight,
                      int64_t V, int64_t ld_w) {
     if (!hidden || !weight) return true;
@@ -563,7 +567,7 @@ dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, in
                              const float* coef, uint16_t* out, int64_t ld_out,
                              hipStream_t stream) {
     const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
-    if (nmt * nvt > 0x7FFFFFFFll) return DART_ERR_UNSUPPORTED;
+    if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
                        target, lse, logp, coef, out, ld_out, nmt, nvt);
@@ -609,7 +613,7 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
         return DART_ERR_INVALID_ARG;
     if (workspace_bytes < dart_lmhead_stats_workspace_bytes(T, V)) return DART_ERR_INVALID_ARG;
     const int64_t nmt = (T + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
-    if (nmt * nvt > 0x7FFFFFFFll) return DART_ERR_UNSUPPORTED;
+    if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
     float4* part = static_cast<float4*>(workspace);
     float* z_y = reinterpret_cast<float*>(part + T * nvt);
     hipLaunchKernelGGL(lmhead_stats_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)), dim3(LmCfg::THREADS),

@@ -272,3 +272,14 @@ def test_lmhead_backward_workspace_bytes():
     assert f(0, 10) == 0 and f(10, 0) == 0 and f(1 << 31, 5) == 0
     assert f(2, 300) == 2 * 304 * 2 and f(3, 8) == 3 * 8 * 2
     assert f(1024, 152064) == 1024 * 152064 * 2
+
+
+@pytest.mark.skipif("_gpu_visible()")
+def test_lmhead_leading_dimension_limit():
+    """Leading dimensions beyond 2^22 elements do not fit the tile's 32-bit
+    row offsets: UNSUPPORTED before anything is launched."""
+    lib = dart.load_library()
+    big = (1 << 22) + 8
+    assert lib.dart_lmhead_tok_stats(*_lm_args(ld_h=big)) == dart.DART_ERR_UNSUPPORTED
+    assert lib.dart_lmhead_tok_stats(*_lm_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
+    assert lib.dart_lmhead_dlogits(*_lm_grad_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
