@@ -581,15 +581,26 @@ constexpr int kMaxDevices = 64;
 std::mutex g_blas_mu;
 rocblas_handle g_blas[kMaxDevices] = {};
 
-// A handle belongs to the device current when it is created.
+// Makes dev the current device for the caller's scope and restores the
+// previous one after.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) return;
+        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (ok) (void)hipSetDevice(prev);
+    }
+};
+
+// The handle of the current device (a handle belongs to the device current
+// when it is created), created on first use.
 rocblas_handle blas_handle(int dev) {
     if (dev < 0 || dev >= kMaxDevices) return nullptr;
-    if (g_blas[dev]) return g_blas[dev];
-    int cur = 0;
-    if (hipGetDevice(&cur) != hipSuccess) return nullptr;
-    if (cur != dev && hipSetDevice(dev) != hipSuccess) return nullptr;
-    if (rocblas_create_handle(&g_blas[dev]) != rocblas_status_success) g_blas[dev] = nullptr;
-    if (cur != dev) (void)hipSetDevice(cur);
+    if (!g_blas[dev] && rocblas_create_handle(&g_blas[dev]) != rocblas_status_success)
+        g_blas[dev] = nullptr;
     return g_blas[dev];
 }
 
@@ -667,6 +678,9 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
     int dev = 0;
     if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess)
         return DART_ERR_HIP;
+    // the stream's device is current while the BLAS library works
+    DeviceGuard on_dev(dev);
+    if (!on_dev.ok) return DART_ERR_HIP;
     std::lock_guard<std::mutex> lock(g_blas_mu);
     rocblas_handle blas = blas_handle(dev);
     if (!blas || rocblas_set_stream(blas, stream) != rocblas_status_success) return DART_ERR_HIP;
