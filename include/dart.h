@@ -18,7 +18,12 @@
  * - Every call is asynchronous on `stream` (0 = the null stream): it checks its
  *   scalar arguments on the host, enqueues its kernels and returns. Outputs are
  *   valid once the stream is synchronised. Device data (target ids in range,
- *   increasing offsets) is a precondition and is not checked.
+ *   strictly increasing offsets with the documented ends, 0/1 step masks) is a
+ *   precondition and is not checked, unless the environment has DART_CHECK=1:
+ *   then every call first validates the device arrays it reads, waits for the
+ *   result (the call synchronises the stream, so this is a debugging mode that
+ *   cannot run under graph capture) and returns DART_ERR_INVALID_ARG, with
+ *   nothing of the call enqueued, on a violation.
  * - Logits are row-major [T, ld] with ld >= V (elements, not bytes). Rows whose
  *   start is 16-byte aligned (base aligned and ld * element size a multiple of
  *   16) take the vectorised path; other rows are still correct, only slower.

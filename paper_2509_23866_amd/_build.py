@@ -7,7 +7,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", "dart.hip"), os.path.join(HERE, "csrc", "lmhead.hip")]
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("dart.hip", "lmhead.hip", "check.hip")]
 LIB = os.path.join(HERE, "libdart.so")
 INCLUDE = os.path.join(ROOT, "include")
 

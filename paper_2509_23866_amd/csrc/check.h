@@ -1,0 +1,35 @@
+// libdart internal: the optional validation of device-side preconditions
+// (DART_CHECK=1 in the environment). Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <initializer_list>
+
+#include "dart.h"
+
+namespace dart_check {
+
+// One device array to validate.
+//   Ids:     n int32 values, each in [0, bound)
+//   Offsets: n + 1 int32 values, 0 = v[0] < v[1] < ... < v[n] = bound
+//   Mask:    n uint8 values, each 0 or 1
+struct Item {
+    enum Kind { Ids, Offsets, Mask } kind;
+    const void* ptr;
+    int64_t n;
+    int64_t bound;
+};
+
+// True when DART_CHECK=1 is set (read on every call, so it can be switched at
+// run time).
+__attribute__((visibility("hidden"))) bool enabled();
+
+// With checks enabled: runs the validation kernels for every item on stream,
+// waits for them and returns DART_ERR_INVALID_ARG if any precondition fails
+// (DART_ERR_HIP on a HIP error). With checks disabled: DART_OK, nothing runs.
+__attribute__((visibility("hidden"))) dart_status_t run(hipStream_t stream,
+                                                        std::initializer_list<Item> items);
+
+}  // namespace dart_check

@@ -28,6 +28,7 @@
 
 #include <type_traits>
 
+#include "check.h"
 #include "dart.h"
 
 namespace {
@@ -1308,6 +1309,9 @@ dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t 
         return DART_ERR_INVALID_ARG;
     if (!(inv_temp > 0.f) || isinf(inv_temp)) return DART_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(logits) % elem_size(dtype)) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
     const dim3 grid((unsigned)T), block(kStatsThreads);
     if (dtype == DART_BF16)
         hipLaunchKernelGGL(
@@ -1333,6 +1337,9 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     const int64_t k = dart_kept_steps(S, rho);
     if (k < 0) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, step_offsets, S, T}}); ck != DART_OK)
+        return ck;
     if (T <= kSelLdsTokens && S <= kSelLdsKeys) {
         hipLaunchKernelGGL(step_select_kernel<true>, dim3(1), dim3(kSelThreads), 0, stream,
                            entropy, T, step_offsets, S, nullptr, rho, k, step_entropy, step_mask,
@@ -1356,6 +1363,10 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll || G < 1 || G > S || G > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
     if (dart_kept_steps(S, rho) < 0) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, step_offsets, S, T},
+                     {dart_check::Item::Offsets, group_step_offsets, G, S}}); ck != DART_OK)
+        return ck;
     hipLaunchKernelGGL(step_mean_kernel, dim3((unsigned)((S + kSelWaves - 1) / kSelWaves)),
                        dim3(kSelThreads), 0, stream, entropy, T, step_offsets, S, step_entropy);
     hipLaunchKernelGGL(step_select_kernel<false>, dim3((unsigned)G), dim3(kSelThreads), 0, stream,
@@ -1374,6 +1385,11 @@ dart_status_t dart_grpo_advantage(const float* reward, int64_t n_traj,
     if (n_traj < 1 || G < 1 || G > n_traj || S < 1 || S > T || T > 0x7FFFFFFFll ||
         G > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, traj_step_offsets, n_traj, S},
+                     {dart_check::Item::Offsets, group_traj_offsets, G, n_traj},
+                     {dart_check::Item::Offsets, step_offsets, S, T}}); ck != DART_OK)
+        return ck;
     hipLaunchKernelGGL(grpo_advantage_kernel, dim3((unsigned)G), dim3(kAdvThreads), 0, stream,
                        reward, traj_step_offsets, n_traj, group_traj_offsets, step_offsets, S, T,
                        adv, group_mean, group_std);
@@ -1400,6 +1416,10 @@ dart_status_t dart_tis_loss_fwd_ex(int64_t T, const float* logp, const float* lo
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     if (!(c.eps_low >= 0.f) || !(c.eps_high >= 0.f) || !(c.C > 0.f)) return DART_ERR_INVALID_ARG;
     if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, step_offsets, S, T},
+                     {dart_check::Item::Mask, step_mask, S, 0}}); ck != DART_OK)
+        return ck;
     LossConfig cfg;
     cfg.eps_low = c.eps_low;
     cfg.eps_high = c.eps_high;
@@ -1426,6 +1446,10 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
     if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
     if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, step_offsets, S, T},
+                     {dart_check::Item::Mask, step_mask, S, 0}}); ck != DART_OK)
+        return ck;
     LossConfig cfg;
     cfg.eps_low = eps_low;
     cfg.eps_high = eps_high;
@@ -1452,6 +1476,9 @@ dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T
     if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
         return DART_ERR_INVALID_ARG;
     if (bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
     // chunks of kGradThreads * kGradUnroll vectors per row; a grid of at most
     // kGradMaxBlocks workgroups strides over the T * nchunk chunks
     const int64_t per = (int64_t)kGradThreads * kGradUnroll;
@@ -1494,6 +1521,14 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
     if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
         return DART_ERR_INVALID_ARG;
     if (T >= 1 && bad_overlap(logits, ld, dlogits, ld_out, T, V, es)) return DART_ERR_INVALID_ARG;
+    // with checks on, all device data is validated before either half enqueues
+    if (T >= 1 && S >= 1 && S <= T) {
+        const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V},
+                     {dart_check::Item::Offsets, step_offsets, S, T},
+                     {dart_check::Item::Mask, step_mask, S, 0}});
+        if (ck != DART_OK) return ck;
+    }
     dart_status_t st = dart_tis_loss_fwd(T, logp, logp_old, logp_rollout, adv, step_offsets, S,
                                          step_mask, eps_low, eps_high, C, loss, tok_coef, stats,
                                          workspace, workspace_bytes, stream);

@@ -30,6 +30,7 @@
 #include <mutex>
 #include <type_traits>
 
+#include "check.h"
 #include "dart.h"
 
 namespace {
@@ -622,6 +623,10 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
     if (!target || !logp || !entropy || !lse || !workspace ||
         reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
+
     if (workspace_bytes < dart_lmhead_stats_workspace_bytes(T, V)) return DART_ERR_INVALID_ARG;
     const int64_t nmt = (T + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
     if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
@@ -647,6 +652,10 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
     if (!target || !lse || !logp || !tok_coef || !dlogits || ld_out < V || ld_out % 8 ||
         reinterpret_cast<uintptr_t>(dlogits) % 16)
         return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
+
     return launch_dlogits(static_cast<const uint16_t*>(hidden), T, d, ld_h,
                           static_cast<const uint16_t*>(weight), V, ld_w, target, lse, logp,
                           tok_coef, static_cast<uint16_t*>(dlogits), ld_out, stream);
@@ -675,6 +684,10 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
     if (chunk_rows > T) chunk_rows = T;
     if (workspace_bytes < dart_lmhead_backward_workspace_bytes(chunk_rows, V))
         return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
+
     int dev = 0;
     if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess)
         return DART_ERR_HIP;

@@ -1,0 +1,161 @@
+"""DART_CHECK=1: device-side preconditions (target ids in range, strictly
+increasing offsets with the right ends, 0/1 step masks) are validated before
+any kernel reads them, and a violation is DART_ERR_INVALID_ARG with nothing
+of the call enqueued. Valid inputs give the same outputs as without checks.
+Every malformed case here runs only with the checks on, so no kernel ever
+reads out of range."""
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+def _cuda(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.fixture
+def checks_on(monkeypatch):
+    monkeypatch.setenv("DART_CHECK", "1")
+
+
+def _invalid(excinfo):
+    import paper_2509_23866_amd as dart
+
+    assert excinfo.value.code == dart.DART_ERR_INVALID_ARG
+
+
+def _small(seed=0, T=40, V=300, S=5):
+    import torch
+
+    rng = np.random.default_rng(seed)
+    logits = torch.from_numpy(rng.normal(0, 2, (T, V)).astype(np.float32)).cuda()
+    target = rng.integers(0, V, T).astype(np.int32)
+    off = np.r_[0, np.sort(rng.choice(np.arange(1, T), S - 1, replace=False)), T].astype(np.int32)
+    return logits, target, off
+
+
+@pytest.mark.parametrize("bad", [-1, 300, 1 << 30])
+def test_target_out_of_range(checks_on, bad):
+    import paper_2509_23866_amd as dart
+
+    logits, target, _ = _small()
+    target[7] = bad
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_tok_stats(logits, _cuda(target))
+    _invalid(e)
+
+
+@pytest.mark.parametrize("case", ["repeat", "start", "end", "decrease"])
+def test_step_offsets_malformed(checks_on, case):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T = 40
+    off = np.array([0, 5, 12, 30, 40], np.int32)
+    if case == "repeat":
+        off[2] = off[1]
+    elif case == "start":
+        off[0] = 1
+    elif case == "end":
+        off[-1] = T - 1
+    else:
+        off[2], off[3] = off[3], off[2]
+    ent = torch.rand(T, device="cuda")
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_step_select(ent, _cuda(off), 0.5)
+    _invalid(e)
+
+
+def test_mask_values(checks_on):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T = 40
+    off = _cuda(np.array([0, 5, 12, 30, 40], np.int32))
+    mask = _cuda(np.array([1, 0, 2, 1], np.uint8))
+    v = [torch.randn(T, device="cuda") for _ in range(4)]
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_tis_loss_fwd(*v, off, mask, 0.2, 0.28, 2.0)
+    _invalid(e)
+
+
+def test_grpo_offsets(checks_on):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    reward = torch.tensor([1.0, 0.0, 1.0], device="cuda")
+    step_off = _cuda(np.array([0, 4, 9, 15, 20], np.int32))  # S = 4, T = 20
+    groups = _cuda(np.array([0, 3], np.int32))
+    for traj in ([0, 2, 2, 4], [0, 1, 3, 5]):  # an empty trajectory; an end past S
+        with pytest.raises(dart.DartError) as e:
+            dart.dart_grpo_advantage(reward, _cuda(np.array(traj, np.int32)), groups, step_off)
+        _invalid(e)
+
+
+def test_fwd_bwd_enqueues_nothing_on_bad_target(checks_on):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    logits, target, off = _small(1)
+    T, V = logits.shape
+    S = off.size - 1
+    logp, _, lse = dart.dart_tok_stats(logits, _cuda(target))
+    bad = target.copy()
+    bad[-1] = V
+    v = [torch.randn(T, device="cuda") for _ in range(3)]
+    loss = torch.full((1,), 123.0, dtype=torch.float64, device="cuda")
+    dz = torch.full((T, V), 7.0, device="cuda")
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_tis_loss_fwd_bwd(logits, _cuda(bad), logp, lse, *v, _cuda(off),
+                                   _cuda(np.ones(S, np.uint8)), 0.2, 0.28, 2.0, dlogits=dz,
+                                   loss=loss)
+    _invalid(e)
+    torch.cuda.synchronize()
+    assert loss.item() == 123.0 and bool(torch.all(dz == 7.0))
+
+
+def test_lmhead_target(checks_on):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 8, 64, 300
+    h = torch.randn(T, d, device="cuda").to(torch.bfloat16)
+    w = torch.randn(V, d, device="cuda").to(torch.bfloat16)
+    y = np.arange(T, dtype=np.int32)
+    y[3] = V
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_lmhead_tok_stats(h, w, _cuda(y))
+    _invalid(e)
+
+
+def test_valid_inputs_unchanged(monkeypatch):
+    """The same valid call with and without checks: bit-identical outputs."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    logits, target, off = _small(2)
+    S = off.size - 1
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("DART_CHECK", flag)
+        logp, ent, lse = dart.dart_tok_stats(logits, _cuda(target))
+        sh, mask, nk = dart.dart_step_select(ent, _cuda(off), 0.6)
+        lp_old = logp + 0.01
+        loss, dz, coef, st = dart.dart_tis_loss_fwd_bwd(
+            logits, _cuda(target), logp, lse, lp_old, lp_old, torch.ones_like(logp), _cuda(off),
+            mask, 0.2, 0.28, 2.0)
+        torch.cuda.synchronize()
+        outs.append([x.cpu() for x in (logp, ent, lse, sh, mask, nk, loss, dz, coef)])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    assert int(outs[0][5].item()) == dart.dart_kept_steps(S, 0.6)
