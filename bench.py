@@ -94,8 +94,15 @@ def cpu_baseline(wl, threads):
         oracle.dlogits(z[r0:r1], wl.target[r0:r1], lse[r0:r1], logp[r0:r1], res["g"][r0:r1],
                        nthreads=threads)
     dt = time.perf_counter() - t0
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                         None)
+    except OSError:
+        pass
     return {"value": wl.T * wl.V / dt, "unit": "logit elements/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt, 3),
+            "kind": "oracle", "seconds": round(dt, 3), "cpu_model": model,
             "sample": f"whole workload ({wl.T} rows x {wl.V}), float64 C oracle, OpenMP over rows"}
 
 
