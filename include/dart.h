@@ -14,7 +14,9 @@
  * --------------------------------
  * - Array arguments are DEVICE pointers unless a comment says otherwise. The
  *   caller owns every buffer; the library allocates no memory and keeps no
- *   state between calls, so concurrent calls on different streams are safe.
+ *   state between calls, so concurrent calls on different streams are safe
+ *   (the one exception, dart_lmhead_backward, keeps a ROCm BLAS handle per
+ *   device and serialises its own calls).
  * - Every call is asynchronous on `stream` (0 = the null stream): it checks its
  *   scalar arguments on the host, enqueues its kernels and returns. Outputs are
  *   valid once the stream is synchronised. Device data (target ids in range,
