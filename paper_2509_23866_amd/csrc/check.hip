@@ -7,6 +7,8 @@
 
 #include <stdlib.h>
 
+#include <mutex>
+
 namespace {
 
 // Violation flags of the last validation on this device: bit 0 ids, bit 1
@@ -59,6 +61,10 @@ bool enabled() {
 
 dart_status_t run(hipStream_t stream, std::initializer_list<Item> items) {
     if (!enabled()) return DART_OK;
+    // one validation at a time in the process: the flags are shared by every
+    // call on a device
+    static std::mutex mu;
+    std::lock_guard<std::mutex> lock(mu);
     unsigned int* flags = nullptr;
     if (hipGetSymbolAddress(reinterpret_cast<void**>(&flags), HIP_SYMBOL(g_flags)) != hipSuccess)
         return DART_ERR_HIP;
