@@ -3,7 +3,7 @@
 // before the real kernels when DART_CHECK=1 so that malformed device data is
 // reported as DART_ERR_INVALID_ARG instead of being read out of range. The
 // calls synchronise the stream, so this is a debugging mode.
-#include "check.h"
+#include "internal.h"
 
 #include <stdlib.h>
 
@@ -65,6 +65,11 @@ dart_status_t run(hipStream_t stream, std::initializer_list<Item> items) {
     // call on a device
     static std::mutex mu;
     std::lock_guard<std::mutex> lock(mu);
+    // the flags of the stream's device
+    const int dev = stream_device(stream);
+    if (dev < 0) return DART_ERR_HIP;
+    DeviceGuard on_dev(dev);
+    if (!on_dev.ok) return DART_ERR_HIP;
     unsigned int* flags = nullptr;
     if (hipGetSymbolAddress(reinterpret_cast<void**>(&flags), HIP_SYMBOL(g_flags)) != hipSuccess)
         return DART_ERR_HIP;

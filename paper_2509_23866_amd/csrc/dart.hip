@@ -28,7 +28,7 @@
 
 #include <type_traits>
 
-#include "check.h"
+#include "internal.h"
 #include "dart.h"
 
 namespace {

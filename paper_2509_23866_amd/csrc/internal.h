@@ -1,5 +1,4 @@
-// libdart internal: the optional validation of device-side preconditions
-// (DART_CHECK=1 in the environment). Not part of the C ABI.
+// libdart internal helpers shared by its sources; not part of the C ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -9,6 +8,34 @@
 
 #include "dart.h"
 
+#pragma GCC visibility push(hidden)
+
+// Makes dev the current device for the caller's scope and restores the
+// previous one after.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) return;
+        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (ok) (void)hipSetDevice(prev);
+    }
+    DeviceGuard(const DeviceGuard&) = delete;
+    DeviceGuard& operator=(const DeviceGuard&) = delete;
+};
+
+// The device a stream belongs to (the current device for the null stream);
+// -1 on a HIP error.
+inline int stream_device(hipStream_t stream) {
+    int dev = -1;
+    if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess) return -1;
+    return dev;
+}
+
+// The optional validation of device-side preconditions (DART_CHECK=1 in the
+// environment).
 namespace dart_check {
 
 // One device array to validate.
@@ -33,3 +60,5 @@ __attribute__((visibility("hidden"))) dart_status_t run(hipStream_t stream,
                                                         std::initializer_list<Item> items);
 
 }  // namespace dart_check
+
+#pragma GCC visibility pop

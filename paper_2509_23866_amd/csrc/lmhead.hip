@@ -30,7 +30,7 @@
 #include <mutex>
 #include <type_traits>
 
-#include "check.h"
+#include "internal.h"
 #include "dart.h"
 
 namespace {
@@ -582,20 +582,6 @@ constexpr int kMaxDevices = 64;
 std::mutex g_blas_mu;
 rocblas_handle g_blas[kMaxDevices] = {};
 
-// Makes dev the current device for the caller's scope and restores the
-// previous one after.
-struct DeviceGuard {
-    int prev = -1;
-    bool ok = false;
-    explicit DeviceGuard(int dev) {
-        if (hipGetDevice(&prev) != hipSuccess) return;
-        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
-    }
-    ~DeviceGuard() {
-        if (ok) (void)hipSetDevice(prev);
-    }
-};
-
 // The handle of the current device (a handle belongs to the device current
 // when it is created), created on first use.
 rocblas_handle blas_handle(int dev) {
@@ -688,9 +674,8 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;
 
-    int dev = 0;
-    if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess)
-        return DART_ERR_HIP;
+    const int dev = stream_device(stream);
+    if (dev < 0) return DART_ERR_HIP;
     // the stream's device is current while the BLAS library works
     DeviceGuard on_dev(dev);
     if (!on_dev.ok) return DART_ERR_HIP;
