@@ -106,6 +106,32 @@ def cpu_baseline(wl, threads):
             "sample": f"whole workload ({wl.T} rows x {wl.V}), float64 C oracle, OpenMP over rows"}
 
 
+def graph_variant(step, stream, dev, n):
+    """The same step captured once into a HIP graph and replayed n times back to
+    back (one pair of events around the replays): the launch gaps a trainer
+    that replays a captured step would see. Never the headline."""
+    import torch
+
+    side = torch.cuda.Stream(device=dev)
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        step(s=side)
+    torch.cuda.synchronize(dev)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        step(s=side)
+    torch.cuda.synchronize(dev)
+    g.replay()
+    torch.cuda.synchronize(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(n):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    return {"ms_per_step": e0.elapsed_time(e1) / n, "replays": n}
+
+
 def lmhead_variant(wl, dev, stream, target, coef, n):
     """The LM head fused in (never the headline): statistics and gradients of
     the logits h W^T formed on the matrix cores, at this workload's T and V and
@@ -219,20 +245,20 @@ def main():
     eps_low, eps_high, C = float(np.float32(wl.eps_low)), float(np.float32(wl.eps_high)), float(np.float32(wl.C))
     stream = torch.cuda.current_stream(dev)
 
-    def step(ev=None):
+    def step(ev=None, s=stream):
         if ev:
-            ev[0].record(stream)
-        dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream)
+            ev[0].record(s)
+        dart.dart_tok_stats(logits, target, logp, ent, lse, stream=s)
         if ev:
-            ev[1].record(stream)
-        dart.dart_step_select(ent, off, wl.rho, step_H, mask, n_kept, stream=stream)
+            ev[1].record(s)
+        dart.dart_step_select(ent, off, wl.rho, step_H, mask, n_kept, stream=s)
         dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C,
-                               loss, coef, stats, stream=stream, workspace=workspace)
+                               loss, coef, stats, stream=s, workspace=workspace)
         if ev:
-            ev[2].record(stream)
-        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream)
+            ev[2].record(s)
+        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=s)
         if ev:
-            ev[3].record(stream)
+            ev[3].record(s)
 
     if args.calib_copy_mib:
         # a plain elementwise kernel that reads and writes exactly this many
@@ -321,6 +347,8 @@ def main():
         variants["stats_only"] = {"ms": stats_ms, "logit_elements_per_s": T * V / (stats_ms * 1e-3),
                                   "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
 
+    if not wl.inplace and not args.no_variants:
+        variants["hip_graph"] = graph_variant(step, stream, dev, args.steps)
     if not args.no_variants and T <= 16384:
         variants["lmhead_fused"] = lmhead_variant(wl, dev, stream, target, coef,
                                                   min(args.steps, 10))

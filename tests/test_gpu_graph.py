@@ -1,0 +1,72 @@
+"""The whole step captured into a HIP graph: every replay reproduces the eager
+result bit for bit, with eager work and synchronisations between replays (the
+library enqueues no memset, so nothing in the graph depends on one)."""
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+def _cuda(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.mark.parametrize("T", [700, 6000])  # one-workgroup and many-workgroup loss
+def test_graph_replays_match_eager(T):
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    V, S = 2048, 30
+    rng = np.random.default_rng(T)
+    logits = torch.from_numpy(rng.normal(0, 3, (T, V)).astype(np.float32)).cuda().to(torch.bfloat16)
+    target = _cuda(rng.integers(0, V, T).astype(np.int32))
+    off = _cuda(np.r_[0, np.sort(rng.choice(np.arange(1, T), S - 1, replace=False)), T].astype(np.int32))
+    logp0, _, _ = dart.dart_tok_stats(logits, target)
+    lp_old = logp0 + _cuda(rng.normal(0, 0.05, T).astype(np.float32))
+    lp_roll = lp_old + _cuda(rng.normal(0, 0.1, T).astype(np.float32))
+    adv = _cuda(rng.normal(0, 1, T).astype(np.float32))
+
+    def buffers():
+        f = lambda n: torch.empty(n, dtype=torch.float32, device="cuda")  # noqa: E731
+        return dict(logp=f(T), ent=f(T), lse=f(T), sh=f(S),
+                    mask=torch.empty(S, dtype=torch.uint8, device="cuda"),
+                    nk=torch.empty(1, dtype=torch.int32, device="cuda"),
+                    loss=torch.empty(1, dtype=torch.float64, device="cuda"), coef=f(T), st=f(4),
+                    ws=torch.empty(dart.dart_tis_loss_workspace_bytes(T), dtype=torch.uint8,
+                                   device="cuda"),
+                    dz=torch.empty_like(logits))
+
+    def step(b, s=None):
+        dart.dart_tok_stats(logits, target, b["logp"], b["ent"], b["lse"], stream=s)
+        dart.dart_step_select(b["ent"], off, 0.8, b["sh"], b["mask"], b["nk"], stream=s)
+        dart.dart_tis_loss_fwd(b["logp"], lp_old, lp_roll, adv, off, b["mask"], 0.2, 0.28, 2.0,
+                               b["loss"], b["coef"], b["st"], stream=s, workspace=b["ws"])
+        dart.dart_tis_grad(logits, target, b["logp"], b["lse"], b["coef"], b["dz"], stream=s)
+
+    eager = buffers()
+    step(eager)
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in eager.items() if k != "ws"}
+
+    gb = buffers()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(gb, side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        step(gb, side)
+    for rep in range(4):
+        for v in gb.values():
+            v.fill_(0)  # stale results must not survive into the check
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(gb[k].view(torch.uint8), v.view(torch.uint8)), (rep, k)
+        step(eager)  # eager work between replays
+        torch.cuda.synchronize()
