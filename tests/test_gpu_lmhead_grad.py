@@ -216,3 +216,28 @@ def test_lmhead_backward_vlm7b_shape():
         rw = max(rw, _check_product(got, dz64[:, sl].T @ h64, adz[:, sl].T @ np.abs(h64),
                                     f"dweight rows {v0}+"))
     H.log(f"lmhead backward vlm7b: dh {rh:.2e} dW {rw:.2e} of |dz||.|")
+
+
+def test_lmhead_caller_workspaces_contents_do_not_matter():
+    """Caller-provided workspaces filled with garbage give the same bits as
+    freshly allocated ones (statistics and backward)."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 300, 136, 2100
+    h, w, y, g = _problem(T, d, V)
+    hd, wd, yd, gd = _dev_bf16(h), _dev_bf16(w), _cuda(y), _cuda(g)
+    a = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    ws = torch.full((dart.dart_lmhead_stats_workspace_bytes(T, V),), 0xC3, dtype=torch.uint8,
+                    device="cuda")
+    b = dart.dart_lmhead_tok_stats(hd, wd, yd, workspace=ws)
+    for u, v in zip(a, b):
+        assert torch.equal(u.view(torch.int32), v.view(torch.int32))
+    logp, _, lse = a
+    dha, dwa = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
+    wsb = torch.full((dart.dart_lmhead_backward_workspace_bytes(128, V),), 0x7F, dtype=torch.uint8,
+                     device="cuda")
+    dhb, dwb = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128, workspace=wsb)
+    torch.cuda.synchronize()
+    assert torch.equal(dha, dhb) and torch.equal(dwa, dwb)
