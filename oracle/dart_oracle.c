@@ -19,8 +19,8 @@
  *                                        trainer's to the rollout policy, cap C)
  *   clipped surrogate .................. Eq. (1) and Eq. (2)
  *   gradient w.r.t. the logits ......... chain rule through log pi_theta in Eq. (2)
- * Readings where the paper is silent are listed in the design doc (R1..R12) and are
- * named at the point of use below.
+ * Where the paper is silent, the reading taken is stated at its point of use
+ * below.
  *
  * Inputs are the exact float32 / bfloat16 values the GPU sees, widened to
  * double. Build: gcc -O2 -fopenmp (no -ffast-math: IEEE semantics are kept). */
@@ -58,13 +58,13 @@ static double logit_at(const void* z, int dtype, int64_t ld, int64_t t, int64_t 
     return (double)f;
 }
 
-/* Sec. 4.3: p_v = softmax(z)_v, H = -sum_v p_v log p_v (nats, R10: natural log),
+/* Sec. 4.3: p_v = softmax(z)_v, H = -sum_v p_v log p_v (nats: the natural log),
  * and log pi(y) = z_y - log sum_v exp(z_v) for the target id y (Eq. 1 numerator).
  * The logits are first multiplied by inv_temp (an inverse sampling temperature;
  * 1 in the paper, App. A.4). Per row: (1) the maximum m; (2) e_v = exp(z_v - m)
  * and their sum s, so that lse = m + log s; (3) p_v = e_v / s and
  * log p_v = (z_v - m) - log s, summed into the entropy from its definition. A term with
- * p_v == 0 contributes 0 (R9: -inf logits allowed, 0 log 0 := 0). */
+ * p_v == 0 contributes 0 (a reading: -inf logits allowed, 0 log 0 := 0). */
 void oracle_token_stats_ex(const void* z, int dtype, int64_t nrows, int64_t V, int64_t ld,
                            const int32_t* target, double inv_temp, double* logp, double* H,
                            double* lse, int nthreads) {
@@ -113,7 +113,7 @@ void oracle_token_stats(const void* z, int dtype, int64_t nrows, int64_t V, int6
 /* Sec. 4.3: the step entropy is the mean of the token entropies over the
  * step's tokens (thought and action concatenated); step s = tokens
  * [off[s], off[s+1]). The mean is taken in double; the selection below decides
- * on it rounded to float32 (R4: the decision is taken in the kernel's
+ * on it rounded to float32 (a reading: the decision is taken in the kernel's
  * precision). */
 void oracle_step_entropy(const double* H, const int32_t* off, int64_t S, double* Hs,
                          float* Hs32) {
@@ -125,7 +125,7 @@ void oracle_step_entropy(const double* H, const int32_t* off, int64_t S, double*
     }
 }
 
-/* R3: number of kept steps k = ceil(rho * S), computed in double with a
+/* Reading: number of kept steps k = ceil(rho * S), computed in double with a
  * 1e-6 guard against representation error of rho (0.8 * 240 must give 192),
  * clamped to [0, S]. */
 int64_t oracle_kept_steps(int64_t S, double rho) {
@@ -135,7 +135,7 @@ int64_t oracle_kept_steps(int64_t S, double rho) {
     return (int64_t)k;
 }
 
-/* Sec. 4.3 / Eq. (2): keep the k highest-entropy steps of the group. R3: the
+/* Sec. 4.3 / Eq. (2): keep the k highest-entropy steps of the group. Reading: the
  * rank of step s counts the steps that beat it, a step with equal entropy and
  * a lower index beating it; s is kept iff its rank is below k. O(S^2), no
  * sorting. Returns k. */
@@ -173,14 +173,14 @@ static double kl_dlogp(int kl, double delta) {
     return 0.0;
 }
 
-/* Eq. (2), per token t of step s(t), as the loss L = -J (R15):
+/* Eq. (2), per token t of step s(t), as the loss L = -J (a reading):
  *   r  = pi_theta / pi_old            = exp(logp - lp_old)             (Eq. 1)
  *   w  = min(pi_old / pi_rollout, C)  = min(exp(lp_old - lp_roll), C)  (Sec. 4.4)
  *   u  = r A,  c = clip(r, 1 - eps_low, 1 + eps_high) A,  o = min(u, c)
  *   l_t = -M_s om_t (w o - beta kl_t)
  *   L  = sum_t l_t
- * om_t is the aggregation weight: 1/N with N the tokens of kept steps (R1,
- * default), 1/T over all tokens, or 1/(K |s|) for the mean over the K kept
+ * om_t is the aggregation weight: 1/N with N the tokens of kept steps (the
+ * default reading), 1/T over all tokens, or 1/(K |s|) for the mean over the K kept
  * steps of each step's token mean. With a step-level ratio (Eq. 1 written for
  * the whole action) r, w and A are taken per step: log r_s and log w_s are the
  * sum (product ratio) or mean (geometric-mean ratio) of the token log-ratios, A_s
@@ -188,10 +188,10 @@ static double kl_dlogp(int kl, double delta) {
  * step's w_s o_s.
  *   g_t = dL/dlogp_t = -M (om_t w d o/dlogp_t - om_t beta dkl_t/dlogp_t), where
  * d o / d logp_t = r A when u <= c (the unclipped branch is the minimum) and 0
- * when u > c (the clipped branch is a constant) (R6); in step mode the step
+ * when u > c (the clipped branch is a constant, a reading); in step mode the step
  * term differentiates through log r_s, whose derivative w.r.t. logp_t is 1
  * (product) or 1/|s| (geometric mean), and the step's weights sum to
- * Om_s = sum_{t in s} om_t. w, M, N, K are constants (R5). The KL term sits
+ * Om_s = sum_{t in s} om_t. w, M, N, K are constants (a reading). The KL term sits
  * inside the indicator and outside the TIS weight, as in Eq. (2).
  * boundary[t] = 1 marks tokens whose gate may legitimately differ between
  * precisions: A != 0 and the ratio within 1e-4 (relative) of a clip bound.
@@ -268,7 +268,7 @@ double oracle_tis_loss_ex(int64_t T, const double* logp, const float* lp_old,
             const double gt = -M * (om_obj * w * d_obj - om * beta * kld);
             if (ell) ell[t] = lt;
             if (g) g[t] = gt;
-            /* R6: the gate u <= c can flip between precisions only when the ratio sits
+            /* The gate u <= c can flip between precisions only when the ratio sits
              * at a clip bound (inside the range clip(r) = r and u == c exactly) */
             if (boundary)
                 boundary[t] = A != 0.0 && (fabs(r - (1.0 - eps_low)) <= 1e-4 * (1.0 - eps_low) ||
@@ -295,8 +295,8 @@ double oracle_tis_loss_ex(int64_t T, const double* logp, const float* lp_old,
     return ksum_value(&L);
 }
 
-/* The paper's default configuration: Eq. (2) without the KL term (R7),
- * per-token ratios (R2), token mean over kept tokens (R1); stats[4]. */
+/* The paper's default configuration: Eq. (2) without the KL term,
+ * per-token ratios, token mean over kept tokens (readings); stats[4]. */
 double oracle_tis_loss(int64_t T, const double* logp, const float* lp_old, const float* lp_roll,
                        const float* adv, const int32_t* off, int64_t S, const uint8_t* mask,
                        double eps_low, double eps_high, double C, double* g, double* ell,
@@ -343,7 +343,7 @@ void oracle_dlogits(const void* z, int dtype, int64_t nrows, int64_t V, int64_t 
  * step of its N trajectories, each step carrying its trajectory's reward R_i.
  * Over D: Rbar = (1/|D|) sum R, sigma^2 = (1/|D|) sum (R - Rbar)^2 (population
  * variance, as written), and every step (i, j) gets A = (R_i - Rbar) / sigma;
- * every token of the step carries it. R8-like guard: sigma == 0 (all rewards
+ * every token of the step carries it. A guard: sigma == 0 (all rewards
  * equal; the data manager excludes such groups) gives A = 0.
  * Layout: trajectories [grp_off[g], grp_off[g+1]) form group g; steps
  * [traj_off[i], traj_off[i+1]) form trajectory i; tokens [off[s], off[s+1])
