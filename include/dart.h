@@ -271,7 +271,7 @@ dart_status_t dart_grpo_advantage(const float* reward, int64_t n_traj,
 /* dart_step_select for G task groups in one call (one workgroup per group):
  * group g is steps [group_step_offsets[g], group_step_offsets[g+1]) and keeps
  * dart_kept_steps(S_g, rho) of its own steps, by the same rule (the paper selects
- * "within the group", Sec. 4.3). n_kept_steps: [G] int32 or NULL. Errors as
+ * each task group on its own, Sec. 4.3). n_kept_steps: [G] int32 or NULL. Errors as
  * dart_step_select; also INVALID_ARG for a null group_step_offsets, G < 1 or
  * G > S. */
 dart_status_t dart_step_select_groups(const float* entropy, int64_t T,

@@ -13,7 +13,7 @@
  *   token entropy and log-prob ........ Sec. 4.3 (definition of H_{t,i} and p)
  *                                        and Eq. (1) (the ratio's numerator)
  *   step entropy (mean over tokens) .... Sec. 4.3 (definition of H_t)
- *   high-entropy step mask ............. Sec. 4.3 ("top 80%" of steps) and the
+ *   high-entropy step mask ............. Sec. 4.3 (the highest-entropy 80% of steps) and the
  *                                        indicator of Eq. (2)
  *   TIS weight ......................... Sec. 4.4 (truncated ratio of the
  *                                        trainer's to the rollout policy, cap C)

@@ -194,7 +194,7 @@ def test_step_entropy_of_closed_form_rows():
 
 
 # --------------------------------------------------------------------------
-# step selection (Sec. 4.3 "top 80%" of steps; indicator of Eq. 2)
+# step selection (Sec. 4.3: the highest-entropy 80% of steps; indicator of Eq. 2)
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("rho,S,k", [(0.8, 240, 192), (0.8, 64, 52), (0.5, 16, 8),
