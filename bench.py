@@ -178,6 +178,15 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
     bwd_ms = timed(lambda: dart.dart_lmhead_backward(h, w, target, lse, logp, coef, chunk_rows=T,
                                                      dhidden=dh, dweight=dw, workspace=wsb,
                                                      stream=stream))
+    skip = dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    wss = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, T, skip),
+                      dtype=torch.uint8, device=dev)
+    skip_ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef,
+                                                         chunk_rows=T, flags=skip, dhidden=dh,
+                                                         dweight=dw, workspace=wss,
+                                                         stream=stream))
+    kept = int(torch.count_nonzero(coef).item())
+    del wss
     gemm_ms = timed(lambda: torch.matmul(h, w.t(), out=zbuf))
     tstats_ms = timed(lambda: dart.dart_tok_stats(zbuf, target, logp, ent, lse, stream=stream))
     flop = 2.0 * T * V * d
@@ -192,6 +201,7 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
         "stats_mfma_frac": tf(stats_ms) / peak,
         "dlogits_ms": dl_ms, "dlogits_TFLOPs": tf(dl_ms), "dlogits_mfma_frac": tf(dl_ms) / peak,
         "backward_ms": bwd_ms, "backward_chunk_rows": T, "backward_TFLOPs": tf(bwd_ms, 3),
+        "backward_skip_zero_rows_ms": skip_ms, "rows_with_gradient": kept,
         "library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
         "unfused_stats_ms": gemm_ms + tstats_ms,
         "logits_bytes_not_materialised": T * V * 2,

@@ -370,6 +370,44 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
  * only. */
 size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V);
 
+/* Flags of dart_lmhead_backward_ex. */
+enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u };
+
+/* dart_lmhead_backward with flags. Rows t with tok_coef[t] == 0 have
+ * dlogits = 0 (the step mask of Sec. 4.3 drops whole steps, and a clipped
+ * ratio in Eq. (2) has zero gradient), so they add nothing to dweight and
+ * their rows of dhidden are 0. With DART_LMHEAD_SKIP_ZERO_ROWS the call
+ * gathers the other rows (hidden rows, target, lse, logp, tok_coef) into the
+ * workspace, runs the chunked dlogits and GEMMs of dart_lmhead_backward over
+ * those rows only, and scatters their dhidden rows back; the rows it skipped
+ * are set to 0. The result equals dart_lmhead_backward's up to the order of
+ * the BLAS library's fp32 sums. Because the GEMM sizes depend on how many rows
+ * are kept, the call copies that count to the host and synchronises the
+ * stream once: it cannot run under graph capture. flags = 0 is
+ * dart_lmhead_backward exactly (asynchronous).
+ *   flags:      0 or DART_LMHEAD_SKIP_ZERO_ROWS; other bits are INVALID_ARG.
+ *   workspace:  device memory of at least
+ *               dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows,
+ *               flags) bytes, 16-byte aligned, owned by the caller; contents
+ *               on entry do not matter.
+ * Other arguments and errors: as for dart_lmhead_backward. */
+dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                      const void* weight, int64_t V, int64_t ld_w,
+                                      const int32_t* target, const float* lse, const float* logp,
+                                      const float* tok_coef, float* dhidden, int64_t ld_dh,
+                                      float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                      uint32_t flags, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/* Bytes of workspace dart_lmhead_backward_ex needs: with flags = 0 those of
+ * dart_lmhead_backward for min(chunk_rows, T) rows; with
+ * DART_LMHEAD_SKIP_ZERO_ROWS also room for T compact hidden rows (bf16), their
+ * fp32 dhidden, five [T] arrays and a counter, each part 256-byte aligned
+ * (about T * (6 d + 20) + min(chunk_rows, T) * ceil8(V) * 2). 0 for bad
+ * arguments or flags. Host only. */
+size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
+                                               int64_t chunk_rows, uint32_t flags);
+
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the
  * number of steps dart_step_select keeps (the guard absorbs the representation
  * error of rho: 0.8 * 240 gives 192). Returns -1 for S < 0 or rho outside

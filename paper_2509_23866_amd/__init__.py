@@ -32,12 +32,14 @@ DART_KL = {"none": 0, "k1": 1, "k2": 2, "k3": 3}
 DART_AGG = {"token_mean": 0, "token_mean_all": 1, "step_mean": 2}
 DART_RATIO = {"token": 0, "step_geomean": 1, "step_product": 2}
 DART_GRAD_SKIP_ZERO_ROWS = 1
+DART_LMHEAD_SKIP_ZERO_ROWS = 1
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
             "dart_lmhead_tok_stats", "dart_lmhead_stats_workspace_bytes", "dart_lmhead_dlogits",
-            "dart_lmhead_backward", "dart_lmhead_backward_workspace_bytes", "dart_kept_steps",
+            "dart_lmhead_backward", "dart_lmhead_backward_workspace_bytes",
+            "dart_lmhead_backward_ex", "dart_lmhead_backward_ex_workspace_bytes", "dart_kept_steps",
             "dart_status_string")
 
 
@@ -113,6 +115,13 @@ def load_library():
                                              _P, _I64, _P, _I64, _I64, _P, ctypes.c_size_t, _P]
         lib.dart_lmhead_backward_workspace_bytes.restype = ctypes.c_size_t
         lib.dart_lmhead_backward_workspace_bytes.argtypes = [_I64, _I64]
+        lib.dart_lmhead_backward_ex.restype = ctypes.c_int
+        lib.dart_lmhead_backward_ex.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P,
+                                                _P, _P, _I64, _P, _I64, _I64, ctypes.c_uint32, _P,
+                                                ctypes.c_size_t, _P]
+        lib.dart_lmhead_backward_ex_workspace_bytes.restype = ctypes.c_size_t
+        lib.dart_lmhead_backward_ex_workspace_bytes.argtypes = [_I64, _I64, _I64, _I64,
+                                                                ctypes.c_uint32]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
         lib.dart_status_string.restype = ctypes.c_char_p
@@ -500,6 +509,12 @@ def dart_lmhead_backward_workspace_bytes(chunk_rows: int, V: int) -> int:
     return int(load_library().dart_lmhead_backward_workspace_bytes(int(chunk_rows), int(V)))
 
 
+def dart_lmhead_backward_ex_workspace_bytes(T: int, d: int, V: int, chunk_rows: int,
+                                            flags: int) -> int:
+    return int(load_library().dart_lmhead_backward_ex_workspace_bytes(
+        int(T), int(d), int(V), int(chunk_rows), int(flags)))
+
+
 def _lmhead_common(hidden, weight, target, lse, logp, tok_coef):
     torch = _torch()
     _matrix_bf16("hidden", hidden)
@@ -533,12 +548,8 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
     return dlogits
 
 
-def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows=1024,
-                         dhidden=None, dweight=None, workspace="auto", stream=None):
-    """(dhidden float32 [T, d], dweight float32 [V, d]) of the loss through the LM
-    head, dlogits formed chunk_rows rows at a time in ``workspace`` ("auto" or a
-    uint8 device tensor of dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
-    bytes)."""
+def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk_rows,
+                     dhidden, dweight, workspace, stream):
     torch = _torch()
     dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
     chunk_rows = max(1, min(int(chunk_rows), T))
@@ -551,21 +562,47 @@ def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows
     if isinstance(workspace, str):
         if workspace != "auto":
             raise ValueError('workspace must be "auto" or a uint8 device tensor')
-        workspace = torch.empty(dart_lmhead_backward_workspace_bytes(chunk_rows, V),
-                                dtype=torch.uint8, device=dev)
+        nbytes = (dart_lmhead_backward_workspace_bytes(chunk_rows, V) if flags is None else
+                  dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags))
+        if nbytes == 0:
+            raise ValueError(f"{name}: bad sizes or flags")
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         if isinstance(stream, torch.cuda.Stream):
             workspace.record_stream(stream)
     if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8
             or workspace.device != dev or not workspace.is_contiguous()):
         raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
-    rc = load_library().dart_lmhead_backward(
-        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
-        target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-        dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0), chunk_rows,
-        workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+            target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
+            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0),
+            chunk_rows]
+    if flags is not None:
+        args.append(int(flags))
+    args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream)]
+    rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
-        raise DartError("dart_lmhead_backward", rc)
+        raise DartError(name, rc)
     return dhidden, dweight
+
+
+def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows=1024,
+                         dhidden=None, dweight=None, workspace="auto", stream=None):
+    """(dhidden float32 [T, d], dweight float32 [V, d]) of the loss through the LM
+    head, dlogits formed chunk_rows rows at a time in ``workspace`` ("auto" or a
+    uint8 device tensor of dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
+    bytes)."""
+    return _lmhead_backward("dart_lmhead_backward", None, hidden, weight, target, lse, logp,
+                            tok_coef, chunk_rows, dhidden, dweight, workspace, stream)
+
+
+def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk_rows=1024,
+                            flags=0, dhidden=None, dweight=None, workspace="auto", stream=None):
+    """dart_lmhead_backward with flags: DART_LMHEAD_SKIP_ZERO_ROWS runs the GEMMs
+    over the rows with tok_coef != 0 only (the call synchronises the stream once);
+    ``workspace`` is "auto" or a uint8 device tensor of
+    dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags) bytes."""
+    return _lmhead_backward("dart_lmhead_backward_ex", int(flags), hidden, weight, target, lse,
+                            logp, tok_coef, chunk_rows, dhidden, dweight, workspace, stream)
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

@@ -549,6 +549,81 @@ lmhead_merge_kernel(const float4* __restrict__ part, const float* __restrict__ z
 int64_t vocab_tiles(int64_t V) { return (V + LmCfg::BN - 1) / LmCfg::BN; }
 
 // Host-side argument rules shared by the LM-head entry points.
+// Rows whose coefficient is not 0, in increasing order: map[0 .. n) and
+// count[0] = n. One workgroup walks the rows 1024 at a time; the position of
+// each kept row is its wave's ballot prefix plus the earlier waves' counts.
+constexpr int kCompactThreads = 1024;
+__global__ void __launch_bounds__(kCompactThreads)
+compact_rows_kernel(const float* __restrict__ coef, int64_t T, int32_t* __restrict__ map,
+                    int32_t* __restrict__ count) {
+    __shared__ int wave_n[kCompactThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int64_t base = 0;
+    for (int64_t t0 = 0; t0 < T; t0 += kCompactThreads) {
+        const int64_t t = t0 + tid;
+        const bool keep = t < T && coef[t] != 0.f;
+        const uint64_t ballot = __ballot(keep);
+        const int before = __popcll(ballot & ((uint64_t(1) << lane) - 1));
+        if (lane == 0) wave_n[wave] = __popcll(ballot);
+        __syncthreads();
+        int off = 0, total = 0;
+        for (int w = 0; w < kCompactThreads / 64; ++w) {
+            off += w < wave ? wave_n[w] : 0;
+            total += wave_n[w];
+        }
+        if (keep) map[base + off + before] = (int32_t)t;
+        base += total;
+        __syncthreads();
+    }
+    if (tid == 0) count[0] = (int32_t)base;
+}
+
+// Row i < count of the compact problem: hidden row map[i] and its per-row
+// values, one workgroup per row (grid-stride over the rows).
+__global__ void __launch_bounds__(64)
+gather_rows_kernel(const int32_t* __restrict__ map, const int32_t* __restrict__ count,
+                   const uint16_t* __restrict__ h, int64_t ld_h, int64_t d,
+                   const int32_t* __restrict__ target, const float* __restrict__ lse,
+                   const float* __restrict__ logp, const float* __restrict__ coef,
+                   uint16_t* __restrict__ h_c, int32_t* __restrict__ target_c,
+                   float* __restrict__ lse_c, float* __restrict__ logp_c, float* __restrict__ coef_c) {
+    const int64_t n = count[0];
+    for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+        const int64_t t = map[i];
+        const u32x4* src = reinterpret_cast<const u32x4*>(h + t * ld_h);
+        u32x4* dst = reinterpret_cast<u32x4*>(h_c + i * d);
+        for (int64_t j = threadIdx.x; j < d / 8; j += 64) dst[j] = src[j];
+        if (threadIdx.x == 0) {
+            target_c[i] = target[t];
+            lse_c[i] = lse[t];
+            logp_c[i] = logp[t];
+            coef_c[i] = coef[t];
+        }
+    }
+}
+
+// Rows [0, rows) of a row-major fp32 matrix set to 0 (columns [0, cols)).
+__global__ void __launch_bounds__(256)
+zero_rows_kernel(float* __restrict__ m, int64_t rows, int64_t cols, int64_t ld) {
+    for (int64_t r = blockIdx.x; r < rows; r += gridDim.x)
+        for (int64_t c = threadIdx.x; c < cols; c += 256) m[r * ld + c] = 0.f;
+}
+
+// dh[map[i]] = dh_c[i] for i < count (grid-stride over the rows).
+__global__ void __launch_bounds__(256)
+scatter_rows_kernel(const int32_t* __restrict__ map, const int32_t* __restrict__ count,
+                    const float* __restrict__ dh_c, int64_t d, float* __restrict__ dh,
+                    int64_t ld_dh) {
+    const int64_t n = count[0];
+    for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+        const int64_t t = map[i];
+        for (int64_t c = threadIdx.x; c < d; c += 256) dh[t * ld_dh + c] = dh_c[i * d + c];
+    }
+}
+
+// Workgroups of the row kernels above: one per row up to this many.
+constexpr int64_t kRowBlocks = 65536;
+
 // The MFMA tile addresses its rows by 32-bit byte offsets from the tile's first
 // row: (BM - 1) rows of ld elements must stay below 2^31 bytes.
 constexpr int64_t kMaxLd = int64_t(1) << 22;
@@ -652,45 +727,53 @@ size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
     return (size_t)chunk_rows * (size_t)((V + 7) / 8 * 8) * 2;
 }
 
-dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
-                                   const void* weight, int64_t V, int64_t ld_w,
-                                   const int32_t* target, const float* lse, const float* logp,
-                                   const float* tok_coef, float* dhidden, int64_t ld_dh,
-                                   float* dweight, int64_t ld_dw, int64_t chunk_rows,
-                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
-    if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
-        return DART_ERR_INVALID_ARG;
-    if (ld_dh < d || ld_dw < d || chunk_rows < 1 ||
-        reinterpret_cast<uintptr_t>(workspace) % 16)
-        return DART_ERR_INVALID_ARG;
-    // the BLAS library takes 32-bit sizes and leading dimensions
-    const int64_t kI32 = 0x7FFFFFFFll;
-    if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
-    if (chunk_rows > T) chunk_rows = T;
-    if (workspace_bytes < dart_lmhead_backward_workspace_bytes(chunk_rows, V))
-        return DART_ERR_INVALID_ARG;
-    if (const dart_status_t ck = dart_check::run(
-            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
-        return ck;
+}  // extern "C"
 
-    const int dev = stream_device(stream);
-    if (dev < 0) return DART_ERR_HIP;
-    // the stream's device is current while the BLAS library works
-    DeviceGuard on_dev(dev);
-    if (!on_dev.ok) return DART_ERR_HIP;
-    std::lock_guard<std::mutex> lock(g_blas_mu);
-    rocblas_handle blas = blas_handle(dev);
-    if (!blas || rocblas_set_stream(blas, stream) != rocblas_status_success) return DART_ERR_HIP;
+namespace {
+
+// Workspace layout of the row-skipping backward (each part 256-byte aligned):
+// the dz chunk, then the compact hidden rows [T, d] bf16, the compact dh
+// [T, d] fp32, the compact target, lse, logp and coefficient [T] each, the
+// row map [T] and the row count.
+struct SkipLayout {
+    size_t dz, h_c, dh_c, target_c, lse_c, logp_c, coef_c, map, count, total;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+SkipLayout skip_layout(int64_t T, int64_t d, int64_t V, int64_t chunk_rows) {
+    SkipLayout L;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o = align256(o + bytes);
+        return at;
+    };
+    L.dz = take((size_t)chunk_rows * (size_t)((V + 7) / 8 * 8) * 2);
+    L.h_c = take((size_t)T * (size_t)d * 2);
+    L.dh_c = take((size_t)T * (size_t)d * 4);
+    L.target_c = take((size_t)T * 4);
+    L.lse_c = take((size_t)T * 4);
+    L.logp_c = take((size_t)T * 4);
+    L.coef_c = take((size_t)T * 4);
+    L.map = take((size_t)T * 4);
+    L.count = take(16);
+    L.total = o;
+    return L;
+}
+
+// dlogits of rows [0, T) chunk by chunk, each followed by the two GEMMs.
+dart_status_t backward_rows(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
+                            int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
+                            const int32_t* target, const float* lse, const float* logp,
+                            const float* coef, float* dhidden, int64_t ld_dh, float* dweight,
+                            int64_t ld_dw, int64_t chunk_rows, uint16_t* dz, hipStream_t stream) {
     const int64_t ld_dz = (V + 7) / 8 * 8;
-    uint16_t* dz = static_cast<uint16_t*>(workspace);
-    const uint16_t* h = static_cast<const uint16_t*>(hidden);
-    const uint16_t* w = static_cast<const uint16_t*>(weight);
     const float one = 1.f, zero = 0.f;
     for (int64_t r0 = 0; r0 < T; r0 += chunk_rows) {
         const int64_t rows = T - r0 < chunk_rows ? T - r0 : chunk_rows;
         dart_status_t st = launch_dlogits(h + r0 * ld_h, rows, d, ld_h, w, V, ld_w, target + r0,
-                                          lse + r0, logp + r0, tok_coef + r0, dz, ld_dz, stream);
+                                          lse + r0, logp + r0, coef + r0, dz, ld_dz, stream);
         if (st != DART_OK) return st;
         // rocBLAS is column-major: a row-major [R, C] matrix with row stride ld
         // is its column-major [C, R] transpose with leading dimension ld.
@@ -714,6 +797,110 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
             return DART_ERR_HIP;
     }
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
+                                               int64_t chunk_rows, uint32_t flags) {
+    if (T < 1 || d < 1 || V < 1 || chunk_rows < 1 || T > 0x7FFFFFFFll || d > 0x7FFFFFFFll ||
+        V > 0x7FFFFFFFll || (flags & ~DART_LMHEAD_SKIP_ZERO_ROWS))
+        return 0;
+    if (chunk_rows > T) chunk_rows = T;
+    if (!(flags & DART_LMHEAD_SKIP_ZERO_ROWS))
+        return dart_lmhead_backward_workspace_bytes(chunk_rows, V);
+    return skip_layout(T, d, V, chunk_rows).total;
+}
+
+dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                      const void* weight, int64_t V, int64_t ld_w,
+                                      const int32_t* target, const float* lse, const float* logp,
+                                      const float* tok_coef, float* dhidden, int64_t ld_dh,
+                                      float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                      uint32_t flags, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+    if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
+        return DART_ERR_INVALID_ARG;
+    if (ld_dh < d || ld_dw < d || chunk_rows < 1 || (flags & ~DART_LMHEAD_SKIP_ZERO_ROWS) ||
+        reinterpret_cast<uintptr_t>(workspace) % 16)
+        return DART_ERR_INVALID_ARG;
+    // the BLAS library takes 32-bit sizes and leading dimensions
+    const int64_t kI32 = 0x7FFFFFFFll;
+    if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
+    if (chunk_rows > T) chunk_rows = T;
+    if (workspace_bytes < dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags))
+        return DART_ERR_INVALID_ARG;
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
+        return ck;
+
+    const int dev = stream_device(stream);
+    if (dev < 0) return DART_ERR_HIP;
+    // the stream's device is current while the BLAS library works
+    DeviceGuard on_dev(dev);
+    if (!on_dev.ok) return DART_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_blas_mu);
+    rocblas_handle blas = blas_handle(dev);
+    if (!blas || rocblas_set_stream(blas, stream) != rocblas_status_success) return DART_ERR_HIP;
+    const uint16_t* h = static_cast<const uint16_t*>(hidden);
+    const uint16_t* w = static_cast<const uint16_t*>(weight);
+    char* ws = static_cast<char*>(workspace);
+    if (!(flags & DART_LMHEAD_SKIP_ZERO_ROWS))
+        return backward_rows(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef,
+                             dhidden, ld_dh, dweight, ld_dw, chunk_rows,
+                             reinterpret_cast<uint16_t*>(ws), stream);
+
+    // rows with a zero coefficient have dz = 0: they add nothing to dW and
+    // their rows of dh are 0, so the GEMMs run over the other rows only
+    const SkipLayout L = skip_layout(T, d, V, chunk_rows);
+    int32_t* map = reinterpret_cast<int32_t*>(ws + L.map);
+    int32_t* count = reinterpret_cast<int32_t*>(ws + L.count);
+    uint16_t* h_c = reinterpret_cast<uint16_t*>(ws + L.h_c);
+    float* dh_c = reinterpret_cast<float*>(ws + L.dh_c);
+    int32_t* target_c = reinterpret_cast<int32_t*>(ws + L.target_c);
+    float* lse_c = reinterpret_cast<float*>(ws + L.lse_c);
+    float* logp_c = reinterpret_cast<float*>(ws + L.logp_c);
+    float* coef_c = reinterpret_cast<float*>(ws + L.coef_c);
+    hipLaunchKernelGGL(compact_rows_kernel, dim3(1), dim3(kCompactThreads), 0, stream, tok_coef,
+                       T, map, count);
+    const unsigned row_blocks = (unsigned)(T < kRowBlocks ? T : kRowBlocks);
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(row_blocks), dim3(64), 0, stream, map, count, h,
+                       ld_h, d, target, lse, logp, tok_coef, h_c, target_c, lse_c, logp_c, coef_c);
+    hipLaunchKernelGGL(zero_rows_kernel, dim3(row_blocks), dim3(256), 0, stream, dhidden, T, d,
+                       ld_dh);
+    if (hipGetLastError() != hipSuccess) return DART_ERR_HIP;
+    // the GEMM sizes are host values: wait for the count
+    int32_t n = 0;
+    if (hipMemcpyAsync(&n, count, sizeof n, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+        return DART_ERR_HIP;
+    if (n == 0) {
+        const unsigned vb = (unsigned)(V < kRowBlocks ? V : kRowBlocks);
+        hipLaunchKernelGGL(zero_rows_kernel, dim3(vb), dim3(256), 0, stream, dweight, V, d, ld_dw);
+        return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+    }
+    const int64_t cr = chunk_rows < n ? chunk_rows : n;
+    const dart_status_t st = backward_rows(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c,
+                                           logp_c, coef_c, dh_c, d, dweight, ld_dw, cr,
+                                           reinterpret_cast<uint16_t*>(ws + L.dz), stream);
+    if (st != DART_OK) return st;
+    hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)(n < kRowBlocks ? n : kRowBlocks)),
+                       dim3(256), 0, stream, map, count, dh_c, d, dhidden, ld_dh);
+    return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                   const void* weight, int64_t V, int64_t ld_w,
+                                   const int32_t* target, const float* lse, const float* logp,
+                                   const float* tok_coef, float* dhidden, int64_t ld_dh,
+                                   float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return dart_lmhead_backward_ex(hidden, T, d, ld_h, weight, V, ld_w, target, lse, logp,
+                                   tok_coef, dhidden, ld_dh, dweight, ld_dw, chunk_rows, 0u,
+                                   workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

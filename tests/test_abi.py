@@ -283,3 +283,42 @@ def test_lmhead_leading_dimension_limit():
     assert lib.dart_lmhead_tok_stats(*_lm_args(ld_h=big)) == dart.DART_ERR_UNSUPPORTED
     assert lib.dart_lmhead_tok_stats(*_lm_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
     assert lib.dart_lmhead_dlogits(*_lm_grad_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
+
+
+def _lm_bwd_ex_args(flags=0, **kw):
+    a = _lm_bwd_args(**kw)[:-1]
+    return a[:16] + [flags] + a[16:] + [None]
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(hidden=0), dict(weight=0), dict(target=0), dict(lse=0), dict(logp=0), dict(coef=0),
+    dict(dh=0), dict(dw=0), dict(workspace=0), dict(T=0), dict(V=0), dict(d=4, ld_h=4, ld_w=4),
+    dict(ld_dh=15), dict(ld_dw=8), dict(chunk=0), dict(ws_bytes=2 * 304 * 2 - 1),
+    dict(workspace=(1 << 22) + 8), dict(flags=2), dict(flags=1 << 31),
+    dict(flags=1, ws_bytes="one short"), dict(flags=1, ws_bytes=2 * 304 * 2),
+])
+def test_lmhead_backward_ex_rejects(kw):
+    """Bad arguments, unknown flags and a workspace too small for the row
+    compaction are INVALID_ARG before anything is enqueued."""
+    lib = dart.load_library()
+    if kw.get("ws_bytes") == "one short":
+        kw["ws_bytes"] = dart.dart_lmhead_backward_ex_workspace_bytes(4, 16, 300, 2, 1) - 1
+    assert lib.dart_lmhead_backward_ex(*_lm_bwd_ex_args(**kw)) == dart.DART_ERR_INVALID_ARG
+
+
+def test_lmhead_backward_ex_workspace_bytes():
+    """flags = 0 needs what dart_lmhead_backward needs; the row compaction adds
+    the compact hidden rows (bf16), their fp32 dhidden, five [T] int/float
+    arrays and a counter, each part rounded up to 256 bytes."""
+    f = dart.dart_lmhead_backward_ex_workspace_bytes
+    plain = dart.dart_lmhead_backward_workspace_bytes
+    up = lambda x: -(-x // 256) * 256
+    for T, d, V, chunk in ((4, 16, 300, 2), (4, 16, 300, 9), (4096, 3584, 152064, 1024),
+                           (5, 8, 7, 1)):
+        c = min(chunk, T)
+        assert f(T, d, V, chunk, 0) == plain(c, V)
+        want = (up(plain(c, V)) + up(T * d * 2) + up(T * d * 4) + 5 * up(T * 4) + up(16))
+        assert f(T, d, V, chunk, 1) == want
+    assert f(0, 16, 300, 2, 1) == 0 and f(4, 0, 300, 2, 1) == 0 and f(4, 16, 0, 2, 1) == 0
+    assert f(4, 16, 300, 0, 1) == 0 and f(4, 16, 300, 2, 2) == 0 and f(1 << 31, 16, 8, 1, 0) == 0

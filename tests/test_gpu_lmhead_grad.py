@@ -191,12 +191,16 @@ def test_lmhead_backward_vlm7b_shape():
     sn.fill_gaussian_device(wd, wl.seed, STREAM_WEIGHT, prob.sigma_w)
     yd = _cuda(wl.target.astype(np.int32))
     logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
-    dh, dw = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=1024)
+    gd = _cuda(g)
+    dh, dw = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=1024)
+    # the row-skipping backward: the GEMMs over the rows of R only
+    dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=1024,
+                                            flags=dart.DART_LMHEAD_SKIP_ZERO_ROWS)
     torch.cuda.synchronize()
-    dh = dh.cpu().numpy()
+    dh, dhs = dh.cpu().numpy(), dhs.cpu().numpy()
     outside = np.ones(T, bool)
     outside[R] = False
-    assert np.all(dh[outside] == 0.0)
+    assert np.all(dh[outside] == 0.0) and np.all(dhs[outside] == 0.0)
 
     hb = prob.hidden_bits(R)
     wb = sn.gaussian_bits_host(wl.seed, STREAM_WEIGHT, V, d, prob.sigma_w)
@@ -207,15 +211,19 @@ def test_lmhead_backward_vlm7b_shape():
     del z
     w64, h64 = oracle.bf16_bits_to_f64(wb), oracle.bf16_bits_to_f64(hb)
     adz = np.abs(dz64)
-    rh = _check_product(dh[R], dz64 @ w64, adz @ np.abs(w64), "dhidden")
+    ref_h, bound_h = dz64 @ w64, adz @ np.abs(w64)
+    rh = _check_product(dh[R], ref_h, bound_h, "dhidden")
+    rhs = _check_product(dhs[R], ref_h, bound_h, "dhidden (rows skipped)")
     del w64
-    rw = 0.0
+    rw = rws = 0.0
     for v0 in range(0, V, 16384):
         sl = slice(v0, min(V, v0 + 16384))
-        got = dw[sl].cpu().numpy()
-        rw = max(rw, _check_product(got, dz64[:, sl].T @ h64, adz[:, sl].T @ np.abs(h64),
-                                    f"dweight rows {v0}+"))
-    H.log(f"lmhead backward vlm7b: dh {rh:.2e} dW {rw:.2e} of |dz||.|")
+        ref, bound = dz64[:, sl].T @ h64, adz[:, sl].T @ np.abs(h64)
+        rw = max(rw, _check_product(dw[sl].cpu().numpy(), ref, bound, f"dweight rows {v0}+"))
+        rws = max(rws, _check_product(dws[sl].cpu().numpy(), ref, bound,
+                                      f"dweight rows {v0}+ (rows skipped)"))
+    H.log(f"lmhead backward vlm7b: dh {rh:.2e} dW {rw:.2e} of |dz||.|; "
+          f"rows skipped: dh {rhs:.2e} dW {rws:.2e}")
 
 
 def test_lmhead_caller_workspaces_contents_do_not_matter():
@@ -241,3 +249,105 @@ def test_lmhead_caller_workspaces_contents_do_not_matter():
     dhb, dwb = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128, workspace=wsb)
     torch.cuda.synchronize()
     assert torch.equal(dha, dhb) and torch.equal(dwa, dwb)
+
+
+def _ones_zeros(kind, rng, T):
+    g = (rng.uniform(-1.0, 1.0, T) * 1e-2).astype(np.float32)
+    if kind == "all_zero":
+        g[:] = 0.0
+    elif kind == "one_row":
+        g[np.arange(T) != T // 2] = 0.0
+    elif kind == "steps":
+        # whole runs of rows dropped, as the step mask drops whole steps
+        for a in range(0, T, 37):
+            if (a // 37) % 3 == 1:
+                g[a:a + 37] = 0.0
+    return g
+
+
+@pytest.mark.parametrize("T,d,V,pad,chunk,kind", [
+    (1, 8, 1, 0, 1, "dense"),
+    (1, 8, 5, 0, 1, "all_zero"),
+    (3, 8, 5, 0, 2, "one_row"),
+    (129, 72, 127, 8, 1024, "steps"),
+    (200, 200, 1000, 0, 64, "quarter"),
+    (300, 512, 16384, 0, 257, "steps"),
+    (1100, 136, 2000, 8, 100, "quarter"),
+    (257, 3584, 2000, 0, 100, "all_zero"),
+])
+def test_lmhead_backward_skip_zero_rows(T, d, V, pad, chunk, kind):
+    """dart_lmhead_backward_ex with DART_LMHEAD_SKIP_ZERO_ROWS against the
+    oracle at the bound of the dense backward, rows with g = 0 exactly 0, the
+    padding of dhidden untouched, and dweight 0 when every row is dropped. The
+    row compaction walks 1024 rows at a time, so T = 1100 spans two passes."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    h, w, y, _ = _problem(T, d, V)
+    rng = np.random.default_rng(T * 7 + d)
+    g = _ones_zeros(kind, rng, T) if kind != "quarter" else _coef(rng, T)
+    rlogp, _, rlse = oracle.lmhead_token_stats(h, w, y)
+    dz64, dh64, dw64 = oracle.lmhead_grads(h, w, y, rlse, rlogp, g)
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    hd, wd, yd = _dev_bf16(h, pad), _dev_bf16(w, pad), _cuda(y)
+    logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    dh = torch.full((T, d + 4), 3.0, dtype=torch.float32, device="cuda")
+    dw = torch.full((V, d), 12345.0, dtype=torch.float32, device="cuda")  # overwritten
+    flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),), 0xA5,
+                    dtype=torch.uint8, device="cuda")
+    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=chunk, flags=flags,
+                                 dhidden=dh[:, :d], dweight=dw, workspace=ws)
+    torch.cuda.synchronize()
+    got_h = dh[:, :d].cpu().numpy()
+    assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
+    assert np.all(got_h[g == 0.0] == 0.0), "a dropped row of dhidden is not 0"
+    if not np.any(g):
+        assert torch.all(dw == 0.0)
+    adz = np.abs(dz64)
+    rh = _check_product(got_h, dh64, adz @ np.abs(w64), "dhidden")
+    rw = _check_product(dw.cpu().numpy(), dw64, adz.T @ np.abs(h64), "dweight")
+    H.log(f"lmhead backward rows skipped T={T} d={d} V={V} chunk={chunk} {kind} "
+          f"({int(np.count_nonzero(g))} rows kept): dh {rh:.2e} dW {rw:.2e} of |dz||.|")
+
+
+def test_lmhead_backward_skip_zero_rows_reused_workspace():
+    """Two calls in a row on one workspace, the second keeping fewer rows: the
+    row map and count left by the first call do not leak into the second, and
+    flags = 0 of the _ex entry point gives dart_lmhead_backward's bits."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 600, 136, 2100
+    h, w, y, g = _problem(T, d, V)
+    hd, wd, yd = _dev_bf16(h), _dev_bf16(w), _cuda(y)
+    logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    ws = torch.empty((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, 128, flags),),
+                     dtype=torch.uint8, device="cuda")
+    g2 = g.copy()
+    g2[T // 3:] = 0.0
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    for gx in (g, g2):
+        gd = _cuda(gx)
+        dha, dwa = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
+        dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128,
+                                                flags=flags, workspace=ws)
+        dh0, dw0 = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128)
+        zbuf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
+        dz = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, dlogits=zbuf[:, :V])
+        dz = dz.double().cpu().numpy()
+        torch.cuda.synchronize()
+        assert torch.equal(dha, dh0) and torch.equal(dwa, dw0)
+        assert np.all(dhs.cpu().numpy()[gx == 0.0] == 0.0)
+        # both are products of the same bf16 dlogits, summed by the library in
+        # fp32 in different orders: each is within fp32 summation error of the
+        # exact product of those dlogits
+        adz = np.abs(dz)
+        for got, ref, bound in ((dhs, dz @ w64, adz @ np.abs(w64)),
+                                (dha, dz @ w64, adz @ np.abs(w64)),
+                                (dws, dz.T @ h64, adz.T @ np.abs(h64)),
+                                (dwa, dz.T @ h64, adz.T @ np.abs(h64))):
+            assert np.all(np.abs(got.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
