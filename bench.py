@@ -182,11 +182,28 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
     wss = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, T, skip),
                       dtype=torch.uint8, device=dev)
     skip_ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef,
-                                                         chunk_rows=T, flags=skip, dhidden=dh,
+                                                         chunk=T, flags=skip, dhidden=dh,
                                                          dweight=dw, workspace=wss,
                                                          stream=stream))
     kept = int(torch.count_nonzero(coef).item())
     del wss
+    # memory-bounded chunkings: the 512 MiB plan (vocabulary chunks when T < V),
+    # with fp32 and with bf16 gradients, and row chunks of 1024 for comparison
+    pchunk, pflags = dart.lmhead_backward_plan(T, V)
+    chunked = {}
+    for name, chunk, flags in (("plan_fp32", pchunk, pflags),
+                               ("plan_bf16", pchunk, pflags | dart.DART_LMHEAD_BF16_GRADS),
+                               ("rows_1024_fp32", 1024, 0)):
+        gdt = torch.bfloat16 if flags & dart.DART_LMHEAD_BF16_GRADS else torch.float32
+        dhx = torch.empty((T, d), dtype=gdt, device=dev)
+        dwx = torch.empty((V, d), dtype=gdt, device=dev)
+        wsx = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),
+                          dtype=torch.uint8, device=dev)
+        ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef, chunk=chunk,
+                                                        flags=flags, dhidden=dhx, dweight=dwx,
+                                                        workspace=wsx, stream=stream))
+        chunked[name] = {"chunk": chunk, "flags": flags, "workspace_bytes": wsx.numel(), "ms": ms}
+        del dhx, dwx, wsx
     gemm_ms = timed(lambda: torch.matmul(h, w.t(), out=zbuf))
     tstats_ms = timed(lambda: dart.dart_tok_stats(zbuf, target, logp, ent, lse, stream=stream))
     flop = 2.0 * T * V * d
@@ -202,6 +219,7 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
         "dlogits_ms": dl_ms, "dlogits_TFLOPs": tf(dl_ms), "dlogits_mfma_frac": tf(dl_ms) / peak,
         "backward_ms": bwd_ms, "backward_chunk_rows": T, "backward_TFLOPs": tf(bwd_ms, 3),
         "backward_skip_zero_rows_ms": skip_ms, "rows_with_gradient": kept,
+        "backward_chunked": chunked,
         "library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
         "unfused_stats_ms": gemm_ms + tstats_ms,
         "logits_bytes_not_materialised": T * V * 2,

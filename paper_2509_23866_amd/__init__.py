@@ -33,6 +33,8 @@ DART_AGG = {"token_mean": 0, "token_mean_all": 1, "step_mean": 2}
 DART_RATIO = {"token": 0, "step_geomean": 1, "step_product": 2}
 DART_GRAD_SKIP_ZERO_ROWS = 1
 DART_LMHEAD_SKIP_ZERO_ROWS = 1
+DART_LMHEAD_CHUNK_VOCAB = 2
+DART_LMHEAD_BF16_GRADS = 4
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
@@ -509,10 +511,10 @@ def dart_lmhead_backward_workspace_bytes(chunk_rows: int, V: int) -> int:
     return int(load_library().dart_lmhead_backward_workspace_bytes(int(chunk_rows), int(V)))
 
 
-def dart_lmhead_backward_ex_workspace_bytes(T: int, d: int, V: int, chunk_rows: int,
+def dart_lmhead_backward_ex_workspace_bytes(T: int, d: int, V: int, chunk: int,
                                             flags: int) -> int:
     return int(load_library().dart_lmhead_backward_ex_workspace_bytes(
-        int(T), int(d), int(V), int(chunk_rows), int(flags)))
+        int(T), int(d), int(V), int(chunk), int(flags)))
 
 
 def _lmhead_common(hidden, weight, target, lse, logp, tok_coef):
@@ -548,22 +550,24 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
     return dlogits
 
 
-def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk_rows,
-                     dhidden, dweight, workspace, stream):
+def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk, dhidden,
+                     dweight, workspace, stream):
     torch = _torch()
     dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
-    chunk_rows = max(1, min(int(chunk_rows), T))
-    dhidden = torch.empty((T, d), dtype=torch.float32, device=dev) if dhidden is None else dhidden
-    dweight = torch.empty((V, d), dtype=torch.float32, device=dev) if dweight is None else dweight
+    f = 0 if flags is None else int(flags)
+    chunk = max(1, min(int(chunk), V if f & DART_LMHEAD_CHUNK_VOCAB else T))
+    gdt = torch.bfloat16 if f & DART_LMHEAD_BF16_GRADS else torch.float32
+    dhidden = torch.empty((T, d), dtype=gdt, device=dev) if dhidden is None else dhidden
+    dweight = torch.empty((V, d), dtype=gdt, device=dev) if dweight is None else dweight
     for n, m, shape in (("dhidden", dhidden, (T, d)), ("dweight", dweight, (V, d))):
-        if (not isinstance(m, torch.Tensor) or m.dtype != torch.float32 or m.device != dev
+        if (not isinstance(m, torch.Tensor) or m.dtype != gdt or m.device != dev
                 or tuple(m.shape) != shape or m.stride(1) != 1):
-            raise ValueError(f"{n} must be a float32 {shape} tensor on {dev} with contiguous rows")
+            raise ValueError(f"{n} must be a {gdt} {shape} tensor on {dev} with contiguous rows")
     if isinstance(workspace, str):
         if workspace != "auto":
             raise ValueError('workspace must be "auto" or a uint8 device tensor')
-        nbytes = (dart_lmhead_backward_workspace_bytes(chunk_rows, V) if flags is None else
-                  dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags))
+        nbytes = (dart_lmhead_backward_workspace_bytes(chunk, V) if flags is None else
+                  dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, f))
         if nbytes == 0:
             raise ValueError(f"{name}: bad sizes or flags")
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -574,10 +578,9 @@ def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, c
         raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
     args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
             target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0),
-            chunk_rows]
+            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0), chunk]
     if flags is not None:
-        args.append(int(flags))
+        args.append(f)
     args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream)]
     rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
@@ -595,14 +598,32 @@ def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows
                             tok_coef, chunk_rows, dhidden, dweight, workspace, stream)
 
 
-def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk_rows=1024,
-                            flags=0, dhidden=None, dweight=None, workspace="auto", stream=None):
-    """dart_lmhead_backward with flags: DART_LMHEAD_SKIP_ZERO_ROWS runs the GEMMs
-    over the rows with tok_coef != 0 only (the call synchronises the stream once);
+def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk=1024, flags=0,
+                            dhidden=None, dweight=None, workspace="auto", stream=None):
+    """dart_lmhead_backward with flags (bitwise or):
+    DART_LMHEAD_CHUNK_VOCAB: ``chunk`` counts vocabulary entries, dlogits formed for
+    all rows and that many entries at a time (cheaper than row chunks when T < V);
+    DART_LMHEAD_BF16_GRADS: dhidden and dweight in bfloat16;
+    DART_LMHEAD_SKIP_ZERO_ROWS: the GEMMs over the rows with tok_coef != 0 only
+    (the call synchronises the stream once).
     ``workspace`` is "auto" or a uint8 device tensor of
-    dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags) bytes."""
+    dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags) bytes."""
     return _lmhead_backward("dart_lmhead_backward_ex", int(flags), hidden, weight, target, lse,
-                            logp, tok_coef, chunk_rows, dhidden, dweight, workspace, stream)
+                            logp, tok_coef, chunk, dhidden, dweight, workspace, stream)
+
+
+def lmhead_backward_plan(T: int, V: int, budget_bytes: int = 512 << 20):
+    """(chunk, flags) for dart_lmhead_backward_ex that keep the bf16 dlogits chunk
+    within budget_bytes: vocabulary chunks when T < V (only the [T, d] dhidden is
+    summed over chunks), else row chunks; chunks are whole 256-wide tiles where the
+    budget allows."""
+    T, V = int(T), int(V)
+    if T < V:
+        cols = max(256, budget_bytes // (2 * T) // 256 * 256)
+        return min(cols, V), DART_LMHEAD_CHUNK_VOCAB
+    row_bytes = 2 * ((V + 7) // 8 * 8)
+    rows = max(256, budget_bytes // row_bytes // 256 * 256)
+    return min(rows, T), 0
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

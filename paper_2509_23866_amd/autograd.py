@@ -14,13 +14,18 @@ only marshal tensors and scale the [T] coefficient.
 
     loss = dart_lmhead_policy_loss(hidden, weight, target, lp_old, lp_roll, adv,
                                    offsets, rho, eps_low, eps_high, C)
-    loss.backward()          # hidden.grad, weight.grad
+    loss.backward()          # hidden.grad, weight.grad (bfloat16)
+
+The LM-head backward writes its gradients in bfloat16 directly and, unless
+told otherwise, chunks the dlogits along the vocabulary when T < V (along the
+rows otherwise) within a 512 MiB workspace.
 """
 
 import torch
 
-from . import (dart_lmhead_backward, dart_lmhead_tok_stats, dart_step_select, dart_tis_grad,
-               dart_tis_loss_fwd, dart_tok_stats)
+from . import (DART_LMHEAD_BF16_GRADS, dart_lmhead_backward_ex, dart_lmhead_tok_stats,
+               dart_step_select, dart_tis_grad, dart_tis_loss_fwd, dart_tok_stats,
+               lmhead_backward_plan)
 
 
 def _scaled(coef, grad):
@@ -64,21 +69,32 @@ class DartLmHeadPolicyLoss(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, hidden, weight, target, logp_old, logp_rollout, adv, step_offsets, rho,
-                eps_low, eps_high, C, chunk_rows):
+                eps_low, eps_high, C, chunk, flags):
         hidden, weight = hidden.detach(), weight.detach()
         logp, ent, lse = dart_lmhead_tok_stats(hidden, weight, target)
         loss, coef = _loss(logp, ent, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
                            eps_high, C)
-        ctx.chunk_rows = chunk_rows
+        ctx.chunk, ctx.flags = lmhead_grad_plan(hidden.shape[0], weight.shape[0], chunk, flags)
         ctx.save_for_backward(hidden, weight, target, logp, lse, coef)
         return loss
 
     @staticmethod
     def backward(ctx, grad):
         hidden, weight, target, logp, lse, coef = ctx.saved_tensors
-        dh, dw = dart_lmhead_backward(hidden, weight, target, lse, logp, _scaled(coef, grad),
-                                      chunk_rows=ctx.chunk_rows)
-        return (dh.to(hidden.dtype), dw.to(weight.dtype)) + (None,) * 10
+        dh, dw = dart_lmhead_backward_ex(hidden, weight, target, lse, logp, _scaled(coef, grad),
+                                         chunk=ctx.chunk, flags=ctx.flags)
+        return (dh, dw) + (None,) * 11
+
+
+def lmhead_grad_plan(T, V, chunk=None, flags=None):
+    """(chunk, flags) the LM-head autograd backward passes to
+    dart_lmhead_backward_ex: the caller's, else lmhead_backward_plan's; always
+    with bfloat16 gradients."""
+    if chunk is None and flags is None:
+        chunk, flags = lmhead_backward_plan(T, V)
+    elif chunk is None or flags is None:
+        raise ValueError("give both chunk and flags, or neither")
+    return int(chunk), int(flags) | DART_LMHEAD_BF16_GRADS
 
 
 def dart_policy_loss(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
@@ -89,8 +105,9 @@ def dart_policy_loss(logits, target, logp_old, logp_rollout, adv, step_offsets, 
 
 
 def dart_lmhead_policy_loss(hidden, weight, target, logp_old, logp_rollout, adv, step_offsets,
-                            rho, eps_low, eps_high, C, chunk_rows=1024):
+                            rho, eps_low, eps_high, C, chunk=None, flags=None):
     """Differentiable DART loss of the LM head's inputs (see the module
-    docstring); the backward forms dlogits chunk_rows rows at a time."""
+    docstring); chunk and flags as for dart_lmhead_backward_ex (both None: the
+    default plan)."""
     return DartLmHeadPolicyLoss.apply(hidden, weight, target, logp_old, logp_rollout, adv,
-                                      step_offsets, rho, eps_low, eps_high, C, chunk_rows)
+                                      step_offsets, rho, eps_low, eps_high, C, chunk, flags)

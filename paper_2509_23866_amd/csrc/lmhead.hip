@@ -416,9 +416,10 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
 }
 
 // dlogits = g_t (onehot(y_t) - exp(z - lse_t)) for rows [0, M) of the chunk
-// (h and out already offset to the chunk's first row), written in bf16
-// (nearest even) to out [M, ld_out]: the gradient pass of the logits path
-// with the logits formed on the fly. The target element is
+// (h and out already offset to the chunk's first row) and the V vocabulary
+// entries vbase .. vbase + V - 1 (w already offset to entry vbase), written in
+// bf16 (nearest even) to out [M, ld_out]: the gradient pass of the logits
+// path with the logits formed on the fly. The target element is
 // g_t * -expm1(logp_t), accurate when p_y -> 1. The fp32 tile is staged
 // through LDS so that each row leaves as 16-byte vectors.
 template <class C>
@@ -427,7 +428,8 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
                       const uint16_t* __restrict__ w, int64_t V, int64_t ldw, int64_t d,
                       const int32_t* __restrict__ target, const float* __restrict__ lse,
                       const float* __restrict__ logp, const float* __restrict__ coef,
-                      uint16_t* __restrict__ out, int64_t ld_out, int64_t nmt, int64_t nvt) {
+                      uint16_t* __restrict__ out, int64_t ld_out, int64_t vbase, int64_t nmt,
+                      int64_t nvt) {
     __shared__ typename C::Smem sm;
     int64_t mt, vt;
     tile_of_block(nmt, nvt, mt, vt);
@@ -457,7 +459,7 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
             float4 rp = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
             if (t < M) {
                 const float g = coef[t];
-                const int64_t yrel = (int64_t)target[t] - n0;
+                const int64_t yrel = (int64_t)target[t] - vbase - n0;
                 rp = make_float4(-g, -lse[t] * 1.4426950408889634f, g * -expm1f(logp[t]),
                                  __int_as_float(yrel >= 0 && yrel < C::BN ? (int)yrel : -1));
             }
@@ -548,7 +550,6 @@ lmhead_merge_kernel(const float4* __restrict__ part, const float* __restrict__ z
 
 int64_t vocab_tiles(int64_t V) { return (V + LmCfg::BN - 1) / LmCfg::BN; }
 
-// Host-side argument rules shared by the LM-head entry points.
 // Rows whose coefficient is not 0, in increasing order: map[0 .. n) and
 // count[0] = n. One workgroup walks the rows 1024 at a time; the position of
 // each kept row is its wave's ballot prefix plus the earlier waves' counts.
@@ -602,23 +603,37 @@ gather_rows_kernel(const int32_t* __restrict__ map, const int32_t* __restrict__ 
     }
 }
 
-// Rows [0, rows) of a row-major fp32 matrix set to 0 (columns [0, cols)).
+// An element of a gradient output: fp32, or bf16 bits rounded to nearest even.
+__device__ __forceinline__ void put(float* p, float v) { *p = v; }
+__device__ __forceinline__ void put(uint16_t* p, float v) { *p = bf16_bits(v); }
+
+// Rows [0, rows) of a row-major matrix set to 0 (columns [0, cols)).
+template <class O>
 __global__ void __launch_bounds__(256)
-zero_rows_kernel(float* __restrict__ m, int64_t rows, int64_t cols, int64_t ld) {
+zero_rows_kernel(O* __restrict__ m, int64_t rows, int64_t cols, int64_t ld) {
     for (int64_t r = blockIdx.x; r < rows; r += gridDim.x)
-        for (int64_t c = threadIdx.x; c < cols; c += 256) m[r * ld + c] = 0.f;
+        for (int64_t c = threadIdx.x; c < cols; c += 256) put(m + r * ld + c, 0.f);
 }
 
 // dh[map[i]] = dh_c[i] for i < count (grid-stride over the rows).
+template <class O>
 __global__ void __launch_bounds__(256)
 scatter_rows_kernel(const int32_t* __restrict__ map, const int32_t* __restrict__ count,
-                    const float* __restrict__ dh_c, int64_t d, float* __restrict__ dh,
-                    int64_t ld_dh) {
+                    const float* __restrict__ dh_c, int64_t d, O* __restrict__ dh, int64_t ld_dh) {
     const int64_t n = count[0];
     for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
         const int64_t t = map[i];
-        for (int64_t c = threadIdx.x; c < d; c += 256) dh[t * ld_dh + c] = dh_c[i * d + c];
+        for (int64_t c = threadIdx.x; c < d; c += 256) put(dh + t * ld_dh + c, dh_c[i * d + c]);
     }
+}
+
+// dst[r, c] = bf16(src[r, c]) for rows [0, rows), columns [0, cols).
+__global__ void __launch_bounds__(256)
+to_bf16_kernel(const float* __restrict__ src, int64_t ld_src, int64_t rows, int64_t cols,
+               uint16_t* __restrict__ dst, int64_t ld_dst) {
+    for (int64_t r = blockIdx.x; r < rows; r += gridDim.x)
+        for (int64_t c = threadIdx.x; c < cols; c += 256)
+            dst[r * ld_dst + c] = bf16_bits(src[r * ld_src + c]);
 }
 
 // Workgroups of the row kernels above: one per row up to this many.
@@ -628,6 +643,7 @@ constexpr int64_t kRowBlocks = 65536;
 // row: (BM - 1) rows of ld elements must stay below 2^31 bytes.
 constexpr int64_t kMaxLd = int64_t(1) << 22;
 
+// Host-side argument rules shared by the LM-head entry points.
 bool bad_lmhead_args(const void* hidden, int64_t T, int64_t d, int64_t ld_h, const void* weight,
                      int64_t V, int64_t ld_w) {
     if (!hidden || !weight) return true;
@@ -640,13 +656,13 @@ bool bad_lmhead_args(const void* hidden, int64_t T, int64_t d, int64_t ld_h, con
 dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, int64_t ld_h,
                              const uint16_t* weight, int64_t V, int64_t ld_w,
                              const int32_t* target, const float* lse, const float* logp,
-                             const float* coef, uint16_t* out, int64_t ld_out,
+                             const float* coef, uint16_t* out, int64_t ld_out, int64_t vbase,
                              hipStream_t stream) {
     const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
     if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
-                       target, lse, logp, coef, out, ld_out, nmt, nvt);
+                       target, lse, logp, coef, out, ld_out, vbase, nmt, nvt);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
@@ -719,7 +735,7 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
 
     return launch_dlogits(static_cast<const uint16_t*>(hidden), T, d, ld_h,
                           static_cast<const uint16_t*>(weight), V, ld_w, target, lse, logp,
-                          tok_coef, static_cast<uint16_t*>(dlogits), ld_out, stream);
+                          tok_coef, static_cast<uint16_t*>(dlogits), ld_out, 0, stream);
 }
 
 size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
@@ -731,108 +747,194 @@ size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
 
 namespace {
 
-// Workspace layout of the row-skipping backward (each part 256-byte aligned):
-// the dz chunk, then the compact hidden rows [T, d] bf16, the compact dh
-// [T, d] fp32, the compact target, lse, logp and coefficient [T] each, the
-// row map [T] and the row count.
-struct SkipLayout {
-    size_t dz, h_c, dh_c, target_c, lse_c, logp_c, coef_c, map, count, total;
-};
+constexpr uint32_t kBackwardFlags =
+    DART_LMHEAD_SKIP_ZERO_ROWS | DART_LMHEAD_CHUNK_VOCAB | DART_LMHEAD_BF16_GRADS;
 
+int64_t ceil8(int64_t x) { return (x + 7) / 8 * 8; }
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-SkipLayout skip_layout(int64_t T, int64_t d, int64_t V, int64_t chunk_rows) {
-    SkipLayout L;
-    size_t o = 0;
+// How a backward call runs and where its parts sit in the workspace (byte
+// offsets, each part 256-byte aligned; total is the end of the last part).
+struct BackwardPlan {
+    bool vocab, bf16, skip;
+    int64_t chunk;    // rows (or vocabulary entries) per chunk, at most T (or V)
+    bool accumulate;  // a bf16 output summed over several chunks goes through fp32
+    size_t dz, acc, h_c, dh_c, target_c, lse_c, logp_c, coef_c, map, count, total;
+};
+
+// total = 0 when the sizes do not fit the address arithmetic.
+BackwardPlan plan_backward(int64_t T, int64_t d, int64_t V, int64_t chunk, uint32_t flags) {
+    BackwardPlan P = {};
+    P.vocab = flags & DART_LMHEAD_CHUNK_VOCAB;
+    P.bf16 = flags & DART_LMHEAD_BF16_GRADS;
+    P.skip = flags & DART_LMHEAD_SKIP_ZERO_ROWS;
+    const int64_t span = P.vocab ? V : T;
+    P.chunk = chunk < span ? chunk : span;
+    const int64_t nchunks = (span + P.chunk - 1) / P.chunk;
+    // dW is summed over row chunks and dh over vocabulary chunks; with rows
+    // skipped, dh is summed in the compact fp32 rows
+    P.accumulate = P.bf16 && nchunks > 1 && !(P.skip && P.vocab);
+    const double big = double(int64_t(1) << 60);
+    if ((double)T * (double)ceil8(V) * 2 > big || (double)V * (double)d * 4 > big ||
+        (double)T * (double)d * 6 > big)
+        return P;
+    size_t end = 0;
     auto take = [&](size_t bytes) {
-        const size_t at = o;
-        o = align256(o + bytes);
+        const size_t at = align256(end);
+        end = at + bytes;
         return at;
     };
-    L.dz = take((size_t)chunk_rows * (size_t)((V + 7) / 8 * 8) * 2);
-    L.h_c = take((size_t)T * (size_t)d * 2);
-    L.dh_c = take((size_t)T * (size_t)d * 4);
-    L.target_c = take((size_t)T * 4);
-    L.lse_c = take((size_t)T * 4);
-    L.logp_c = take((size_t)T * 4);
-    L.coef_c = take((size_t)T * 4);
-    L.map = take((size_t)T * 4);
-    L.count = take(16);
-    L.total = o;
-    return L;
+    P.dz = take(P.vocab ? (size_t)T * (size_t)ceil8(P.chunk) * 2
+                        : (size_t)P.chunk * (size_t)ceil8(V) * 2);
+    if (P.accumulate) P.acc = take((size_t)(P.vocab ? T : V) * (size_t)d * 4);
+    if (P.skip) {
+        P.h_c = take((size_t)T * (size_t)d * 2);
+        P.dh_c = take((size_t)T * (size_t)d * 4);
+        P.target_c = take((size_t)T * 4);
+        P.lse_c = take((size_t)T * 4);
+        P.logp_c = take((size_t)T * 4);
+        P.coef_c = take((size_t)T * 4);
+        P.map = take((size_t)T * 4);
+        P.count = take(4);
+    }
+    P.total = end;
+    return P;
 }
 
-// dlogits of rows [0, T) chunk by chunk, each followed by the two GEMMs.
-dart_status_t backward_rows(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
+// A gradient output: row-major, fp32 or bf16.
+struct Grad {
+    void* p;
+    int64_t ld;
+    bool bf16;
+    void* row(int64_t r) const {
+        return static_cast<char*>(p) + r * ld * (bf16 ? 2 : 4);
+    }
+};
+
+// rocBLAS is column-major: a row-major [R, C] matrix with row stride ld is
+// its column-major [C, R] transpose with leading dimension ld. Both products
+// take bf16 inputs and accumulate in fp32; accumulate adds to the output.
+// dh[rows, d] (+)= dz[rows, K] W[K, d]   <=>   dh^T = W^T dz^T
+bool gemm_dh(rocblas_handle blas, const uint16_t* dz, int64_t ld_dz, int64_t rows, int64_t K,
+             const uint16_t* w, int64_t ld_w, int64_t d, bool accumulate, const Grad& out) {
+    const float one = 1.f, zero = 0.f;
+    const rocblas_datatype ot = out.bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+    return rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)d,
+                           (rocblas_int)rows, (rocblas_int)K, &one, w, rocblas_datatype_bf16_r,
+                           (rocblas_int)ld_w, dz, rocblas_datatype_bf16_r, (rocblas_int)ld_dz,
+                           accumulate ? &one : &zero, out.p, ot, (rocblas_int)out.ld, out.p, ot,
+                           (rocblas_int)out.ld, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
+                           0, 0) == rocblas_status_success;
+}
+
+// dW[cols, d] (+)= dz[K, cols]^T h[K, d]   <=>   dW^T = h^T dz
+bool gemm_dw(rocblas_handle blas, const uint16_t* h, int64_t ld_h, int64_t K, const uint16_t* dz,
+             int64_t ld_dz, int64_t cols, int64_t d, bool accumulate, const Grad& out) {
+    const float one = 1.f, zero = 0.f;
+    const rocblas_datatype ot = out.bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+    return rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
+                           (rocblas_int)d, (rocblas_int)cols, (rocblas_int)K, &one, h,
+                           rocblas_datatype_bf16_r, (rocblas_int)ld_h, dz, rocblas_datatype_bf16_r,
+                           (rocblas_int)ld_dz, accumulate ? &one : &zero, out.p, ot,
+                           (rocblas_int)out.ld, out.p, ot, (rocblas_int)out.ld,
+                           rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0,
+                           0) == rocblas_status_success;
+}
+
+void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& dst,
+                    hipStream_t stream) {
+    const unsigned blocks = (unsigned)(rows < kRowBlocks ? rows : kRowBlocks);
+    hipLaunchKernelGGL(to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, src, cols, rows, cols,
+                       static_cast<uint16_t*>(dst.p), dst.ld);
+}
+
+// The gradient pass over rows [0, T) of h, in chunks of rows or of vocabulary
+// entries: per chunk, its dlogits into dz (bf16), then the two GEMMs. The
+// output summed over chunks (dW over rows, dh over vocabulary) is summed in
+// fp32: in the output itself, or in acc ([V, d] or [T, d]) when the output is
+// bf16 and there is more than one chunk, rounded to bf16 at the end. Each
+// element of the other output is one GEMM's result, rounded once.
+dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
                             int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
                             const int32_t* target, const float* lse, const float* logp,
-                            const float* coef, float* dhidden, int64_t ld_dh, float* dweight,
-                            int64_t ld_dw, int64_t chunk_rows, uint16_t* dz, hipStream_t stream) {
-    const int64_t ld_dz = (V + 7) / 8 * 8;
-    const float one = 1.f, zero = 0.f;
-    for (int64_t r0 = 0; r0 < T; r0 += chunk_rows) {
-        const int64_t rows = T - r0 < chunk_rows ? T - r0 : chunk_rows;
-        dart_status_t st = launch_dlogits(h + r0 * ld_h, rows, d, ld_h, w, V, ld_w, target + r0,
-                                          lse + r0, logp + r0, coef + r0, dz, ld_dz, stream);
-        if (st != DART_OK) return st;
-        // rocBLAS is column-major: a row-major [R, C] matrix with row stride ld
-        // is its column-major [C, R] transpose with leading dimension ld.
-        // dh[rows, d] = dz[rows, V] W[V, d]   <=>   dh^T = W^T dz^T
-        if (rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)d,
-                            (rocblas_int)rows, (rocblas_int)V, &one, w, rocblas_datatype_bf16_r,
-                            (rocblas_int)ld_w, dz, rocblas_datatype_bf16_r, (rocblas_int)ld_dz,
-                            &zero, dhidden + r0 * ld_dh, rocblas_datatype_f32_r,
-                            (rocblas_int)ld_dh, dhidden + r0 * ld_dh, rocblas_datatype_f32_r,
-                            (rocblas_int)ld_dh, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
-                            0, 0) != rocblas_status_success)
-            return DART_ERR_HIP;
-        // dW[V, d] (+)= dz^T[V, rows] h[rows, d]   <=>   dW^T = h^T dz
-        if (rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
-                            (rocblas_int)d, (rocblas_int)V, (rocblas_int)rows, &one, h + r0 * ld_h,
-                            rocblas_datatype_bf16_r, (rocblas_int)ld_h, dz,
-                            rocblas_datatype_bf16_r, (rocblas_int)ld_dz, r0 == 0 ? &zero : &one,
-                            dweight, rocblas_datatype_f32_r, (rocblas_int)ld_dw, dweight,
-                            rocblas_datatype_f32_r, (rocblas_int)ld_dw, rocblas_datatype_f32_r,
-                            rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
-            return DART_ERR_HIP;
+                            const float* coef, const Grad& dh, const Grad& dw, bool vocab,
+                            int64_t chunk, uint16_t* dz, float* acc, hipStream_t stream) {
+    if (!vocab) {
+        if (chunk > T) chunk = T;
+        const int64_t ld_dz = ceil8(V);
+        const bool via_acc = dw.bf16 && chunk < T;
+        const Grad sum = via_acc ? Grad{acc, d, false} : dw;
+        for (int64_t r0 = 0; r0 < T; r0 += chunk) {
+            const int64_t rows = T - r0 < chunk ? T - r0 : chunk;
+            const dart_status_t st =
+                launch_dlogits(h + r0 * ld_h, rows, d, ld_h, w, V, ld_w, target + r0, lse + r0,
+                               logp + r0, coef + r0, dz, ld_dz, 0, stream);
+            if (st != DART_OK) return st;
+            if (!gemm_dh(blas, dz, ld_dz, rows, V, w, ld_w, d, false,
+                         Grad{dh.row(r0), dh.ld, dh.bf16}) ||
+                !gemm_dw(blas, h + r0 * ld_h, ld_h, rows, dz, ld_dz, V, d, r0 > 0, sum))
+                return DART_ERR_HIP;
+        }
+        if (via_acc) launch_to_bf16(acc, V, d, dw, stream);
+    } else {
+        if (chunk > V) chunk = V;
+        const int64_t ld_dz = ceil8(chunk);
+        const bool via_acc = dh.bf16 && chunk < V;
+        const Grad sum = via_acc ? Grad{acc, d, false} : dh;
+        for (int64_t c0 = 0; c0 < V; c0 += chunk) {
+            const int64_t cols = V - c0 < chunk ? V - c0 : chunk;
+            const uint16_t* wc = w + c0 * ld_w;
+            const dart_status_t st = launch_dlogits(h, T, d, ld_h, wc, cols, ld_w, target, lse,
+                                                    logp, coef, dz, ld_dz, c0, stream);
+            if (st != DART_OK) return st;
+            if (!gemm_dh(blas, dz, ld_dz, T, cols, wc, ld_w, d, c0 > 0, sum) ||
+                !gemm_dw(blas, h, ld_h, T, dz, ld_dz, cols, d, false,
+                         Grad{dw.row(c0), dw.ld, dw.bf16}))
+                return DART_ERR_HIP;
+        }
+        if (via_acc) launch_to_bf16(acc, T, d, dh, stream);
     }
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+template <class O>
+void launch_zero_rows(void* m, int64_t rows, int64_t cols, int64_t ld, hipStream_t stream) {
+    const unsigned blocks = (unsigned)(rows < kRowBlocks ? rows : kRowBlocks);
+    hipLaunchKernelGGL(zero_rows_kernel<O>, dim3(blocks), dim3(256), 0, stream,
+                       static_cast<O*>(m), rows, cols, ld);
 }
 
 }  // namespace
 
 extern "C" {
 
-size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
-                                               int64_t chunk_rows, uint32_t flags) {
-    if (T < 1 || d < 1 || V < 1 || chunk_rows < 1 || T > 0x7FFFFFFFll || d > 0x7FFFFFFFll ||
-        V > 0x7FFFFFFFll || (flags & ~DART_LMHEAD_SKIP_ZERO_ROWS))
+size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t chunk,
+                                               uint32_t flags) {
+    if (T < 1 || d < 1 || V < 1 || chunk < 1 || T > 0x7FFFFFFFll || d > 0x7FFFFFFFll ||
+        V > 0x7FFFFFFFll || (flags & ~kBackwardFlags))
         return 0;
-    if (chunk_rows > T) chunk_rows = T;
-    if (!(flags & DART_LMHEAD_SKIP_ZERO_ROWS))
-        return dart_lmhead_backward_workspace_bytes(chunk_rows, V);
-    return skip_layout(T, d, V, chunk_rows).total;
+    return plan_backward(T, d, V, chunk, flags).total;
 }
 
 dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                       const void* weight, int64_t V, int64_t ld_w,
                                       const int32_t* target, const float* lse, const float* logp,
-                                      const float* tok_coef, float* dhidden, int64_t ld_dh,
-                                      float* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                      const float* tok_coef, void* dhidden, int64_t ld_dh,
+                                      void* dweight, int64_t ld_dw, int64_t chunk,
                                       uint32_t flags, void* workspace, size_t workspace_bytes,
                                       hipStream_t stream) {
     if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
     if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
         return DART_ERR_INVALID_ARG;
-    if (ld_dh < d || ld_dw < d || chunk_rows < 1 || (flags & ~DART_LMHEAD_SKIP_ZERO_ROWS) ||
+    if (ld_dh < d || ld_dw < d || chunk < 1 || (flags & ~kBackwardFlags) ||
         reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
     // the BLAS library takes 32-bit sizes and leading dimensions
     const int64_t kI32 = 0x7FFFFFFFll;
     if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
-    if (chunk_rows > T) chunk_rows = T;
-    if (workspace_bytes < dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, flags))
-        return DART_ERR_INVALID_ARG;
+    const BackwardPlan P = plan_backward(T, d, V, chunk, flags);
+    if (P.total == 0) return DART_ERR_UNSUPPORTED;
+    if (workspace_bytes < P.total) return DART_ERR_INVALID_ARG;
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;
@@ -848,29 +950,32 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     const uint16_t* h = static_cast<const uint16_t*>(hidden);
     const uint16_t* w = static_cast<const uint16_t*>(weight);
     char* ws = static_cast<char*>(workspace);
-    if (!(flags & DART_LMHEAD_SKIP_ZERO_ROWS))
-        return backward_rows(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef,
-                             dhidden, ld_dh, dweight, ld_dw, chunk_rows,
-                             reinterpret_cast<uint16_t*>(ws), stream);
+    uint16_t* dz = reinterpret_cast<uint16_t*>(ws + P.dz);
+    float* acc = P.accumulate ? reinterpret_cast<float*>(ws + P.acc) : nullptr;
+    const Grad dh{dhidden, ld_dh, P.bf16}, dw{dweight, ld_dw, P.bf16};
+    if (!P.skip)
+        return backward_core(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef, dh,
+                             dw, P.vocab, P.chunk, dz, acc, stream);
 
     // rows with a zero coefficient have dz = 0: they add nothing to dW and
     // their rows of dh are 0, so the GEMMs run over the other rows only
-    const SkipLayout L = skip_layout(T, d, V, chunk_rows);
-    int32_t* map = reinterpret_cast<int32_t*>(ws + L.map);
-    int32_t* count = reinterpret_cast<int32_t*>(ws + L.count);
-    uint16_t* h_c = reinterpret_cast<uint16_t*>(ws + L.h_c);
-    float* dh_c = reinterpret_cast<float*>(ws + L.dh_c);
-    int32_t* target_c = reinterpret_cast<int32_t*>(ws + L.target_c);
-    float* lse_c = reinterpret_cast<float*>(ws + L.lse_c);
-    float* logp_c = reinterpret_cast<float*>(ws + L.logp_c);
-    float* coef_c = reinterpret_cast<float*>(ws + L.coef_c);
+    int32_t* map = reinterpret_cast<int32_t*>(ws + P.map);
+    int32_t* count = reinterpret_cast<int32_t*>(ws + P.count);
+    uint16_t* h_c = reinterpret_cast<uint16_t*>(ws + P.h_c);
+    float* dh_c = reinterpret_cast<float*>(ws + P.dh_c);
+    int32_t* target_c = reinterpret_cast<int32_t*>(ws + P.target_c);
+    float* lse_c = reinterpret_cast<float*>(ws + P.lse_c);
+    float* logp_c = reinterpret_cast<float*>(ws + P.logp_c);
+    float* coef_c = reinterpret_cast<float*>(ws + P.coef_c);
     hipLaunchKernelGGL(compact_rows_kernel, dim3(1), dim3(kCompactThreads), 0, stream, tok_coef,
                        T, map, count);
     const unsigned row_blocks = (unsigned)(T < kRowBlocks ? T : kRowBlocks);
     hipLaunchKernelGGL(gather_rows_kernel, dim3(row_blocks), dim3(64), 0, stream, map, count, h,
                        ld_h, d, target, lse, logp, tok_coef, h_c, target_c, lse_c, logp_c, coef_c);
-    hipLaunchKernelGGL(zero_rows_kernel, dim3(row_blocks), dim3(256), 0, stream, dhidden, T, d,
-                       ld_dh);
+    if (P.bf16)
+        launch_zero_rows<uint16_t>(dhidden, T, d, ld_dh, stream);
+    else
+        launch_zero_rows<float>(dhidden, T, d, ld_dh, stream);
     if (hipGetLastError() != hipSuccess) return DART_ERR_HIP;
     // the GEMM sizes are host values: wait for the count
     int32_t n = 0;
@@ -878,17 +983,23 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
         hipStreamSynchronize(stream) != hipSuccess)
         return DART_ERR_HIP;
     if (n == 0) {
-        const unsigned vb = (unsigned)(V < kRowBlocks ? V : kRowBlocks);
-        hipLaunchKernelGGL(zero_rows_kernel, dim3(vb), dim3(256), 0, stream, dweight, V, d, ld_dw);
+        if (P.bf16)
+            launch_zero_rows<uint16_t>(dweight, V, d, ld_dw, stream);
+        else
+            launch_zero_rows<float>(dweight, V, d, ld_dw, stream);
         return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
     }
-    const int64_t cr = chunk_rows < n ? chunk_rows : n;
-    const dart_status_t st = backward_rows(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c,
-                                           logp_c, coef_c, dh_c, d, dweight, ld_dw, cr,
-                                           reinterpret_cast<uint16_t*>(ws + L.dz), stream);
+    const dart_status_t st =
+        backward_core(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c,
+                      Grad{dh_c, d, false}, dw, P.vocab, P.chunk, dz, acc, stream);
     if (st != DART_OK) return st;
-    hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)(n < kRowBlocks ? n : kRowBlocks)),
-                       dim3(256), 0, stream, map, count, dh_c, d, dhidden, ld_dh);
+    const unsigned nb = (unsigned)(n < kRowBlocks ? n : kRowBlocks);
+    if (P.bf16)
+        hipLaunchKernelGGL(scatter_rows_kernel<uint16_t>, dim3(nb), dim3(256), 0, stream, map,
+                           count, dh_c, d, static_cast<uint16_t*>(dhidden), ld_dh);
+    else
+        hipLaunchKernelGGL(scatter_rows_kernel<float>, dim3(nb), dim3(256), 0, stream, map, count,
+                           dh_c, d, static_cast<float*>(dhidden), ld_dh);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 

@@ -295,7 +295,7 @@ def _lm_bwd_ex_args(flags=0, **kw):
     dict(hidden=0), dict(weight=0), dict(target=0), dict(lse=0), dict(logp=0), dict(coef=0),
     dict(dh=0), dict(dw=0), dict(workspace=0), dict(T=0), dict(V=0), dict(d=4, ld_h=4, ld_w=4),
     dict(ld_dh=15), dict(ld_dw=8), dict(chunk=0), dict(ws_bytes=2 * 304 * 2 - 1),
-    dict(workspace=(1 << 22) + 8), dict(flags=2), dict(flags=1 << 31),
+    dict(workspace=(1 << 22) + 8), dict(flags=8), dict(flags=1 << 31),
     dict(flags=1, ws_bytes="one short"), dict(flags=1, ws_bytes=2 * 304 * 2),
 ])
 def test_lmhead_backward_ex_rejects(kw):
@@ -308,17 +308,45 @@ def test_lmhead_backward_ex_rejects(kw):
 
 
 def test_lmhead_backward_ex_workspace_bytes():
-    """flags = 0 needs what dart_lmhead_backward needs; the row compaction adds
-    the compact hidden rows (bf16), their fp32 dhidden, five [T] int/float
-    arrays and a counter, each part rounded up to 256 bytes."""
+    """The parts of the workspace, each starting at a multiple of 256 bytes: the
+    bf16 dlogits chunk; an fp32 accumulator for a bf16 output summed over
+    several chunks (dweight over row chunks, dhidden over vocabulary chunks,
+    none when skipped rows go with vocabulary chunks); the compact hidden rows
+    (bf16), their fp32 dhidden, five [T] int/float arrays and a counter. flags =
+    0 needs what dart_lmhead_backward needs."""
     f = dart.dart_lmhead_backward_ex_workspace_bytes
     plain = dart.dart_lmhead_backward_workspace_bytes
     up = lambda x: -(-x // 256) * 256
+    c8 = lambda x: -(-x // 8) * 8
+    SKIP, VOC, BF = dart.DART_LMHEAD_SKIP_ZERO_ROWS, dart.DART_LMHEAD_CHUNK_VOCAB, \
+        dart.DART_LMHEAD_BF16_GRADS
     for T, d, V, chunk in ((4, 16, 300, 2), (4, 16, 300, 9), (4096, 3584, 152064, 1024),
-                           (5, 8, 7, 1)):
-        c = min(chunk, T)
-        assert f(T, d, V, chunk, 0) == plain(c, V)
-        want = (up(plain(c, V)) + up(T * d * 2) + up(T * d * 4) + 5 * up(T * 4) + up(16))
-        assert f(T, d, V, chunk, 1) == want
+                           (5, 8, 7, 1), (300, 136, 2100, 512), (300, 136, 2100, 5000)):
+        for flags in range(8):
+            vocab, bf16, skip = bool(flags & VOC), bool(flags & BF), bool(flags & SKIP)
+            span = V if vocab else T
+            c = min(chunk, span)
+            parts = [T * c8(c) * 2 if vocab else c * c8(V) * 2]
+            if bf16 and -(-span // c) > 1 and not (skip and vocab):
+                parts.append((T if vocab else V) * d * 4)
+            if skip:
+                parts += [T * d * 2, T * d * 4] + [T * 4] * 5 + [4]
+            want = sum(up(x) for x in parts[:-1]) + parts[-1]
+            assert f(T, d, V, chunk, flags) == want, (T, d, V, chunk, flags)
+            if flags == 0:
+                assert want == plain(c, V)
     assert f(0, 16, 300, 2, 1) == 0 and f(4, 0, 300, 2, 1) == 0 and f(4, 16, 0, 2, 1) == 0
-    assert f(4, 16, 300, 0, 1) == 0 and f(4, 16, 300, 2, 2) == 0 and f(1 << 31, 16, 8, 1, 0) == 0
+    assert f(4, 16, 300, 0, 1) == 0 and f(4, 16, 300, 2, 8) == 0 and f(1 << 31, 16, 8, 1, 0) == 0
+
+
+def test_lmhead_backward_plan():
+    """Vocabulary chunks when T < V, row chunks otherwise, whole 256-wide tiles
+    within the byte budget."""
+    plan = dart.lmhead_backward_plan
+    c, fl = plan(4096, 152064)
+    assert fl == dart.DART_LMHEAD_CHUNK_VOCAB and c % 256 == 0 and 4096 * c * 2 <= 512 << 20
+    assert plan(500, 1000) == (1000, dart.DART_LMHEAD_CHUNK_VOCAB)
+    assert plan(4096, 1000) == (4096, 0)
+    c, fl = plan(152569, 152064)
+    assert fl == 0 and c % 256 == 0 and c * 152064 * 2 <= 512 << 20
+    assert plan(100, 50) == (100, 0)

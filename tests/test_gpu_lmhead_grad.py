@@ -78,6 +78,20 @@ def _check_product(got, ref, bound, name):
     return float((err / np.maximum(bound, 1e-300)).max())
 
 
+def _check_product_bf16(got, ref, bound, name):
+    """A bf16 gradient: the bound of the fp32 outputs plus the output's own
+    rounding (2^-9 |value|), with the same factor 2."""
+    got = got.float().cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    tol = BF16_REL * (bound + np.abs(ref)) + 1e-30
+    bad = err > tol
+    if np.any(bad):
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{name}: {bad.sum()} elements beyond 2^-8 (|dz||.| + |ref|); first "
+                             f"at {i}: got {got[i]!r} ref {ref[i]!r} bound {bound[i]!r}")
+    return float((err / np.maximum(bound + np.abs(ref), 1e-300)).max())
+
+
 SHAPES = [
     # (T, d, V, pad of the hidden / weight rows)
     (1, 8, 1, 0),
@@ -194,7 +208,7 @@ def test_lmhead_backward_vlm7b_shape():
     gd = _cuda(g)
     dh, dw = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=1024)
     # the row-skipping backward: the GEMMs over the rows of R only
-    dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=1024,
+    dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=1024,
                                             flags=dart.DART_LMHEAD_SKIP_ZERO_ROWS)
     torch.cuda.synchronize()
     dh, dhs = dh.cpu().numpy(), dhs.cpu().numpy()
@@ -297,7 +311,7 @@ def test_lmhead_backward_skip_zero_rows(T, d, V, pad, chunk, kind):
     flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS
     ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),), 0xA5,
                     dtype=torch.uint8, device="cuda")
-    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=chunk, flags=flags,
+    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk=chunk, flags=flags,
                                  dhidden=dh[:, :d], dweight=dw, workspace=ws)
     torch.cuda.synchronize()
     got_h = dh[:, :d].cpu().numpy()
@@ -333,9 +347,9 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
     for gx in (g, g2):
         gd = _cuda(gx)
         dha, dwa = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
-        dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128,
+        dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=128,
                                                 flags=flags, workspace=ws)
-        dh0, dw0 = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128)
+        dh0, dw0 = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=128)
         zbuf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
         dz = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, dlogits=zbuf[:, :V])
         dz = dz.double().cpu().numpy()
@@ -351,3 +365,96 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
                                 (dws, dz.T @ h64, adz.T @ np.abs(h64)),
                                 (dwa, dz.T @ h64, adz.T @ np.abs(h64))):
             assert np.all(np.abs(got.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
+
+
+_SKIP, _VOC, _BF = 1, 2, 4
+
+
+@pytest.mark.parametrize("T,d,V,pad,chunk,flags", [
+    (1, 8, 5, 0, 2, _VOC),
+    (129, 72, 127, 8, 64, _VOC),
+    (129, 72, 127, 8, 64, _VOC | _BF),
+    (300, 512, 16384, 0, 4096, _VOC | _BF),
+    (300, 512, 16384, 0, 1000, _VOC),
+    (257, 3584, 2000, 0, 777, _VOC | _BF),
+    (257, 3584, 2000, 0, 100, _BF),
+    (257, 3584, 2000, 0, 1024, _BF),
+    (1100, 136, 2000, 8, 256, _SKIP | _VOC),
+    (1100, 136, 2000, 8, 256, _SKIP | _VOC | _BF),
+    (1100, 136, 2000, 8, 300, _SKIP | _BF),
+    (200, 200, 1000, 0, 5000, _SKIP | _VOC | _BF),
+])
+def test_lmhead_backward_ex_modes(T, d, V, pad, chunk, flags):
+    """dart_lmhead_backward_ex in vocabulary chunks (ragged: chunk sizes that
+    are not whole tiles, a last chunk shorter than the others, one chunk
+    covering V), with bf16 gradients (summed over several chunks in fp32 first,
+    or written straight from a single chunk) and with zero rows skipped, each
+    against the oracle; padding of dhidden untouched; skipped rows exactly 0."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    h, w, y, g = _problem(T, d, V)
+    rlogp, _, rlse = oracle.lmhead_token_stats(h, w, y)
+    dz64, dh64, dw64 = oracle.lmhead_grads(h, w, y, rlse, rlogp, g)
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    hd, wd, yd = _dev_bf16(h, pad), _dev_bf16(w, pad), _cuda(y)
+    logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    gdt = torch.bfloat16 if flags & _BF else torch.float32
+    dh = torch.full((T, d + 4), 3.0, dtype=gdt, device="cuda")
+    dw = torch.full((V, d), 12345.0, dtype=gdt, device="cuda")  # overwritten
+    ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),), 0x5A,
+                    dtype=torch.uint8, device="cuda")
+    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk=chunk, flags=flags,
+                                 dhidden=dh[:, :d], dweight=dw, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
+    if flags & _SKIP:
+        assert torch.all(dh[:, :d][torch.from_numpy(g == 0.0).cuda()] == 0.0)
+    adz = np.abs(dz64)
+    bh, bw = adz @ np.abs(w64), adz.T @ np.abs(h64)
+    if flags & _BF:
+        rh = _check_product_bf16(dh[:, :d], dh64, bh, "dhidden")
+        rw = _check_product_bf16(dw, dw64, bw, "dweight")
+    else:
+        rh = _check_product(dh[:, :d].cpu().numpy(), dh64, bh, "dhidden")
+        rw = _check_product(dw.cpu().numpy(), dw64, bw, "dweight")
+    H.log(f"lmhead backward_ex T={T} d={d} V={V} chunk={chunk} flags={flags}: "
+          f"dh {rh:.2e} dW {rw:.2e}")
+
+
+def test_lmhead_backward_vocab_chunks_match_row_chunks():
+    """The same bf16 dlogits summed in another order: vocabulary and row chunks,
+    fp32 outputs, each within fp32 summation error of the exact products of
+    those dlogits; bf16 outputs equal the fp32 ones rounded, within one bf16
+    ulp."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 300, 256, 3000
+    h, w, y, g = _problem(T, d, V)
+    hd, wd, yd, gd = _dev_bf16(h), _dev_bf16(w), _cuda(y), _cuda(g)
+    logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    zbuf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
+    dz = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, dlogits=zbuf[:, :V])
+    dz = dz.double().cpu().numpy()
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    adz = np.abs(dz)
+    refs = ((dz @ w64, adz @ np.abs(w64)), (dz.T @ h64, adz.T @ np.abs(h64)))
+    runs = [dict(chunk=77, flags=0), dict(chunk=700, flags=_VOC), dict(chunk=256, flags=_VOC)]
+    outs = []
+    for kw in runs:
+        outs.append(dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, **kw))
+    bf = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=700, flags=_VOC | _BF)
+    torch.cuda.synchronize()
+    for got in outs:
+        for x, (ref, bound) in zip(got, refs):
+            assert np.all(np.abs(x.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
+    for xb, xf, (_, bound) in zip(bf, outs[1], refs):
+        # dweight is one GEMM per element; dhidden sums the chunks in fp32 and
+        # rounds once: both within one bf16 ulp of the fp32 result of the same
+        # chunking, up to the fp32 summation order of the library's kernels
+        a = xb.float().cpu().numpy().astype(np.float64)
+        b = xf.cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(a - b) <= 2.0 ** -8 * np.abs(b) + 1e-4 * bound + 1e-37)
