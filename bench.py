@@ -136,8 +136,11 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
     """The LM head fused in (never the headline): statistics and gradients of
     the logits h W^T formed on the matrix cores, at this workload's T and V and
     the 7B VLM's hidden size, with the headline step's own loss coefficients;
-    beside it the library GEMM that materialises the same logits. Per-launch
-    HIP events on the bench stream; medians of n launches after one warm-up."""
+    beside it the library GEMM that materialises the same logits. Above 16384
+    tokens the calls that need a whole [T, V] buffer (dlogits written whole,
+    the one-block backward, the library GEMM) are left out and every backward
+    runs in blocks within 512 MiB. Per-launch HIP events on the bench stream;
+    medians of n launches after one warm-up."""
     import numpy as np
     import torch
 
@@ -148,6 +151,7 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
 
     prob = synth.lmhead_problem(wl.name)
     T, V, d = wl.T, wl.V, prob.d
+    whole = T <= 16384
     bf = torch.bfloat16
     h = torch.empty((T, d), dtype=bf, device=dev)
     w = torch.empty((V, d), dtype=bf, device=dev)
@@ -155,10 +159,8 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
     sn.fill_gaussian_device(w, wl.seed, STREAM_WEIGHT, prob.sigma_w)
     logp, ent, lse = (torch.empty(T, dtype=torch.float32, device=dev) for _ in range(3))
     ws = torch.empty(dart.dart_lmhead_stats_workspace_bytes(T, V), dtype=torch.uint8, device=dev)
-    zbuf = torch.empty((T, V), dtype=bf, device=dev)
     dh = torch.empty((T, d), dtype=torch.float32, device=dev)
     dw = torch.empty((V, d), dtype=torch.float32, device=dev)
-    wsb = torch.empty(dart.dart_lmhead_backward_workspace_bytes(T, V), dtype=torch.uint8, device=dev)
 
     def timed(f):
         f()
@@ -171,59 +173,70 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
         torch.cuda.synchronize(dev)
         return float(np.median([a.elapsed_time(b) for a, b in ev]))
 
-    stats_ms = timed(lambda: dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, workspace=ws,
-                                                        stream=stream))
-    dl_ms = timed(lambda: dart.dart_lmhead_dlogits(h, w, target, lse, logp, coef, dlogits=zbuf,
-                                                   stream=stream))
-    bwd_ms = timed(lambda: dart.dart_lmhead_backward(h, w, target, lse, logp, coef, chunk_rows=T,
-                                                     dhidden=dh, dweight=dw, workspace=wsb,
-                                                     stream=stream))
-    skip = dart.DART_LMHEAD_SKIP_ZERO_ROWS
-    wss = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, T, skip),
-                      dtype=torch.uint8, device=dev)
-    skip_ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef,
-                                                         chunk=T, flags=skip, dhidden=dh,
-                                                         dweight=dw, workspace=wss,
-                                                         stream=stream))
-    kept = int(torch.count_nonzero(coef).item())
-    del wss
-    # memory-bounded chunkings: the 512 MiB plan (vocabulary chunks when T < V),
-    # with fp32 and with bf16 gradients, and row chunks of 1024 for comparison
-    pchunk, pflags = dart.lmhead_backward_plan(T, V)
-    chunked = {}
-    for name, chunk, flags in (("plan_fp32", pchunk, pflags),
-                               ("plan_bf16", pchunk, pflags | dart.DART_LMHEAD_BF16_GRADS),
-                               ("rows_1024_fp32", 1024, 0)):
-        gdt = torch.bfloat16 if flags & dart.DART_LMHEAD_BF16_GRADS else torch.float32
-        dhx = torch.empty((T, d), dtype=gdt, device=dev)
-        dwx = torch.empty((V, d), dtype=gdt, device=dev)
-        wsx = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),
-                          dtype=torch.uint8, device=dev)
-        ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef, chunk=chunk,
-                                                        flags=flags, dhidden=dhx, dweight=dwx,
-                                                        workspace=wsx, stream=stream))
-        chunked[name] = {"chunk": chunk, "flags": flags, "workspace_bytes": wsx.numel(), "ms": ms}
-        del dhx, dwx, wsx
-    gemm_ms = timed(lambda: torch.matmul(h, w.t(), out=zbuf))
-    tstats_ms = timed(lambda: dart.dart_tok_stats(zbuf, target, logp, ent, lse, stream=stream))
     flop = 2.0 * T * V * d
     peak = 2500.0  # dense bf16 MFMA, TFLOP/s
 
     def tf(ms, k=1):
         return k * flop / (ms * 1e-3) / 1e12
 
-    return {
-        "shape": {"T": T, "d": d, "V": V}, "flop_per_gemm": flop, "peak_TFLOPs": peak,
-        "stats_kernels_ms": stats_ms, "stats_TFLOPs": tf(stats_ms),
-        "stats_mfma_frac": tf(stats_ms) / peak,
-        "dlogits_ms": dl_ms, "dlogits_TFLOPs": tf(dl_ms), "dlogits_mfma_frac": tf(dl_ms) / peak,
-        "backward_ms": bwd_ms, "backward_chunk_rows": T, "backward_TFLOPs": tf(bwd_ms, 3),
-        "backward_skip_zero_rows_ms": skip_ms, "rows_with_gradient": kept,
-        "backward_chunked": chunked,
-        "library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
-        "unfused_stats_ms": gemm_ms + tstats_ms,
-        "logits_bytes_not_materialised": T * V * 2,
+    stats_ms = timed(lambda: dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, workspace=ws,
+                                                        stream=stream))
+    del ws
+    out = {"shape": {"T": T, "d": d, "V": V}, "flop_per_gemm": flop, "peak_TFLOPs": peak,
+           "stats_kernels_ms": stats_ms, "stats_TFLOPs": tf(stats_ms),
+           "stats_mfma_frac": tf(stats_ms) / peak,
+           "logits_bytes_not_materialised": T * V * 2}
+    if whole:
+        zbuf = torch.empty((T, V), dtype=bf, device=dev)
+        wsb = torch.empty(dart.dart_lmhead_backward_workspace_bytes(T, V), dtype=torch.uint8,
+                          device=dev)
+        dl_ms = timed(lambda: dart.dart_lmhead_dlogits(h, w, target, lse, logp, coef,
+                                                       dlogits=zbuf, stream=stream))
+        bwd_ms = timed(lambda: dart.dart_lmhead_backward(h, w, target, lse, logp, coef,
+                                                         chunk_rows=T, dhidden=dh, dweight=dw,
+                                                         workspace=wsb, stream=stream))
+        del wsb
+        out.update({"dlogits_ms": dl_ms, "dlogits_TFLOPs": tf(dl_ms),
+                    "dlogits_mfma_frac": tf(dl_ms) / peak, "backward_ms": bwd_ms,
+                    "backward_chunk_rows": T, "backward_TFLOPs": tf(bwd_ms, 3)})
+
+    kept = int(torch.count_nonzero(coef).item())
+
+    def blocked(rows, cols, flags):
+        gdt = torch.bfloat16 if flags & dart.DART_LMHEAD_BF16_GRADS else torch.float32
+        dhx = torch.empty((T, d), dtype=gdt, device=dev)
+        dwx = torch.empty((V, d), dtype=gdt, device=dev)
+        wsx = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, flags),
+                          dtype=torch.uint8, device=dev)
+        ms = timed(lambda: dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef,
+                                                        chunk_rows=rows, chunk_cols=cols,
+                                                        flags=flags, dhidden=dhx, dweight=dwx,
+                                                        workspace=wsx, stream=stream))
+        # three GEMM-equivalents over the rows the call forms
+        formed = kept / T if flags & dart.DART_LMHEAD_SKIP_ZERO_ROWS else 1.0
+        return {"chunk_rows": min(rows, T), "chunk_cols": min(cols, V), "flags": flags,
+                "workspace_bytes": wsx.numel(), "ms": ms, "TFLOPs": tf(ms, 3) * formed}
+
+    skip = dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    pr, pc = dart.lmhead_backward_plan(T, V)
+    sr, sc = (T, V) if whole else (pr, pc)
+    out["backward_skip_zero_rows"] = blocked(sr, sc, skip)
+    out["rows_with_gradient"] = kept
+    # memory-bounded blockings within 512 MiB of dlogits: the plan, with fp32
+    # and with bf16 gradients, and whole vocabulary rows in row chunks
+    rows_only = max(256, ((512 << 20) // (2 * ((V + 7) // 8 * 8))) // 256 * 256)
+    out["backward_chunked"] = {
+        "plan_fp32": blocked(pr, pc, 0),
+        "plan_bf16": blocked(pr, pc, dart.DART_LMHEAD_BF16_GRADS),
+        "rows_only_fp32": blocked(rows_only, V, 0),
     }
+    if whole:
+        gemm_ms = timed(lambda: torch.matmul(h, w.t(), out=zbuf))
+        tstats_ms = timed(lambda: dart.dart_tok_stats(zbuf, target, logp, ent, lse,
+                                                      stream=stream))
+        out.update({"library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
+                    "unfused_stats_ms": gemm_ms + tstats_ms})
+    return out
 
 
 def main():
@@ -376,7 +389,7 @@ def main():
 
     if not wl.inplace and not args.no_variants:
         variants["hip_graph"] = graph_variant(step, stream, dev, args.steps)
-    if not args.no_variants and T <= 16384:
+    if not args.no_variants:
         variants["lmhead_fused"] = lmhead_variant(wl, dev, stream, target, coef,
                                                   min(args.steps, 10))
 

@@ -371,35 +371,33 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
 size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V);
 
 /* Flags of dart_lmhead_backward_ex (bitwise or). */
-enum {
-    DART_LMHEAD_SKIP_ZERO_ROWS = 1u,
-    DART_LMHEAD_CHUNK_VOCAB = 2u,
-    DART_LMHEAD_BF16_GRADS = 4u
-};
+enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
 
-/* dart_lmhead_backward with flags; flags = 0 is dart_lmhead_backward exactly.
+/* dart_lmhead_backward in blocks of chunk_rows rows x chunk_cols vocabulary
+ * entries, with flags. dart_lmhead_backward(..., chunk_rows, ...) is this call
+ * with chunk_cols = V and flags = 0.
  *
- * DART_LMHEAD_CHUNK_VOCAB: `chunk` counts vocabulary entries instead of rows:
- * each chunk forms dlogits for all T rows and `chunk` entries of the
- * vocabulary (workspace T * ceil8(chunk) bf16), adds that chunk's share to
- * dhidden and writes that chunk's rows of dweight. With row chunks every
- * chunk reads and rewrites the whole [V, d] dweight; with vocabulary chunks
- * only the [T, d] dhidden is summed over chunks, which is the cheaper side
- * when T < V (a step group of a few thousand tokens against a vocabulary of
- * 152k). The GEMMs are those of dart_lmhead_backward.
+ * Each block forms its dlogits (bf16, in the workspace), adds its share to
+ * its rows of dhidden (summed over the vocabulary blocks) and to its entries'
+ * rows of dweight (summed over the row blocks), with the GEMMs of
+ * dart_lmhead_backward. Summing costs traffic: every row block reads and
+ * rewrites the [V, d] dweight, every vocabulary block the [T, d] dhidden. For
+ * a given workspace (chunk_rows * chunk_cols bf16) whole rows suit T >> V,
+ * whole vocabulary rows (chunk_rows = T) suit T << V, such as a step group of
+ * a few thousand tokens against a vocabulary of 152k, and square blocks suit
+ * T ~ V.
  *
  * DART_LMHEAD_BF16_GRADS: dhidden and dweight are bfloat16 (round to nearest
  * even) instead of float32, as an autograd caller needs them for bf16
- * parameters. The output summed over several chunks (dweight over row chunks,
- * dhidden over vocabulary chunks) is summed in float32 in the workspace and
- * rounded once at the end; every other element is one GEMM's fp32 result
- * rounded once.
+ * parameters. An output that several blocks add to is summed in float32 in the
+ * workspace and rounded once at the end; an element that one block writes is
+ * that GEMM's fp32 result rounded once.
  *
  * DART_LMHEAD_SKIP_ZERO_ROWS: rows t with tok_coef[t] == 0 have dlogits = 0
  * (the step mask of Sec. 4.3 drops whole steps, and a clipped ratio in
  * Eq. (2) has zero gradient), so they add nothing to dweight and their rows of
  * dhidden are 0. The call gathers the other rows (hidden rows, target, lse,
- * logp, tok_coef) into the workspace, runs the chunked backward over those
+ * logp, tok_coef) into the workspace, runs the blocked backward over those
  * rows only, and scatters their dhidden rows back; the rows it skipped are set
  * to 0. The result equals the dense call's up to the order of the BLAS
  * library's fp32 sums. Because the GEMM sizes depend on how many rows are
@@ -410,13 +408,13 @@ enum {
  *   dhidden:    [T, ld_dh] output, float32, or bfloat16 with
  *               DART_LMHEAD_BF16_GRADS; ld_dh >= d.
  *   dweight:    [V, ld_dw] output, as dhidden; ld_dw >= d; overwritten.
- *   chunk:      rows (or vocabulary entries) per chunk, >= 1; values above T
- *               (or V) are taken as T (or V).
- *   flags:      a combination of the three flags; other bits are INVALID_ARG.
+ *   chunk_rows, chunk_cols: the block, each >= 1; values above T (or V) are
+ *               taken as T (or V).
+ *   flags:      a combination of the two flags; other bits are INVALID_ARG.
  *   workspace:  device memory of at least
- *               dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags)
- *               bytes, 16-byte aligned, owned by the caller; contents on entry
- *               do not matter.
+ *               dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows,
+ *               chunk_cols, flags) bytes, 16-byte aligned, owned by the
+ *               caller; contents on entry do not matter.
  * Other arguments: as for dart_lmhead_backward. Errors: as for
  * dart_lmhead_backward; UNSUPPORTED also when the sizes are too large for the
  * workspace arithmetic. */
@@ -424,21 +422,21 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
                                       const void* weight, int64_t V, int64_t ld_w,
                                       const int32_t* target, const float* lse, const float* logp,
                                       const float* tok_coef, void* dhidden, int64_t ld_dh,
-                                      void* dweight, int64_t ld_dw, int64_t chunk,
-                                      uint32_t flags, void* workspace, size_t workspace_bytes,
-                                      hipStream_t stream);
+                                      void* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                      int64_t chunk_cols, uint32_t flags, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
 
 /* Bytes of workspace dart_lmhead_backward_ex needs (host only; 0 for bad
  * arguments or flags). The parts, each starting 256-byte aligned: the dlogits
- * chunk (min(chunk, T) * ceil8(V) bf16, or T * ceil8(min(chunk, V)) with
- * DART_LMHEAD_CHUNK_VOCAB); with DART_LMHEAD_BF16_GRADS and more than one
- * chunk, an fp32 accumulator for the summed output (V * d, or T * d with
- * vocabulary chunks; none when rows are skipped with vocabulary chunks, where
- * the compact fp32 dhidden rows serve); with DART_LMHEAD_SKIP_ZERO_ROWS, T
- * compact hidden rows (bf16), their fp32 dhidden, five [T] int/float arrays and
- * a counter. With flags = 0 the value is that of
- * dart_lmhead_backward_workspace_bytes(min(chunk, T), V). */
-size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t chunk,
+ * block, R * ceil8(C) bf16 with R = min(chunk_rows, T), C = min(chunk_cols,
+ * V); with DART_LMHEAD_BF16_GRADS, an fp32 accumulator of V * d when R < T and
+ * one of T * d when C < V (none when rows are skipped: the compact fp32
+ * dhidden rows serve); with DART_LMHEAD_SKIP_ZERO_ROWS, T compact hidden rows
+ * (bf16), their fp32 dhidden, five [T] int/float arrays and a counter. With
+ * chunk_cols >= V and flags = 0 the value is that of
+ * dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V). */
+size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
+                                               int64_t chunk_rows, int64_t chunk_cols,
                                                uint32_t flags);
 
 /* Host helper (no device work): k = clamp(ceil(rho * S - 1e-6), 0, S), the

@@ -33,7 +33,6 @@ DART_AGG = {"token_mean": 0, "token_mean_all": 1, "step_mean": 2}
 DART_RATIO = {"token": 0, "step_geomean": 1, "step_product": 2}
 DART_GRAD_SKIP_ZERO_ROWS = 1
 DART_LMHEAD_SKIP_ZERO_ROWS = 1
-DART_LMHEAD_CHUNK_VOCAB = 2
 DART_LMHEAD_BF16_GRADS = 4
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
@@ -119,10 +118,10 @@ def load_library():
         lib.dart_lmhead_backward_workspace_bytes.argtypes = [_I64, _I64]
         lib.dart_lmhead_backward_ex.restype = ctypes.c_int
         lib.dart_lmhead_backward_ex.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P,
-                                                _P, _P, _I64, _P, _I64, _I64, ctypes.c_uint32, _P,
-                                                ctypes.c_size_t, _P]
+                                                _P, _P, _I64, _P, _I64, _I64, _I64,
+                                                ctypes.c_uint32, _P, ctypes.c_size_t, _P]
         lib.dart_lmhead_backward_ex_workspace_bytes.restype = ctypes.c_size_t
-        lib.dart_lmhead_backward_ex_workspace_bytes.argtypes = [_I64, _I64, _I64, _I64,
+        lib.dart_lmhead_backward_ex_workspace_bytes.argtypes = [_I64, _I64, _I64, _I64, _I64,
                                                                 ctypes.c_uint32]
         lib.dart_kept_steps.restype = _I64
         lib.dart_kept_steps.argtypes = [_I64, ctypes.c_double]
@@ -511,10 +510,10 @@ def dart_lmhead_backward_workspace_bytes(chunk_rows: int, V: int) -> int:
     return int(load_library().dart_lmhead_backward_workspace_bytes(int(chunk_rows), int(V)))
 
 
-def dart_lmhead_backward_ex_workspace_bytes(T: int, d: int, V: int, chunk: int,
-                                            flags: int) -> int:
+def dart_lmhead_backward_ex_workspace_bytes(T: int, d: int, V: int, chunk_rows: int,
+                                            chunk_cols: int, flags: int) -> int:
     return int(load_library().dart_lmhead_backward_ex_workspace_bytes(
-        int(T), int(d), int(V), int(chunk), int(flags)))
+        int(T), int(d), int(V), int(chunk_rows), int(chunk_cols), int(flags)))
 
 
 def _lmhead_common(hidden, weight, target, lse, logp, tok_coef):
@@ -550,12 +549,13 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
     return dlogits
 
 
-def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk, dhidden,
-                     dweight, workspace, stream):
+def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk_rows,
+                     chunk_cols, dhidden, dweight, workspace, stream):
     torch = _torch()
     dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
     f = 0 if flags is None else int(flags)
-    chunk = max(1, min(int(chunk), V if f & DART_LMHEAD_CHUNK_VOCAB else T))
+    chunk_rows = max(1, min(int(chunk_rows), T))
+    chunk_cols = max(1, min(int(chunk_cols), V))
     gdt = torch.bfloat16 if f & DART_LMHEAD_BF16_GRADS else torch.float32
     dhidden = torch.empty((T, d), dtype=gdt, device=dev) if dhidden is None else dhidden
     dweight = torch.empty((V, d), dtype=gdt, device=dev) if dweight is None else dweight
@@ -566,8 +566,8 @@ def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, c
     if isinstance(workspace, str):
         if workspace != "auto":
             raise ValueError('workspace must be "auto" or a uint8 device tensor')
-        nbytes = (dart_lmhead_backward_workspace_bytes(chunk, V) if flags is None else
-                  dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, f))
+        nbytes = (dart_lmhead_backward_workspace_bytes(chunk_rows, V) if flags is None else
+                  dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, chunk_cols, f))
         if nbytes == 0:
             raise ValueError(f"{name}: bad sizes or flags")
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -578,9 +578,10 @@ def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, c
         raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
     args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
             target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0), chunk]
+            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0),
+            chunk_rows]
     if flags is not None:
-        args.append(f)
+        args += [chunk_cols, f]
     args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream)]
     rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
@@ -595,35 +596,50 @@ def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows
     uint8 device tensor of dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
     bytes)."""
     return _lmhead_backward("dart_lmhead_backward", None, hidden, weight, target, lse, logp,
-                            tok_coef, chunk_rows, dhidden, dweight, workspace, stream)
+                            tok_coef, chunk_rows, weight.shape[0], dhidden, dweight, workspace,
+                            stream)
 
 
-def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk=1024, flags=0,
-                            dhidden=None, dweight=None, workspace="auto", stream=None):
-    """dart_lmhead_backward with flags (bitwise or):
-    DART_LMHEAD_CHUNK_VOCAB: ``chunk`` counts vocabulary entries, dlogits formed for
-    all rows and that many entries at a time (cheaper than row chunks when T < V);
+def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk_rows=None,
+                            chunk_cols=None, flags=0, dhidden=None, dweight=None,
+                            workspace="auto", stream=None):
+    """dart_lmhead_backward in blocks of chunk_rows rows x chunk_cols vocabulary
+    entries (both None: lmhead_backward_plan's block), with flags (bitwise or):
     DART_LMHEAD_BF16_GRADS: dhidden and dweight in bfloat16;
     DART_LMHEAD_SKIP_ZERO_ROWS: the GEMMs over the rows with tok_coef != 0 only
     (the call synchronises the stream once).
     ``workspace`` is "auto" or a uint8 device tensor of
-    dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags) bytes."""
+    dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk_rows, chunk_cols, flags)
+    bytes."""
+    if chunk_rows is None and chunk_cols is None:
+        chunk_rows, chunk_cols = lmhead_backward_plan(hidden.shape[0], weight.shape[0])
+    elif chunk_rows is None or chunk_cols is None:
+        raise ValueError("give both chunk_rows and chunk_cols, or neither")
     return _lmhead_backward("dart_lmhead_backward_ex", int(flags), hidden, weight, target, lse,
-                            logp, tok_coef, chunk, dhidden, dweight, workspace, stream)
+                            logp, tok_coef, chunk_rows, chunk_cols, dhidden, dweight, workspace,
+                            stream)
 
 
 def lmhead_backward_plan(T: int, V: int, budget_bytes: int = 512 << 20):
-    """(chunk, flags) for dart_lmhead_backward_ex that keep the bf16 dlogits chunk
-    within budget_bytes: vocabulary chunks when T < V (only the [T, d] dhidden is
-    summed over chunks), else row chunks; chunks are whole 256-wide tiles where the
-    budget allows."""
+    """(chunk_rows, chunk_cols) for dart_lmhead_backward_ex: the block whose bf16
+    dlogits fit budget_bytes and that rewrites the summed outputs least. Each of
+    the ceil(T / rows) row blocks rewrites the [V, d] dweight and each of the
+    ceil(V / cols) vocabulary blocks the [T, d] dhidden, so the cost is
+    ceil(T / rows) V + ceil(V / cols) T; blocks are whole 256-wide tiles (or all
+    of T, V). All rows when T << V, square blocks when T ~ V."""
     T, V = int(T), int(V)
-    if T < V:
-        cols = max(256, budget_bytes // (2 * T) // 256 * 256)
-        return min(cols, V), DART_LMHEAD_CHUNK_VOCAB
-    row_bytes = 2 * ((V + 7) // 8 * 8)
-    rows = max(256, budget_bytes // row_bytes // 256 * 256)
-    return min(rows, T), 0
+    elems = max(budget_bytes // 2, 256 * 256)
+    best = None
+    for rows in sorted({T} | set(range(256, T, 256))):
+        cols = V if rows * V <= elems else (elems // rows) // 256 * 256
+        if cols < 256:
+            continue
+        cost = -(-T // rows) * V + -(-V // cols) * T
+        if best is None or cost < best[0]:
+            best = (cost, rows, cols)
+    if best is None:
+        return min(T, 256), min(V, 256)
+    return best[1], best[2]
 
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,

@@ -17,8 +17,8 @@ only marshal tensors and scale the [T] coefficient.
     loss.backward()          # hidden.grad, weight.grad (bfloat16)
 
 The LM-head backward writes its gradients in bfloat16 directly and, unless
-told otherwise, chunks the dlogits along the vocabulary when T < V (along the
-rows otherwise) within a 512 MiB workspace.
+told otherwise, forms the dlogits in the blocks of rows x vocabulary entries
+that lmhead_backward_plan picks for a 512 MiB workspace.
 """
 
 import torch
@@ -69,32 +69,34 @@ class DartLmHeadPolicyLoss(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, hidden, weight, target, logp_old, logp_rollout, adv, step_offsets, rho,
-                eps_low, eps_high, C, chunk, flags):
+                eps_low, eps_high, C, chunk_rows, chunk_cols, flags):
         hidden, weight = hidden.detach(), weight.detach()
         logp, ent, lse = dart_lmhead_tok_stats(hidden, weight, target)
         loss, coef = _loss(logp, ent, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
                            eps_high, C)
-        ctx.chunk, ctx.flags = lmhead_grad_plan(hidden.shape[0], weight.shape[0], chunk, flags)
+        ctx.plan = lmhead_grad_plan(hidden.shape[0], weight.shape[0], chunk_rows, chunk_cols,
+                                    flags)
         ctx.save_for_backward(hidden, weight, target, logp, lse, coef)
         return loss
 
     @staticmethod
     def backward(ctx, grad):
         hidden, weight, target, logp, lse, coef = ctx.saved_tensors
+        rows, cols, flags = ctx.plan
         dh, dw = dart_lmhead_backward_ex(hidden, weight, target, lse, logp, _scaled(coef, grad),
-                                         chunk=ctx.chunk, flags=ctx.flags)
-        return (dh, dw) + (None,) * 11
+                                         chunk_rows=rows, chunk_cols=cols, flags=flags)
+        return (dh, dw) + (None,) * 12
 
 
-def lmhead_grad_plan(T, V, chunk=None, flags=None):
-    """(chunk, flags) the LM-head autograd backward passes to
-    dart_lmhead_backward_ex: the caller's, else lmhead_backward_plan's; always
-    with bfloat16 gradients."""
-    if chunk is None and flags is None:
-        chunk, flags = lmhead_backward_plan(T, V)
-    elif chunk is None or flags is None:
-        raise ValueError("give both chunk and flags, or neither")
-    return int(chunk), int(flags) | DART_LMHEAD_BF16_GRADS
+def lmhead_grad_plan(T, V, chunk_rows=None, chunk_cols=None, flags=None):
+    """(chunk_rows, chunk_cols, flags) the LM-head autograd backward passes to
+    dart_lmhead_backward_ex: the caller's block, else lmhead_backward_plan's;
+    the caller's flags (default none), always with bfloat16 gradients."""
+    if chunk_rows is None and chunk_cols is None:
+        chunk_rows, chunk_cols = lmhead_backward_plan(T, V)
+    elif chunk_rows is None or chunk_cols is None:
+        raise ValueError("give both chunk_rows and chunk_cols, or neither")
+    return int(chunk_rows), int(chunk_cols), int(flags or 0) | DART_LMHEAD_BF16_GRADS
 
 
 def dart_policy_loss(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
@@ -105,9 +107,11 @@ def dart_policy_loss(logits, target, logp_old, logp_rollout, adv, step_offsets, 
 
 
 def dart_lmhead_policy_loss(hidden, weight, target, logp_old, logp_rollout, adv, step_offsets,
-                            rho, eps_low, eps_high, C, chunk=None, flags=None):
+                            rho, eps_low, eps_high, C, chunk_rows=None, chunk_cols=None,
+                            flags=None):
     """Differentiable DART loss of the LM head's inputs (see the module
-    docstring); chunk and flags as for dart_lmhead_backward_ex (both None: the
-    default plan)."""
+    docstring); chunk_rows, chunk_cols and flags as for dart_lmhead_backward_ex
+    (no block: the default plan)."""
     return DartLmHeadPolicyLoss.apply(hidden, weight, target, logp_old, logp_rollout, adv,
-                                      step_offsets, rho, eps_low, eps_high, C, chunk, flags)
+                                      step_offsets, rho, eps_low, eps_high, C, chunk_rows,
+                                      chunk_cols, flags)

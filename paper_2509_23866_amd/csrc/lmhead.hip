@@ -747,8 +747,7 @@ size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
 
 namespace {
 
-constexpr uint32_t kBackwardFlags =
-    DART_LMHEAD_SKIP_ZERO_ROWS | DART_LMHEAD_CHUNK_VOCAB | DART_LMHEAD_BF16_GRADS;
+constexpr uint32_t kBackwardFlags = DART_LMHEAD_SKIP_ZERO_ROWS | DART_LMHEAD_BF16_GRADS;
 
 int64_t ceil8(int64_t x) { return (x + 7) / 8 * 8; }
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -756,26 +755,26 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // How a backward call runs and where its parts sit in the workspace (byte
 // offsets, each part 256-byte aligned; total is the end of the last part).
 struct BackwardPlan {
-    bool vocab, bf16, skip;
-    int64_t chunk;    // rows (or vocabulary entries) per chunk, at most T (or V)
-    bool accumulate;  // a bf16 output summed over several chunks goes through fp32
-    size_t dz, acc, h_c, dh_c, target_c, lse_c, logp_c, coef_c, map, count, total;
+    bool bf16, skip;
+    int64_t rows, cols;  // block of rows x vocabulary entries, at most T x V
+    bool acc_w;          // dW summed over row blocks into bf16: through fp32
+    bool acc_h;          // dh summed over vocabulary blocks into bf16: through fp32
+    size_t dz, accw, acch, h_c, dh_c, target_c, lse_c, logp_c, coef_c, map, count, total;
 };
 
 // total = 0 when the sizes do not fit the address arithmetic.
-BackwardPlan plan_backward(int64_t T, int64_t d, int64_t V, int64_t chunk, uint32_t flags) {
+BackwardPlan plan_backward(int64_t T, int64_t d, int64_t V, int64_t chunk_rows,
+                           int64_t chunk_cols, uint32_t flags) {
     BackwardPlan P = {};
-    P.vocab = flags & DART_LMHEAD_CHUNK_VOCAB;
     P.bf16 = flags & DART_LMHEAD_BF16_GRADS;
     P.skip = flags & DART_LMHEAD_SKIP_ZERO_ROWS;
-    const int64_t span = P.vocab ? V : T;
-    P.chunk = chunk < span ? chunk : span;
-    const int64_t nchunks = (span + P.chunk - 1) / P.chunk;
-    // dW is summed over row chunks and dh over vocabulary chunks; with rows
-    // skipped, dh is summed in the compact fp32 rows
-    P.accumulate = P.bf16 && nchunks > 1 && !(P.skip && P.vocab);
+    P.rows = chunk_rows < T ? chunk_rows : T;
+    P.cols = chunk_cols < V ? chunk_cols : V;
+    // with rows skipped, dh is summed in the compact fp32 rows
+    P.acc_w = P.bf16 && P.rows < T;
+    P.acc_h = P.bf16 && P.cols < V && !P.skip;
     const double big = double(int64_t(1) << 60);
-    if ((double)T * (double)ceil8(V) * 2 > big || (double)V * (double)d * 4 > big ||
+    if ((double)P.rows * (double)ceil8(P.cols) * 2 > big || (double)V * (double)d * 4 > big ||
         (double)T * (double)d * 6 > big)
         return P;
     size_t end = 0;
@@ -784,9 +783,9 @@ BackwardPlan plan_backward(int64_t T, int64_t d, int64_t V, int64_t chunk, uint3
         end = at + bytes;
         return at;
     };
-    P.dz = take(P.vocab ? (size_t)T * (size_t)ceil8(P.chunk) * 2
-                        : (size_t)P.chunk * (size_t)ceil8(V) * 2);
-    if (P.accumulate) P.acc = take((size_t)(P.vocab ? T : V) * (size_t)d * 4);
+    P.dz = take((size_t)P.rows * (size_t)ceil8(P.cols) * 2);
+    if (P.acc_w) P.accw = take((size_t)V * (size_t)d * 4);
+    if (P.acc_h) P.acch = take((size_t)T * (size_t)d * 4);
     if (P.skip) {
         P.h_c = take((size_t)T * (size_t)d * 2);
         P.dh_c = take((size_t)T * (size_t)d * 4);
@@ -848,52 +847,44 @@ void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& ds
                        static_cast<uint16_t*>(dst.p), dst.ld);
 }
 
-// The gradient pass over rows [0, T) of h, in chunks of rows or of vocabulary
-// entries: per chunk, its dlogits into dz (bf16), then the two GEMMs. The
-// output summed over chunks (dW over rows, dh over vocabulary) is summed in
-// fp32: in the output itself, or in acc ([V, d] or [T, d]) when the output is
-// bf16 and there is more than one chunk, rounded to bf16 at the end. Each
-// element of the other output is one GEMM's result, rounded once.
+// The gradient pass over rows [0, T) of h in blocks of rows x vocabulary
+// entries: per block, its dlogits into dz (bf16), then the block's share of
+// dh (summed over the vocabulary blocks of its rows) and of dW (summed over
+// the row blocks of its entries). A sum goes into its fp32 output directly,
+// or, for a bf16 output that more than one block adds to, into acc_h ([T, d])
+// or acc_w ([V, d]) and is rounded to bf16 once at the end; an output that
+// one block writes is that GEMM's fp32 result rounded once.
 dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
                             int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
                             const int32_t* target, const float* lse, const float* logp,
-                            const float* coef, const Grad& dh, const Grad& dw, bool vocab,
-                            int64_t chunk, uint16_t* dz, float* acc, hipStream_t stream) {
-    if (!vocab) {
-        if (chunk > T) chunk = T;
-        const int64_t ld_dz = ceil8(V);
-        const bool via_acc = dw.bf16 && chunk < T;
-        const Grad sum = via_acc ? Grad{acc, d, false} : dw;
-        for (int64_t r0 = 0; r0 < T; r0 += chunk) {
-            const int64_t rows = T - r0 < chunk ? T - r0 : chunk;
-            const dart_status_t st =
-                launch_dlogits(h + r0 * ld_h, rows, d, ld_h, w, V, ld_w, target + r0, lse + r0,
-                               logp + r0, coef + r0, dz, ld_dz, 0, stream);
-            if (st != DART_OK) return st;
-            if (!gemm_dh(blas, dz, ld_dz, rows, V, w, ld_w, d, false,
-                         Grad{dh.row(r0), dh.ld, dh.bf16}) ||
-                !gemm_dw(blas, h + r0 * ld_h, ld_h, rows, dz, ld_dz, V, d, r0 > 0, sum))
-                return DART_ERR_HIP;
-        }
-        if (via_acc) launch_to_bf16(acc, V, d, dw, stream);
-    } else {
-        if (chunk > V) chunk = V;
-        const int64_t ld_dz = ceil8(chunk);
-        const bool via_acc = dh.bf16 && chunk < V;
-        const Grad sum = via_acc ? Grad{acc, d, false} : dh;
-        for (int64_t c0 = 0; c0 < V; c0 += chunk) {
-            const int64_t cols = V - c0 < chunk ? V - c0 : chunk;
+                            const float* coef, const Grad& dh, const Grad& dw, int64_t R,
+                            int64_t C, uint16_t* dz, float* acc_h, float* acc_w,
+                            hipStream_t stream) {
+    if (R > T) R = T;
+    if (C > V) C = V;
+    const int64_t ld_dz = ceil8(C);
+    const bool via_h = dh.bf16 && C < V, via_w = dw.bf16 && R < T;
+    const Grad sum_h = via_h ? Grad{acc_h, d, false} : dh;
+    const Grad sum_w = via_w ? Grad{acc_w, d, false} : dw;
+    for (int64_t r0 = 0; r0 < T; r0 += R) {
+        const int64_t rows = T - r0 < R ? T - r0 : R;
+        const uint16_t* hr = h + r0 * ld_h;
+        for (int64_t c0 = 0; c0 < V; c0 += C) {
+            const int64_t cols = V - c0 < C ? V - c0 : C;
             const uint16_t* wc = w + c0 * ld_w;
-            const dart_status_t st = launch_dlogits(h, T, d, ld_h, wc, cols, ld_w, target, lse,
-                                                    logp, coef, dz, ld_dz, c0, stream);
+            const dart_status_t st =
+                launch_dlogits(hr, rows, d, ld_h, wc, cols, ld_w, target + r0, lse + r0,
+                               logp + r0, coef + r0, dz, ld_dz, c0, stream);
             if (st != DART_OK) return st;
-            if (!gemm_dh(blas, dz, ld_dz, T, cols, wc, ld_w, d, c0 > 0, sum) ||
-                !gemm_dw(blas, h, ld_h, T, dz, ld_dz, cols, d, false,
-                         Grad{dw.row(c0), dw.ld, dw.bf16}))
+            if (!gemm_dh(blas, dz, ld_dz, rows, cols, wc, ld_w, d, c0 > 0,
+                         Grad{sum_h.row(r0), sum_h.ld, sum_h.bf16}) ||
+                !gemm_dw(blas, hr, ld_h, rows, dz, ld_dz, cols, d, r0 > 0,
+                         Grad{sum_w.row(c0), sum_w.ld, sum_w.bf16}))
                 return DART_ERR_HIP;
         }
-        if (via_acc) launch_to_bf16(acc, T, d, dh, stream);
     }
+    if (via_h) launch_to_bf16(acc_h, T, d, dh, stream);
+    if (via_w) launch_to_bf16(acc_w, V, d, dw, stream);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
@@ -908,31 +899,32 @@ void launch_zero_rows(void* m, int64_t rows, int64_t cols, int64_t ld, hipStream
 
 extern "C" {
 
-size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t chunk,
+size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
+                                               int64_t chunk_rows, int64_t chunk_cols,
                                                uint32_t flags) {
-    if (T < 1 || d < 1 || V < 1 || chunk < 1 || T > 0x7FFFFFFFll || d > 0x7FFFFFFFll ||
-        V > 0x7FFFFFFFll || (flags & ~kBackwardFlags))
+    if (T < 1 || d < 1 || V < 1 || chunk_rows < 1 || chunk_cols < 1 || T > 0x7FFFFFFFll ||
+        d > 0x7FFFFFFFll || V > 0x7FFFFFFFll || (flags & ~kBackwardFlags))
         return 0;
-    return plan_backward(T, d, V, chunk, flags).total;
+    return plan_backward(T, d, V, chunk_rows, chunk_cols, flags).total;
 }
 
 dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                       const void* weight, int64_t V, int64_t ld_w,
                                       const int32_t* target, const float* lse, const float* logp,
                                       const float* tok_coef, void* dhidden, int64_t ld_dh,
-                                      void* dweight, int64_t ld_dw, int64_t chunk,
-                                      uint32_t flags, void* workspace, size_t workspace_bytes,
-                                      hipStream_t stream) {
+                                      void* dweight, int64_t ld_dw, int64_t chunk_rows,
+                                      int64_t chunk_cols, uint32_t flags, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream) {
     if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
     if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
         return DART_ERR_INVALID_ARG;
-    if (ld_dh < d || ld_dw < d || chunk < 1 || (flags & ~kBackwardFlags) ||
-        reinterpret_cast<uintptr_t>(workspace) % 16)
+    if (ld_dh < d || ld_dw < d || chunk_rows < 1 || chunk_cols < 1 ||
+        (flags & ~kBackwardFlags) || reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
     // the BLAS library takes 32-bit sizes and leading dimensions
     const int64_t kI32 = 0x7FFFFFFFll;
     if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
-    const BackwardPlan P = plan_backward(T, d, V, chunk, flags);
+    const BackwardPlan P = plan_backward(T, d, V, chunk_rows, chunk_cols, flags);
     if (P.total == 0) return DART_ERR_UNSUPPORTED;
     if (workspace_bytes < P.total) return DART_ERR_INVALID_ARG;
     if (const dart_status_t ck = dart_check::run(
@@ -951,11 +943,12 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     const uint16_t* w = static_cast<const uint16_t*>(weight);
     char* ws = static_cast<char*>(workspace);
     uint16_t* dz = reinterpret_cast<uint16_t*>(ws + P.dz);
-    float* acc = P.accumulate ? reinterpret_cast<float*>(ws + P.acc) : nullptr;
+    float* acc_w = P.acc_w ? reinterpret_cast<float*>(ws + P.accw) : nullptr;
+    float* acc_h = P.acc_h ? reinterpret_cast<float*>(ws + P.acch) : nullptr;
     const Grad dh{dhidden, ld_dh, P.bf16}, dw{dweight, ld_dw, P.bf16};
     if (!P.skip)
         return backward_core(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef, dh,
-                             dw, P.vocab, P.chunk, dz, acc, stream);
+                             dw, P.rows, P.cols, dz, acc_h, acc_w, stream);
 
     // rows with a zero coefficient have dz = 0: they add nothing to dW and
     // their rows of dh are 0, so the GEMMs run over the other rows only
@@ -991,7 +984,7 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     }
     const dart_status_t st =
         backward_core(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c,
-                      Grad{dh_c, d, false}, dw, P.vocab, P.chunk, dz, acc, stream);
+                      Grad{dh_c, d, false}, dw, P.rows, P.cols, dz, nullptr, acc_w, stream);
     if (st != DART_OK) return st;
     const unsigned nb = (unsigned)(n < kRowBlocks ? n : kRowBlocks);
     if (P.bf16)
@@ -1010,7 +1003,7 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
                                    float* dweight, int64_t ld_dw, int64_t chunk_rows,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
     return dart_lmhead_backward_ex(hidden, T, d, ld_h, weight, V, ld_w, target, lse, logp,
-                                   tok_coef, dhidden, ld_dh, dweight, ld_dw, chunk_rows, 0u,
+                                   tok_coef, dhidden, ld_dh, dweight, ld_dw, chunk_rows, V, 0u,
                                    workspace, workspace_bytes, stream);
 }
 

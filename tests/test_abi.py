@@ -285,9 +285,9 @@ def test_lmhead_leading_dimension_limit():
     assert lib.dart_lmhead_dlogits(*_lm_grad_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
 
 
-def _lm_bwd_ex_args(flags=0, **kw):
+def _lm_bwd_ex_args(flags=0, chunk_cols=300, **kw):
     a = _lm_bwd_args(**kw)[:-1]
-    return a[:16] + [flags] + a[16:] + [None]
+    return a[:16] + [chunk_cols, flags] + a[16:] + [None]
 
 
 @pytest.mark.skipif("_gpu_visible()")
@@ -295,58 +295,71 @@ def _lm_bwd_ex_args(flags=0, **kw):
     dict(hidden=0), dict(weight=0), dict(target=0), dict(lse=0), dict(logp=0), dict(coef=0),
     dict(dh=0), dict(dw=0), dict(workspace=0), dict(T=0), dict(V=0), dict(d=4, ld_h=4, ld_w=4),
     dict(ld_dh=15), dict(ld_dw=8), dict(chunk=0), dict(ws_bytes=2 * 304 * 2 - 1),
-    dict(workspace=(1 << 22) + 8), dict(flags=8), dict(flags=1 << 31),
-    dict(flags=1, ws_bytes="one short"), dict(flags=1, ws_bytes=2 * 304 * 2),
+    dict(workspace=(1 << 22) + 8), dict(flags=2), dict(flags=8), dict(flags=1 << 31),
+    dict(chunk_cols=0), dict(flags=1, ws_bytes="one short"), dict(flags=1, ws_bytes=2 * 304 * 2),
+    dict(flags=4, chunk_cols=100, ws_bytes="one short"),
 ])
 def test_lmhead_backward_ex_rejects(kw):
     """Bad arguments, unknown flags and a workspace too small for the row
     compaction are INVALID_ARG before anything is enqueued."""
     lib = dart.load_library()
     if kw.get("ws_bytes") == "one short":
-        kw["ws_bytes"] = dart.dart_lmhead_backward_ex_workspace_bytes(4, 16, 300, 2, 1) - 1
+        kw["ws_bytes"] = dart.dart_lmhead_backward_ex_workspace_bytes(
+            4, 16, 300, 2, kw.get("chunk_cols", 300), kw["flags"]) - 1
     assert lib.dart_lmhead_backward_ex(*_lm_bwd_ex_args(**kw)) == dart.DART_ERR_INVALID_ARG
 
 
 def test_lmhead_backward_ex_workspace_bytes():
     """The parts of the workspace, each starting at a multiple of 256 bytes: the
-    bf16 dlogits chunk; an fp32 accumulator for a bf16 output summed over
-    several chunks (dweight over row chunks, dhidden over vocabulary chunks,
-    none when skipped rows go with vocabulary chunks); the compact hidden rows
-    (bf16), their fp32 dhidden, five [T] int/float arrays and a counter. flags =
-    0 needs what dart_lmhead_backward needs."""
+    bf16 dlogits block; with bf16 gradients, an fp32 accumulator for each
+    output that several blocks add to (dweight when the rows come in several
+    blocks, dhidden when the vocabulary does, but not with rows skipped); with
+    rows skipped, the compact hidden rows (bf16), their fp32 dhidden, five [T]
+    int/float arrays and a counter. chunk_cols >= V with flags = 0 needs what
+    dart_lmhead_backward needs."""
     f = dart.dart_lmhead_backward_ex_workspace_bytes
     plain = dart.dart_lmhead_backward_workspace_bytes
     up = lambda x: -(-x // 256) * 256
     c8 = lambda x: -(-x // 8) * 8
-    SKIP, VOC, BF = dart.DART_LMHEAD_SKIP_ZERO_ROWS, dart.DART_LMHEAD_CHUNK_VOCAB, \
-        dart.DART_LMHEAD_BF16_GRADS
-    for T, d, V, chunk in ((4, 16, 300, 2), (4, 16, 300, 9), (4096, 3584, 152064, 1024),
-                           (5, 8, 7, 1), (300, 136, 2100, 512), (300, 136, 2100, 5000)):
-        for flags in range(8):
-            vocab, bf16, skip = bool(flags & VOC), bool(flags & BF), bool(flags & SKIP)
-            span = V if vocab else T
-            c = min(chunk, span)
-            parts = [T * c8(c) * 2 if vocab else c * c8(V) * 2]
-            if bf16 and -(-span // c) > 1 and not (skip and vocab):
-                parts.append((T if vocab else V) * d * 4)
+    SKIP, BF = dart.DART_LMHEAD_SKIP_ZERO_ROWS, dart.DART_LMHEAD_BF16_GRADS
+    for T, d, V, cr, cc in ((4, 16, 300, 2, 300), (4, 16, 300, 9, 100), (4096, 3584, 152064, 4096, 65536),
+                            (5, 8, 7, 1, 1), (300, 136, 2100, 512, 700), (300, 136, 2100, 100, 5000),
+                            (152569, 3584, 152064, 15360, 17408)):
+        for flags in (0, SKIP, BF, SKIP | BF):
+            bf16, skip = bool(flags & BF), bool(flags & SKIP)
+            R, C = min(cr, T), min(cc, V)
+            parts = [R * c8(C) * 2]
+            if bf16 and R < T:
+                parts.append(V * d * 4)
+            if bf16 and C < V and not skip:
+                parts.append(T * d * 4)
             if skip:
                 parts += [T * d * 2, T * d * 4] + [T * 4] * 5 + [4]
             want = sum(up(x) for x in parts[:-1]) + parts[-1]
-            assert f(T, d, V, chunk, flags) == want, (T, d, V, chunk, flags)
-            if flags == 0:
-                assert want == plain(c, V)
-    assert f(0, 16, 300, 2, 1) == 0 and f(4, 0, 300, 2, 1) == 0 and f(4, 16, 0, 2, 1) == 0
-    assert f(4, 16, 300, 0, 1) == 0 and f(4, 16, 300, 2, 8) == 0 and f(1 << 31, 16, 8, 1, 0) == 0
+            assert f(T, d, V, cr, cc, flags) == want, (T, d, V, cr, cc, flags)
+            if flags == 0 and C == V:
+                assert want == plain(R, V)
+    assert f(0, 16, 300, 2, 5, 1) == 0 and f(4, 0, 300, 2, 5, 1) == 0 and f(4, 16, 0, 2, 5, 1) == 0
+    assert f(4, 16, 300, 0, 5, 1) == 0 and f(4, 16, 300, 2, 0, 1) == 0
+    assert f(4, 16, 300, 2, 5, 2) == 0 and f(4, 16, 300, 2, 5, 8) == 0
+    assert f(1 << 31, 16, 8, 1, 1, 0) == 0
 
 
 def test_lmhead_backward_plan():
-    """Vocabulary chunks when T < V, row chunks otherwise, whole 256-wide tiles
-    within the byte budget."""
+    """All rows with vocabulary chunks when T << V, near-square blocks when
+    T ~ V; whole 256-wide tiles within the byte budget, and the cost (summed
+    outputs rewritten) no larger than that of any other such block."""
     plan = dart.lmhead_backward_plan
-    c, fl = plan(4096, 152064)
-    assert fl == dart.DART_LMHEAD_CHUNK_VOCAB and c % 256 == 0 and 4096 * c * 2 <= 512 << 20
-    assert plan(500, 1000) == (1000, dart.DART_LMHEAD_CHUNK_VOCAB)
-    assert plan(4096, 1000) == (4096, 0)
-    c, fl = plan(152569, 152064)
-    assert fl == 0 and c % 256 == 0 and c * 152064 * 2 <= 512 << 20
-    assert plan(100, 50) == (100, 0)
+    assert plan(4096, 152064) == (4096, 65536)
+    assert plan(500, 1000) == (500, 1000) and plan(100, 50) == (100, 50)
+    for T, V in ((152569, 152064), (34585, 152064), (16384, 151936), (4096, 152064)):
+        r, c = plan(T, V)
+        assert (r == T or r % 256 == 0) and (c == V or c % 256 == 0)
+        assert r * c * 2 <= 512 << 20
+        cost = -(-T // r) * V + -(-V // c) * T
+        for r2 in range(256, T + 1, 256):
+            c2 = min(V, (((512 << 20) // 2) // r2) // 256 * 256)
+            if c2 >= 256:
+                assert cost <= -(-T // r2) * V + -(-V // c2) * T
+    r, c = plan(152569, 152064)
+    assert 8192 <= r <= 32768 and 8192 <= c <= 32768

@@ -62,11 +62,13 @@ def test_policy_loss_autograd_matches_direct():
     assert torch.equal(x.grad.view(torch.int16), dz.view(torch.int16))
 
 
-@pytest.mark.parametrize("chunk,flags", [(None, None), (256, 0), (1000, 2), (300, 1)])
-def test_lmhead_policy_loss_autograd_matches_direct(chunk, flags):
+@pytest.mark.parametrize("rows,cols,flags", [(None, None, None), (256, 5000, 0), (600, 1000, 0),
+                                             (256, 1000, 0), (300, 5000, 1)])
+def test_lmhead_policy_loss_autograd_matches_direct(rows, cols, flags):
     """The autograd gradients are the bits of the direct bf16-gradient call
-    with the same chunking (the default plan: one vocabulary chunk here); with
-    row chunks, dweight is the fp32 sum rounded once, so it equals the fp32
+    with the same blocking (the default plan: one block here; row chunks,
+    vocabulary chunks, both, rows skipped); with row chunks over the whole
+    vocabulary, dweight is the fp32 sum rounded once, so it equals the fp32
     call's dweight rounded to bf16."""
     import torch
 
@@ -89,21 +91,22 @@ def test_lmhead_policy_loss_autograd_matches_direct(chunk, flags):
     _, mask, _ = dart.dart_step_select(ent, off, 0.7)
     loss_ref, coef, _ = dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, 0.2, 0.28,
                                                2.0)
-    c, f = lmhead_grad_plan(T, V, chunk, flags)
+    r, c, f = lmhead_grad_plan(T, V, rows, cols, flags)
     assert f & dart.DART_LMHEAD_BF16_GRADS
-    dh_ref, dw_ref = dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk=c, flags=f)
+    dh_ref, dw_ref = dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=r,
+                                                  chunk_cols=c, flags=f)
     # autograd
     hx = h.clone().requires_grad_(True)
     wx = w.clone().requires_grad_(True)
     loss = dart_lmhead_policy_loss(hx, wx, y, lp_old, lp_roll, adv, off, 0.7, 0.2, 0.28, 2.0,
-                                   chunk=chunk, flags=flags)
+                                   chunk_rows=rows, chunk_cols=cols, flags=flags)
     loss.backward()
     torch.cuda.synchronize()
     assert loss.item() == loss_ref.item()
     assert hx.grad.dtype == torch.bfloat16 and wx.grad.dtype == torch.bfloat16
     assert torch.equal(hx.grad.view(torch.int16), dh_ref.view(torch.int16))
     assert torch.equal(wx.grad.view(torch.int16), dw_ref.view(torch.int16))
-    if (chunk, flags) == (256, 0):
+    if (rows, cols, flags) == (256, 5000, 0):
         _, dw32 = dart.dart_lmhead_backward(h, w, y, lse, logp, coef, chunk_rows=256)
         torch.cuda.synchronize()
         assert torch.equal(wx.grad.view(torch.int16), dw32.to(torch.bfloat16).view(torch.int16))

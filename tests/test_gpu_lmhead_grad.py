@@ -208,8 +208,8 @@ def test_lmhead_backward_vlm7b_shape():
     gd = _cuda(g)
     dh, dw = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=1024)
     # the row-skipping backward: the GEMMs over the rows of R only
-    dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=1024,
-                                            flags=dart.DART_LMHEAD_SKIP_ZERO_ROWS)
+    dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=1024,
+                                            chunk_cols=V, flags=dart.DART_LMHEAD_SKIP_ZERO_ROWS)
     torch.cuda.synchronize()
     dh, dhs = dh.cpu().numpy(), dhs.cpu().numpy()
     outside = np.ones(T, bool)
@@ -309,10 +309,10 @@ def test_lmhead_backward_skip_zero_rows(T, d, V, pad, chunk, kind):
     dh = torch.full((T, d + 4), 3.0, dtype=torch.float32, device="cuda")
     dw = torch.full((V, d), 12345.0, dtype=torch.float32, device="cuda")  # overwritten
     flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS
-    ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),), 0xA5,
-                    dtype=torch.uint8, device="cuda")
-    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk=chunk, flags=flags,
-                                 dhidden=dh[:, :d], dweight=dw, workspace=ws)
+    ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, V, flags),),
+                    0xA5, dtype=torch.uint8, device="cuda")
+    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=chunk, chunk_cols=V,
+                                 flags=flags, dhidden=dh[:, :d], dweight=dw, workspace=ws)
     torch.cuda.synchronize()
     got_h = dh[:, :d].cpu().numpy()
     assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
@@ -339,7 +339,7 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
     hd, wd, yd = _dev_bf16(h), _dev_bf16(w), _cuda(y)
     logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
     flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS
-    ws = torch.empty((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, 128, flags),),
+    ws = torch.empty((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, 128, V, flags),),
                      dtype=torch.uint8, device="cuda")
     g2 = g.copy()
     g2[T // 3:] = 0.0
@@ -347,9 +347,10 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
     for gx in (g, g2):
         gd = _cuda(gx)
         dha, dwa = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
-        dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=128,
-                                                flags=flags, workspace=ws)
-        dh0, dw0 = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=128)
+        dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128,
+                                                chunk_cols=V, flags=flags, workspace=ws)
+        dh0, dw0 = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128,
+                                                chunk_cols=V)
         zbuf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
         dz = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, dlogits=zbuf[:, :V])
         dz = dz.double().cpu().numpy()
@@ -367,29 +368,34 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
             assert np.all(np.abs(got.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
 
 
-_SKIP, _VOC, _BF = 1, 2, 4
+_SKIP, _BF = 1, 4
 
 
-@pytest.mark.parametrize("T,d,V,pad,chunk,flags", [
-    (1, 8, 5, 0, 2, _VOC),
-    (129, 72, 127, 8, 64, _VOC),
-    (129, 72, 127, 8, 64, _VOC | _BF),
-    (300, 512, 16384, 0, 4096, _VOC | _BF),
-    (300, 512, 16384, 0, 1000, _VOC),
-    (257, 3584, 2000, 0, 777, _VOC | _BF),
-    (257, 3584, 2000, 0, 100, _BF),
-    (257, 3584, 2000, 0, 1024, _BF),
-    (1100, 136, 2000, 8, 256, _SKIP | _VOC),
-    (1100, 136, 2000, 8, 256, _SKIP | _VOC | _BF),
-    (1100, 136, 2000, 8, 300, _SKIP | _BF),
-    (200, 200, 1000, 0, 5000, _SKIP | _VOC | _BF),
+@pytest.mark.parametrize("T,d,V,pad,rows,cols,flags", [
+    (1, 8, 5, 0, 1, 2, 0),
+    (129, 72, 127, 8, 129, 64, 0),
+    (129, 72, 127, 8, 129, 64, _BF),
+    (300, 512, 16384, 0, 300, 4096, _BF),
+    (300, 512, 16384, 0, 300, 1000, 0),
+    (257, 3584, 2000, 0, 257, 777, _BF),
+    (257, 3584, 2000, 0, 100, 2000, _BF),
+    (257, 3584, 2000, 0, 1024, 2000, _BF),
+    (1100, 136, 2000, 8, 300, 700, 0),
+    (1100, 136, 2000, 8, 300, 700, _BF),
+    (1100, 136, 2000, 8, 1100, 256, _SKIP),
+    (1100, 136, 2000, 8, 1100, 256, _SKIP | _BF),
+    (1100, 136, 2000, 8, 300, 2000, _SKIP | _BF),
+    (1100, 136, 2000, 8, 256, 512, _SKIP | _BF),
+    (200, 200, 1000, 0, 5000, 5000, _SKIP | _BF),
 ])
-def test_lmhead_backward_ex_modes(T, d, V, pad, chunk, flags):
-    """dart_lmhead_backward_ex in vocabulary chunks (ragged: chunk sizes that
-    are not whole tiles, a last chunk shorter than the others, one chunk
-    covering V), with bf16 gradients (summed over several chunks in fp32 first,
-    or written straight from a single chunk) and with zero rows skipped, each
-    against the oracle; padding of dhidden untouched; skipped rows exactly 0."""
+def test_lmhead_backward_ex_modes(T, d, V, pad, rows, cols, flags):
+    """dart_lmhead_backward_ex in blocks of rows x vocabulary entries (all rows
+    with vocabulary chunks, row chunks over the whole vocabulary, both split;
+    ragged: blocks that are not whole tiles, last blocks shorter than the
+    others, one block covering everything), with bf16 gradients (summed over
+    several blocks in fp32 first, or written straight from one block) and with
+    zero rows skipped, each against the oracle; padding of dhidden untouched;
+    skipped rows exactly 0."""
     import torch
 
     import paper_2509_23866_amd as dart
@@ -403,10 +409,10 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, chunk, flags):
     gdt = torch.bfloat16 if flags & _BF else torch.float32
     dh = torch.full((T, d + 4), 3.0, dtype=gdt, device="cuda")
     dw = torch.full((V, d), 12345.0, dtype=gdt, device="cuda")  # overwritten
-    ws = torch.full((dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, chunk, flags),), 0x5A,
-                    dtype=torch.uint8, device="cuda")
-    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk=chunk, flags=flags,
-                                 dhidden=dh[:, :d], dweight=dw, workspace=ws)
+    nb = dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, flags)
+    ws = torch.full((nb,), 0x5A, dtype=torch.uint8, device="cuda")
+    dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=rows, chunk_cols=cols,
+                                 flags=flags, dhidden=dh[:, :d], dweight=dw, workspace=ws)
     torch.cuda.synchronize()
     assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
     if flags & _SKIP:
@@ -419,15 +425,15 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, chunk, flags):
     else:
         rh = _check_product(dh[:, :d].cpu().numpy(), dh64, bh, "dhidden")
         rw = _check_product(dw.cpu().numpy(), dw64, bw, "dweight")
-    H.log(f"lmhead backward_ex T={T} d={d} V={V} chunk={chunk} flags={flags}: "
+    H.log(f"lmhead backward_ex T={T} d={d} V={V} block={rows}x{cols} flags={flags}: "
           f"dh {rh:.2e} dW {rw:.2e}")
 
 
-def test_lmhead_backward_vocab_chunks_match_row_chunks():
-    """The same bf16 dlogits summed in another order: vocabulary and row chunks,
-    fp32 outputs, each within fp32 summation error of the exact products of
-    those dlogits; bf16 outputs equal the fp32 ones rounded, within one bf16
-    ulp."""
+def test_lmhead_backward_blockings_agree():
+    """The same bf16 dlogits summed in other orders: row chunks, vocabulary
+    chunks and 2-D blocks, fp32 outputs, each within fp32 summation error of
+    the exact products of those dlogits; bf16 outputs equal the fp32 ones of
+    the same blocking rounded, within one bf16 ulp."""
     import torch
 
     import paper_2509_23866_amd as dart
@@ -442,19 +448,19 @@ def test_lmhead_backward_vocab_chunks_match_row_chunks():
     h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
     adz = np.abs(dz)
     refs = ((dz @ w64, adz @ np.abs(w64)), (dz.T @ h64, adz.T @ np.abs(h64)))
-    runs = [dict(chunk=77, flags=0), dict(chunk=700, flags=_VOC), dict(chunk=256, flags=_VOC)]
-    outs = []
-    for kw in runs:
-        outs.append(dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, **kw))
-    bf = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk=700, flags=_VOC | _BF)
+    blocks = [(77, V), (T, 700), (T, 256), (128, 1000)]
+    outs = [dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=r, chunk_cols=c)
+            for r, c in blocks]
+    bfs = [dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=r, chunk_cols=c,
+                                        flags=_BF) for r, c in blocks]
     torch.cuda.synchronize()
     for got in outs:
         for x, (ref, bound) in zip(got, refs):
             assert np.all(np.abs(x.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
-    for xb, xf, (_, bound) in zip(bf, outs[1], refs):
-        # dweight is one GEMM per element; dhidden sums the chunks in fp32 and
-        # rounds once: both within one bf16 ulp of the fp32 result of the same
-        # chunking, up to the fp32 summation order of the library's kernels
-        a = xb.float().cpu().numpy().astype(np.float64)
-        b = xf.cpu().numpy().astype(np.float64)
-        assert np.all(np.abs(a - b) <= 2.0 ** -8 * np.abs(b) + 1e-4 * bound + 1e-37)
+    for bf, fp in zip(bfs, outs):
+        for xb, xf, (_, bound) in zip(bf, fp, refs):
+            # one rounding of the fp32 sum, up to the fp32 summation order of
+            # the library's kernels for bf16 and fp32 outputs
+            a = xb.float().cpu().numpy().astype(np.float64)
+            b = xf.cpu().numpy().astype(np.float64)
+            assert np.all(np.abs(a - b) <= 2.0 ** -8 * np.abs(b) + 1e-4 * bound + 1e-37)
