@@ -32,3 +32,35 @@ def test_traffic_only_for_the_measured_source():
         else:
             assert got is None
     assert bench.measured_traffic("tiny") is None
+
+
+def test_cpu_baseline_sample_is_whole_steps():
+    """Workloads above the sample size are cut to their first whole steps; the
+    cut keeps every per-token input of those rows and the step offsets."""
+    sys.path.insert(0, ROOT)
+    import numpy as np
+
+    import bench
+    import synth
+
+    wl = synth.make_workload("microbatch")
+    sub, n = bench._steps_prefix(wl, bench.CPU_SAMPLE_MAX_ROWS)
+    assert 0 < sub.T <= bench.CPU_SAMPLE_MAX_ROWS and sub.S == n
+    assert sub.T == int(wl.off[n]) and int(wl.off[n + 1]) > bench.CPU_SAMPLE_MAX_ROWS
+    assert np.array_equal(sub.off, wl.off[:n + 1])
+    for k in ("target", "adv", "old_offset", "roll_offset", "kind", "src_row", "spike_col",
+              "spike_val"):
+        assert np.array_equal(getattr(sub, k), getattr(wl, k)[:sub.T])
+    # a first step longer than the sample is still taken whole
+    one, n1 = bench._steps_prefix(wl, 1)
+    assert n1 == 1 and one.T == int(wl.off[1])
+
+
+def test_cpu_baseline_runs_on_the_small_workload():
+    sys.path.insert(0, ROOT)
+    import bench
+    import synth
+
+    r = bench.cpu_baseline(synth.make_workload("tiny"), threads=2, min_seconds=0.05, max_passes=3)
+    assert r["kind"] == "oracle" and r["cores"] == 2 and r["value"] > 0
+    assert 1 <= r["passes"] <= 3 and r["sample"].startswith("whole workload")
