@@ -23,9 +23,10 @@
  *   strictly increasing offsets with the documented ends, 0/1 step masks) is a
  *   precondition and is not checked, unless the environment has DART_CHECK=1:
  *   then every call first validates the device arrays it reads, waits for the
- *   result (the call synchronises the stream, so this is a debugging mode that
- *   cannot run under graph capture) and returns DART_ERR_INVALID_ARG, with
- *   nothing of the call enqueued, on a violation.
+ *   result (the call synchronises the stream, so this is a debugging mode: on
+ *   a stream that is being captured into a graph every call returns
+ *   DART_ERR_UNSUPPORTED) and returns DART_ERR_INVALID_ARG, with nothing of
+ *   the call enqueued, on a violation.
  * - Logits are row-major [T, ld] with ld >= V (elements, not bytes). Rows whose
  *   start is 16-byte aligned (base aligned and ld * element size a multiple of
  *   16) take the vectorised path; other rows are still correct, only slower.
@@ -402,7 +403,8 @@ enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
  * to 0. The result equals the dense call's up to the order of the BLAS
  * library's fp32 sums. Because the GEMM sizes depend on how many rows are
  * kept, the call copies that count to the host and synchronises the stream
- * once: it cannot run under graph capture. Without this flag the call is
+ * once: on a stream that is being captured into a graph it returns
+ * DART_ERR_UNSUPPORTED with nothing enqueued. Without this flag the call is
  * asynchronous.
  *
  *   dhidden:    [T, ld_dh] output, float32, or bfloat16 with

@@ -61,6 +61,8 @@ bool enabled() {
 
 dart_status_t run(hipStream_t stream, std::initializer_list<Item> items) {
     if (!enabled()) return DART_OK;
+    // the validation waits for its result: not possible under graph capture
+    if (const dart_status_t st = may_synchronize(stream); st != DART_OK) return st;
     // one validation at a time in the process: the flags are shared by every
     // call on a device
     static std::mutex mu;

@@ -34,6 +34,15 @@ inline int stream_device(hipStream_t stream) {
     return dev;
 }
 
+// DART_OK when work on the stream may wait for the host (the stream is not
+// being captured into a graph), DART_ERR_UNSUPPORTED when it is being captured,
+// DART_ERR_HIP when HIP cannot tell.
+inline dart_status_t may_synchronize(hipStream_t stream) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return DART_ERR_HIP;
+    return cs == hipStreamCaptureStatusNone ? DART_OK : DART_ERR_UNSUPPORTED;
+}
+
 // The optional validation of device-side preconditions (DART_CHECK=1 in the
 // environment).
 namespace dart_check {

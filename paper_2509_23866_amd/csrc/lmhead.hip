@@ -927,6 +927,9 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     const BackwardPlan P = plan_backward(T, d, V, chunk_rows, chunk_cols, flags);
     if (P.total == 0) return DART_ERR_UNSUPPORTED;
     if (workspace_bytes < P.total) return DART_ERR_INVALID_ARG;
+    // skipping rows waits for the kept-row count: not possible under graph capture
+    if (P.skip)
+        if (const dart_status_t st = may_synchronize(stream); st != DART_OK) return st;
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;

@@ -70,3 +70,61 @@ def test_graph_replays_match_eager(T):
             assert torch.equal(gb[k].view(torch.uint8), v.view(torch.uint8)), (rep, k)
         step(eager)  # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_synchronising_modes_refused_under_capture(monkeypatch):
+    """The row-skipping LM-head backward and DART_CHECK=1 wait for the host; on a
+    stream that is being captured they return DART_ERR_UNSUPPORTED with nothing
+    enqueued, the capture goes on (a statistics call captured after them
+    replays to the eager bits), and the row-skipping call works eagerly."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 64, 64, 300
+    rng = np.random.default_rng(5)
+    h = torch.from_numpy(rng.normal(0, 1, (T, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    w = torch.from_numpy(rng.normal(0, 0.3, (V, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    y = _cuda(rng.integers(0, V, T).astype(np.int32))
+    logits = torch.from_numpy(rng.normal(0, 3, (T, V)).astype(np.float32)).cuda()
+    logp, _, lse = dart.dart_lmhead_tok_stats(h, w, y)
+    coef = _cuda(np.where(rng.random(T) < 0.3, 0.0, 1e-2).astype(np.float32))
+    skip = dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    dh = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    dw = torch.empty((V, d), dtype=torch.float32, device="cuda")
+    ws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, T, V, skip),
+                     dtype=torch.uint8, device="cuda")
+    out = [torch.empty(T, dtype=torch.float32, device="cuda") for _ in range(3)]
+    ref = dart.dart_tok_stats(logits, y)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    codes = []
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        try:
+            dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=T, chunk_cols=V,
+                                         flags=skip, dhidden=dh, dweight=dw, workspace=ws,
+                                         stream=side)
+        except dart.DartError as e:
+            codes.append(e.code)
+        monkeypatch.setenv("DART_CHECK", "1")
+        try:
+            dart.dart_tok_stats(logits, y, *out, stream=side)
+        except dart.DartError as e:
+            codes.append(e.code)
+        monkeypatch.setenv("DART_CHECK", "0")
+        dart.dart_tok_stats(logits, y, *out, stream=side)
+    assert codes == [dart.DART_ERR_UNSUPPORTED, dart.DART_ERR_UNSUPPORTED]
+    for _ in range(2):
+        for o in out:
+            o.fill_(-1.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, r in zip(out, ref):
+            assert torch.equal(o, r)
+    dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=T, chunk_cols=V, flags=skip,
+                                 dhidden=dh, dweight=dw, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.all(dh[torch.from_numpy(coef.cpu().numpy() == 0.0).cuda()] == 0.0)
