@@ -405,7 +405,8 @@ enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
  * kept, the call copies that count to the host and synchronises the stream
  * once: on a stream that is being captured into a graph it returns
  * DART_ERR_UNSUPPORTED with nothing enqueued. Without this flag the call is
- * asynchronous.
+ * asynchronous and can be captured into a HIP graph (the BLAS library's
+ * kernels included).
  *
  *   dhidden:    [T, ld_dh] output, float32, or bfloat16 with
  *               DART_LMHEAD_BF16_GRADS; ld_dh >= d.

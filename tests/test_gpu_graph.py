@@ -128,3 +128,67 @@ def test_synchronising_modes_refused_under_capture(monkeypatch):
                                  dhidden=dh, dweight=dw, workspace=ws)
     torch.cuda.synchronize()
     assert torch.all(dh[torch.from_numpy(coef.cpu().numpy() == 0.0).cuda()] == 0.0)
+
+
+@pytest.mark.parametrize("rows,cols,bf16", [(256, 300, False), (100, 128, True)])
+def test_lmhead_step_graph_replays_match_eager(rows, cols, bf16):
+    """The fused LM-head step (statistics, selection, loss, blocked backward
+    with its library GEMMs) captured once: every replay gives the eager bits,
+    with eager work and synchronisations between replays."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V, S = 256, 64, 300, 8
+    rng = np.random.default_rng(11)
+    h = torch.from_numpy(rng.normal(0, 1, (T, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    w = torch.from_numpy(rng.normal(0, 0.3, (V, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    y = _cuda(rng.integers(0, V, T).astype(np.int32))
+    off = _cuda(np.r_[0, np.sort(rng.choice(np.arange(1, T), S - 1, replace=False)), T].astype(np.int32))
+    lp_old = _cuda(rng.normal(-5, 1, T).astype(np.float32))
+    lp_roll = lp_old + _cuda(rng.normal(0, 0.1, T).astype(np.float32))
+    adv = _cuda(rng.normal(0, 1, T).astype(np.float32))
+    flags = dart.DART_LMHEAD_BF16_GRADS if bf16 else 0
+    gdt = torch.bfloat16 if bf16 else torch.float32
+    f = lambda n: torch.empty(n, dtype=torch.float32, device="cuda")  # noqa: E731
+    b = dict(logp=f(T), ent=f(T), lse=f(T), sh=f(S),
+             mask=torch.empty(S, dtype=torch.uint8, device="cuda"),
+             nk=torch.empty(1, dtype=torch.int32, device="cuda"),
+             loss=torch.empty(1, dtype=torch.float64, device="cuda"), coef=f(T), st=f(4),
+             sws=torch.empty(dart.dart_lmhead_stats_workspace_bytes(T, V), dtype=torch.uint8,
+                             device="cuda"),
+             lws=torch.empty(dart.dart_tis_loss_workspace_bytes(T), dtype=torch.uint8, device="cuda"),
+             bws=torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, flags),
+                             dtype=torch.uint8, device="cuda"),
+             dh=torch.empty((T, d), dtype=gdt, device="cuda"),
+             dw=torch.empty((V, d), dtype=gdt, device="cuda"))
+
+    def step(s):
+        dart.dart_lmhead_tok_stats(h, w, y, b["logp"], b["ent"], b["lse"], workspace=b["sws"],
+                                   stream=s)
+        dart.dart_step_select(b["ent"], off, 0.6, b["sh"], b["mask"], b["nk"], stream=s)
+        dart.dart_tis_loss_fwd(b["logp"], lp_old, lp_roll, adv, off, b["mask"], 0.2, 0.28, 2.0,
+                               loss=b["loss"], tok_coef=b["coef"], stats=b["st"],
+                               workspace=b["lws"], stream=s)
+        dart.dart_lmhead_backward_ex(h, w, y, b["lse"], b["logp"], b["coef"], chunk_rows=rows,
+                                     chunk_cols=cols, flags=flags, dhidden=b["dh"],
+                                     dweight=b["dw"], workspace=b["bws"], stream=s)
+
+    keys = ("logp", "ent", "lse", "mask", "loss", "coef", "dh", "dw")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(side)
+    torch.cuda.synchronize()
+    eager = {k: b[k].clone() for k in keys}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        step(side)
+    for _ in range(3):
+        for k in keys:
+            b[k].view(torch.uint8).fill_(0x7F)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in keys:
+            assert torch.equal(b[k].view(torch.uint8), eager[k].view(torch.uint8)), k
