@@ -271,7 +271,69 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
                                                       stream=stream))
         out.update({"library_gemm_logits_ms": gemm_ms, "library_gemm_TFLOPs": tf(gemm_ms),
                     "unfused_stats_ms": gemm_ms + tstats_ms})
+        out["training_step"] = training_steps(wl, dev, stream, h, w, target, zbuf, timed)
     return out
+
+
+def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
+    """One whole LM-head training step with bf16 gradients, two ways: fused
+    (statistics, selection, loss and the blocked backward in its 512 MiB plan;
+    the logits are formed twice and never stored) and through the library
+    (the logits and the dlogits materialised in bf16: GEMM, statistics,
+    selection, loss, gradient pass, two GEMMs), with the workload's steps,
+    advantages and old-policy log-probs."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, V, d = h.shape[0], w.shape[0], h.shape[1]
+    dv = lambda a: torch.from_numpy(a).to(dev)  # noqa: E731
+    off, adv = dv(wl.off.astype("int32")), dv(wl.adv)
+    f = lambda n: torch.empty(n, dtype=torch.float32, device=dev)  # noqa: E731
+    logp, ent, lse, coef, sh, st = f(T), f(T), f(T), f(T), f(wl.S), f(4)
+    mask = torch.empty(wl.S, dtype=torch.uint8, device=dev)
+    nk = torch.empty(1, dtype=torch.int32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, stream=stream)
+    torch.cuda.synchronize(dev)
+    lp_old = (logp.double() + dv(wl.old_offset)).float()
+    lp_roll = (lp_old.double() + dv(wl.roll_offset)).float()
+    lws = torch.empty(dart.dart_tis_loss_workspace_bytes(T), dtype=torch.uint8, device=dev)
+    sws = torch.empty(dart.dart_lmhead_stats_workspace_bytes(T, V), dtype=torch.uint8, device=dev)
+    rows, cols = dart.lmhead_backward_plan(T, V)
+    bf = dart.DART_LMHEAD_BF16_GRADS
+    bws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, bf),
+                      dtype=torch.uint8, device=dev)
+    dh = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((V, d), dtype=torch.bfloat16, device=dev)
+    dzbuf = torch.empty_like(zbuf)
+
+    def loss_part():
+        dart.dart_step_select(ent, off, wl.rho, sh, mask, nk, stream=stream)
+        dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, wl.eps_low, wl.eps_high,
+                               wl.C, loss=loss, tok_coef=coef, stats=st, workspace=lws,
+                               stream=stream)
+
+    def fused():
+        dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, workspace=sws, stream=stream)
+        loss_part()
+        dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef, chunk_rows=rows,
+                                     chunk_cols=cols, flags=bf, dhidden=dh, dweight=dw,
+                                     workspace=bws, stream=stream)
+
+    def library():
+        with torch.cuda.stream(stream):
+            torch.matmul(h, w.t(), out=zbuf)
+            dart.dart_tok_stats(zbuf, target, logp, ent, lse, stream=stream)
+            loss_part()
+            dart.dart_tis_grad(zbuf, target, logp, lse, coef, dzbuf, stream=stream)
+            torch.matmul(dzbuf, w, out=dh)
+            torch.matmul(dzbuf.t(), h, out=dw)
+
+    fused_ms, library_ms = timed(fused), timed(library)
+    return {"fused_ms": fused_ms, "fused_workspace_bytes": sws.numel() + bws.numel(),
+            "library_ms": library_ms, "library_logits_bytes": 2 * zbuf.numel() * 2,
+            "block": [rows, cols]}
 
 
 def main():
