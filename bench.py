@@ -52,7 +52,8 @@ def parse_args():
 
 def kernel_source_hash():
     src = os.path.join(ROOT, "paper_2509_23866_amd", "csrc", "dart.hip")
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    with open(src, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
 def measured_traffic(workload):
@@ -61,7 +62,8 @@ def measured_traffic(workload):
     path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path))
+    with open(path) as fh:
+        rec = json.load(fh)
     if rec.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")

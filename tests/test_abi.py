@@ -18,7 +18,8 @@ def _declared_functions():
     names = set()
     for fn in os.listdir(os.path.join(ROOT, "include")):
         if fn.endswith(".h"):
-            text = open(os.path.join(ROOT, "include", fn)).read()
+            with open(os.path.join(ROOT, "include", fn)) as fh:
+                text = fh.read()
             text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
             names.update(re.findall(r"\b(dart_[a-z_0-9]+)\s*\(", text))
     return names

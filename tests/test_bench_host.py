@@ -23,7 +23,8 @@ def test_traffic_only_for_the_measured_source():
 
     for wl in ("vlm7b", "longhorizon"):
         path = os.path.join(ROOT, "profiles", f"tis_grad_kernel_{wl}_traffic.json")
-        rec = json.load(open(path))
+        with open(path) as fh:
+            rec = json.load(fh)
         got = bench.measured_traffic(wl)
         if rec["kernel_source_sha256_16"] == bench.kernel_source_hash():
             assert got == rec["hbm_bytes_per_launch"]

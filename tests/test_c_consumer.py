@@ -18,7 +18,8 @@ ROCM = "/opt/rocm"
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    with open(HEADER) as fh:
+        text = fh.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(dart_\w+)\s*\(", text)))
 

@@ -76,7 +76,8 @@ MUTATIONS = {
 @pytest.mark.parametrize("name", sorted(MUTATIONS))
 def test_planted_mistake_is_caught(name, tmp_path):
     old, new = MUTATIONS[name]
-    src = open(oracle.SRC).read()
+    with open(oracle.SRC) as fh:
+        src = fh.read()
     assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
     mutated = tmp_path / "mutated.c"
     mutated.write_text(src.replace(old, new))
