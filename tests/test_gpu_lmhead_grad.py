@@ -8,9 +8,19 @@ points); the oracle side computes its float64 statistics and gradients from
 the same bf16 inputs. The per-token coefficient g = dL/dlogp is an input of
 both (seeded float32, with zeros as dropped tokens have).
 
-dhidden and dweight: the GPU rounds dlogits to bf16 (relative error at most
-2^-9) and accumulates in fp32, so each element is compared against
-2^-8 * (|dz| |W|) (resp. |dz|^T |h|), twice the rounding bound."""
+dhidden and dweight, each element two ways, with B = |dz| |W| (resp.
+|dz|^T |h|) the sum of the absolute terms:
+- against the oracle's exact product: the GPU's bf16 dlogits are within one
+  bf16 ulp of the correctly rounded value (checked element by element above),
+  so within 1.5 ulp <= 3 U of the exact value (U = 2^-8, the unit roundoff of
+  bf16's 8-bit significand, and an ulp is at most 2 U relative), and the
+  library sums in fp32: tolerance 3 U B + A B, with A = 2^-13 for the fp32
+  sums;
+- against the exact product of the GPU's own bf16 dlogits (the same kernel's
+  output, bit for bit the values the backward multiplies): only the fp32 sums
+  differ, tolerance A B. This is the tight check: a block left out or added
+  twice, or a wrong offset, moves an element by far more than A B.
+A bf16 gradient adds its own rounding, U |value| (round to nearest even)."""
 
 import math
 import zlib
@@ -27,7 +37,8 @@ from tests import _harness as H
 
 pytestmark = pytest.mark.gpu
 
-BF16_REL = 2.0 ** -8
+U = 2.0 ** -8   # unit roundoff of bf16
+A = 2.0 ** -13  # fp32 summation by the BLAS library, relative to the sum of |terms|
 
 
 def _dev_bf16(bits, pad=0):
@@ -67,29 +78,42 @@ def _bits(t):
     return t.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def _check_product(got, ref, bound, name):
-    err = np.abs(got.astype(np.float64) - ref)
-    tol = BF16_REL * bound + 1e-30
-    bad = err > tol
-    if np.any(bad):
-        i = tuple(np.argwhere(bad)[0])
-        raise AssertionError(f"{name}: {bad.sum()} elements beyond 2^-8 |dz||.|; first at {i}: "
-                             f"got {got[i]!r} ref {ref[i]!r} bound {bound[i]!r}")
-    return float((err / np.maximum(bound, 1e-300)).max())
+def _as_f64(x):
+    import torch
+
+    if isinstance(x, torch.Tensor):
+        x = x.float().cpu().numpy()
+    return np.asarray(x, dtype=np.float64)
 
 
-def _check_product_bf16(got, ref, bound, name):
-    """A bf16 gradient: the bound of the fp32 outputs plus the output's own
-    rounding (2^-9 |value|), with the same factor 2."""
-    got = got.float().cpu().numpy().astype(np.float64)
-    err = np.abs(got - ref)
-    tol = BF16_REL * (bound + np.abs(ref)) + 1e-30
-    bad = err > tol
-    if np.any(bad):
-        i = tuple(np.argwhere(bad)[0])
-        raise AssertionError(f"{name}: {bad.sum()} elements beyond 2^-8 (|dz||.| + |ref|); first "
-                             f"at {i}: got {got[i]!r} ref {ref[i]!r} bound {bound[i]!r}")
-    return float((err / np.maximum(bound + np.abs(ref), 1e-300)).max())
+def _check_grad(got, ref, own, bound, name, bf16=False):
+    """got against the oracle's exact product ref (3 U B + A B) and against the
+    exact product own of the GPU's own bf16 dlogits (A B); a bf16 output adds
+    U |value| to both. Returns the largest error against ref in units of B."""
+    got = _as_f64(got)
+    for what, target, tol in (("oracle", ref, (3 * U + A) * bound),
+                              ("own dlogits", own, A * bound)):
+        if bf16:
+            tol = tol + U * np.abs(target)
+        err = np.abs(got - target)
+        bad = err > tol + 1e-30
+        if np.any(bad):
+            i = tuple(np.argwhere(bad)[0])
+            raise AssertionError(f"{name} vs {what}: {bad.sum()} elements out of tolerance; first "
+                                 f"at {i}: got {got[i]!r} ref {target[i]!r} B {bound[i]!r}")
+    return float((np.abs(got - ref) / np.maximum(bound, 1e-300)).max())
+
+
+def _own_dz(hd, wd, yd, lse, logp, gd):
+    """The GPU's own bf16 dlogits (the kernel every backward runs), as float64."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, V = hd.shape[0], wd.shape[0]
+    buf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
+    dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, dlogits=buf[:, :V])
+    return buf[:, :V].double().cpu().numpy()
 
 
 SHAPES = [
@@ -150,10 +174,11 @@ def test_lmhead_backward_shapes(T, d, V, pad, chunk):
     dw = torch.full((V, d), 12345.0, dtype=torch.float32, device="cuda")  # overwritten
     dart.dart_lmhead_backward(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=chunk,
                               dhidden=dh[:, :d], dweight=dw)
+    dzo = _own_dz(hd, wd, yd, lse, logp, _cuda(g))
     torch.cuda.synchronize()
     adz = np.abs(dz64)
-    rh = _check_product(dh[:, :d].cpu().numpy(), dh64, adz @ np.abs(w64), "dhidden")
-    rw = _check_product(dw.cpu().numpy(), dw64, adz.T @ np.abs(h64), "dweight")
+    rh = _check_grad(dh[:, :d], dh64, dzo @ w64, adz @ np.abs(w64), "dhidden")
+    rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight")
     assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
     H.log(f"lmhead backward T={T} d={d} V={V} chunk={chunk}: dh {rh:.2e} dW {rw:.2e} of |dz||.|")
 
@@ -171,15 +196,16 @@ def test_lmhead_backward_chunking_consistent():
     logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
     dha, dwa = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=300)
     dhb, dwb = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=77)
-    dz = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd).float()
+    dz = _own_dz(hd, wd, yd, lse, logp, gd)
     torch.cuda.synchronize()
-    ref = (dz.T.cpu().double() @ torch.from_numpy(oracle.bf16_bits_to_f64(h))).numpy()
-    bound = np.abs(dz.T.cpu().double().numpy()) @ np.abs(oracle.bf16_bits_to_f64(h))
-    for dwx in (dwa, dwb):
-        # against the bf16 dlogits themselves: only fp32 summation error remains
-        err = np.abs(dwx.cpu().numpy() - ref)
-        assert np.all(err <= 1e-4 * bound + 1e-30)
-    assert torch.allclose(dha, dhb, rtol=1e-5, atol=1e-7)
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    # against the exact products of the GPU's own bf16 dlogits: only the fp32
+    # summation differs between chunkings
+    for x, ref, bound in ((dwa, dz.T @ h64, np.abs(dz).T @ np.abs(h64)),
+                          (dwb, dz.T @ h64, np.abs(dz).T @ np.abs(h64)),
+                          (dha, dz @ w64, np.abs(dz) @ np.abs(w64)),
+                          (dhb, dz @ w64, np.abs(dz) @ np.abs(w64))):
+        assert np.all(np.abs(x.cpu().numpy() - ref) <= A * bound + 1e-30)
 
 
 def test_lmhead_backward_vlm7b_shape():
@@ -210,11 +236,17 @@ def test_lmhead_backward_vlm7b_shape():
     # the row-skipping backward: the GEMMs over the rows of R only
     dhs, dws = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=1024,
                                             chunk_cols=V, flags=dart.DART_LMHEAD_SKIP_ZERO_ROWS)
+    # the default plan's blocks with bf16 gradients, as the autograd function runs them
+    pr, pc = dart.lmhead_backward_plan(T, V)
+    assert pc < V
+    dhb, dwb = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=pr, chunk_cols=pc,
+                                            flags=dart.DART_LMHEAD_BF16_GRADS)
     torch.cuda.synchronize()
     dh, dhs = dh.cpu().numpy(), dhs.cpu().numpy()
     outside = np.ones(T, bool)
     outside[R] = False
     assert np.all(dh[outside] == 0.0) and np.all(dhs[outside] == 0.0)
+    assert torch.all(dhb[torch.from_numpy(outside).cuda()] == 0.0)
 
     hb = prob.hidden_bits(R)
     wb = sn.gaussian_bits_host(wl.seed, STREAM_WEIGHT, V, d, prob.sigma_w)
@@ -224,20 +256,28 @@ def test_lmhead_backward_vlm7b_shape():
     dz64 = oracle.dlogits(z, y, rlse, rlogp, g[R])
     del z
     w64, h64 = oracle.bf16_bits_to_f64(wb), oracle.bf16_bits_to_f64(hb)
+    # the GPU's own dlogits of the rows of R
+    Rd = torch.from_numpy(R).cuda()
+    dzo = _own_dz(hd[Rd].contiguous(), wd, yd[Rd].contiguous(), lse[Rd].contiguous(),
+                  logp[Rd].contiguous(), gd[Rd].contiguous())
     adz = np.abs(dz64)
-    ref_h, bound_h = dz64 @ w64, adz @ np.abs(w64)
-    rh = _check_product(dh[R], ref_h, bound_h, "dhidden")
-    rhs = _check_product(dhs[R], ref_h, bound_h, "dhidden (rows skipped)")
+    ref_h, own_h, bound_h = dz64 @ w64, dzo @ w64, adz @ np.abs(w64)
+    rh = _check_grad(dh[R], ref_h, own_h, bound_h, "dhidden")
+    rhs = _check_grad(dhs[R], ref_h, own_h, bound_h, "dhidden (rows skipped)")
+    rhb = _check_grad(dhb[Rd], ref_h, own_h, bound_h, "dhidden (plan, bf16)", bf16=True)
     del w64
-    rw = rws = 0.0
+    rw = rws = rwb = 0.0
     for v0 in range(0, V, 16384):
         sl = slice(v0, min(V, v0 + 16384))
-        ref, bound = dz64[:, sl].T @ h64, adz[:, sl].T @ np.abs(h64)
-        rw = max(rw, _check_product(dw[sl].cpu().numpy(), ref, bound, f"dweight rows {v0}+"))
-        rws = max(rws, _check_product(dws[sl].cpu().numpy(), ref, bound,
-                                      f"dweight rows {v0}+ (rows skipped)"))
+        ref, own = dz64[:, sl].T @ h64, dzo[:, sl].T @ h64
+        bound = adz[:, sl].T @ np.abs(h64)
+        rw = max(rw, _check_grad(dw[sl], ref, own, bound, f"dweight rows {v0}+"))
+        rws = max(rws, _check_grad(dws[sl], ref, own, bound, f"dweight rows {v0}+ (rows skipped)"))
+        rwb = max(rwb, _check_grad(dwb[sl], ref, own, bound, f"dweight rows {v0}+ (plan, bf16)",
+                                   bf16=True))
     H.log(f"lmhead backward vlm7b: dh {rh:.2e} dW {rw:.2e} of |dz||.|; "
-          f"rows skipped: dh {rhs:.2e} dW {rws:.2e}")
+          f"rows skipped: dh {rhs:.2e} dW {rws:.2e}; plan {pr}x{pc} bf16: dh {rhb:.2e} "
+          f"dW {rwb:.2e}")
 
 
 def test_lmhead_caller_workspaces_contents_do_not_matter():
@@ -319,9 +359,10 @@ def test_lmhead_backward_skip_zero_rows(T, d, V, pad, chunk, kind):
     assert np.all(got_h[g == 0.0] == 0.0), "a dropped row of dhidden is not 0"
     if not np.any(g):
         assert torch.all(dw == 0.0)
+    dzo = _own_dz(hd, wd, yd, lse, logp, _cuda(g))
     adz = np.abs(dz64)
-    rh = _check_product(got_h, dh64, adz @ np.abs(w64), "dhidden")
-    rw = _check_product(dw.cpu().numpy(), dw64, adz.T @ np.abs(h64), "dweight")
+    rh = _check_grad(got_h, dh64, dzo @ w64, adz @ np.abs(w64), "dhidden")
+    rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight")
     H.log(f"lmhead backward rows skipped T={T} d={d} V={V} chunk={chunk} {kind} "
           f"({int(np.count_nonzero(g))} rows kept): dh {rh:.2e} dW {rw:.2e} of |dz||.|")
 
@@ -365,7 +406,7 @@ def test_lmhead_backward_skip_zero_rows_reused_workspace():
                                 (dha, dz @ w64, adz @ np.abs(w64)),
                                 (dws, dz.T @ h64, adz.T @ np.abs(h64)),
                                 (dwa, dz.T @ h64, adz.T @ np.abs(h64))):
-            assert np.all(np.abs(got.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
+            assert np.all(np.abs(got.cpu().numpy() - ref) <= A * bound + 1e-30)
 
 
 _SKIP, _BF = 1, 4
@@ -417,14 +458,11 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, rows, cols, flags):
     assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
     if flags & _SKIP:
         assert torch.all(dh[:, :d][torch.from_numpy(g == 0.0).cuda()] == 0.0)
+    dzo = _own_dz(hd, wd, yd, lse, logp, _cuda(g))
     adz = np.abs(dz64)
-    bh, bw = adz @ np.abs(w64), adz.T @ np.abs(h64)
-    if flags & _BF:
-        rh = _check_product_bf16(dh[:, :d], dh64, bh, "dhidden")
-        rw = _check_product_bf16(dw, dw64, bw, "dweight")
-    else:
-        rh = _check_product(dh[:, :d].cpu().numpy(), dh64, bh, "dhidden")
-        rw = _check_product(dw.cpu().numpy(), dw64, bw, "dweight")
+    bf = bool(flags & _BF)
+    rh = _check_grad(dh[:, :d], dh64, dzo @ w64, adz @ np.abs(w64), "dhidden", bf16=bf)
+    rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight", bf16=bf)
     H.log(f"lmhead backward_ex T={T} d={d} V={V} block={rows}x{cols} flags={flags}: "
           f"dh {rh:.2e} dW {rw:.2e}")
 
@@ -456,11 +494,11 @@ def test_lmhead_backward_blockings_agree():
     torch.cuda.synchronize()
     for got in outs:
         for x, (ref, bound) in zip(got, refs):
-            assert np.all(np.abs(x.cpu().numpy() - ref) <= 1e-4 * bound + 1e-30)
+            assert np.all(np.abs(x.cpu().numpy() - ref) <= A * bound + 1e-30)
     for bf, fp in zip(bfs, outs):
         for xb, xf, (_, bound) in zip(bf, fp, refs):
             # one rounding of the fp32 sum, up to the fp32 summation order of
             # the library's kernels for bf16 and fp32 outputs
             a = xb.float().cpu().numpy().astype(np.float64)
             b = xf.cpu().numpy().astype(np.float64)
-            assert np.all(np.abs(a - b) <= 2.0 ** -8 * np.abs(b) + 1e-4 * bound + 1e-37)
+            assert np.all(np.abs(a - b) <= U * np.abs(b) + A * bound + 1e-37)
