@@ -16,7 +16,7 @@
  *   caller owns every buffer; the library allocates no memory and keeps no
  *   state between calls, so concurrent calls on different streams are safe
  *   (the one exception, dart_lmhead_backward, keeps a ROCm BLAS handle per
- *   device and serialises its own calls).
+ *   device and stream and serialises its own calls).
  * - Every call is asynchronous on `stream` (0 = the null stream): it checks its
  *   scalar arguments on the host, enqueues its kernels and returns. Outputs are
  *   valid once the stream is synchronised. Device data (target ids in range,
@@ -352,9 +352,10 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
  *               dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
  *               bytes, 16-byte aligned, owned by the caller; contents on entry
  *               do not matter.
- * The first call on a device creates that device's BLAS handle (the library
- * allocates its own memory then); the handle lives until the process ends and
- * calls into this function are serialised on it. Errors: as for
+ * The first call on a device and stream creates a BLAS handle for them (the
+ * library allocates its own memory then, including a device workspace that two
+ * streams must not share); the handle lives until the process ends, and calls
+ * into this function are serialised while they enqueue. Errors: as for
  * dart_lmhead_dlogits, INVALID_ARG also for a null output, bad ld_dh/ld_dw,
  * chunk_rows < 1 or a workspace that is too small; UNSUPPORTED for a leading
  * dimension above INT32_MAX (the BLAS library's limit); HIP when the BLAS

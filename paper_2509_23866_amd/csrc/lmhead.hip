@@ -29,6 +29,7 @@
 
 #include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "internal.h"
 #include "dart.h"
@@ -666,20 +667,36 @@ dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, in
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
-// One rocBLAS handle per device, created on first use and kept until the
-// process ends; calls that use it are serialised by the mutex (the handle's
-// stream is set per call).
-constexpr int kMaxDevices = 64;
+// One rocBLAS handle per device and stream, created on the first call on that
+// stream and kept until the process ends. A handle owns a device workspace that
+// some of the library's kernels use, so two streams never share one: their
+// GEMMs may run at the same time. Calls are serialised by the mutex (the
+// lookup, and the enqueueing on one handle).
 std::mutex g_blas_mu;
-rocblas_handle g_blas[kMaxDevices] = {};
+struct BlasEntry {
+    int dev;
+    hipStream_t stream;
+    rocblas_handle handle;
+};
+std::vector<BlasEntry> g_blas;
 
-// The handle of the current device (a handle belongs to the device current
-// when it is created), created on first use.
-rocblas_handle blas_handle(int dev) {
-    if (dev < 0 || dev >= kMaxDevices) return nullptr;
-    if (!g_blas[dev] && rocblas_create_handle(&g_blas[dev]) != rocblas_status_success)
-        g_blas[dev] = nullptr;
-    return g_blas[dev];
+// The handle of (dev, stream), bound to that stream; dev must be current (a
+// handle belongs to the device current when it is created). The caller holds
+// g_blas_mu.
+rocblas_handle blas_handle(int dev, hipStream_t stream) {
+    for (const BlasEntry& e : g_blas)
+        if (e.dev == dev && e.stream == stream)
+            // the stream may be a new one at the address of a destroyed one
+            return rocblas_set_stream(e.handle, stream) == rocblas_status_success ? e.handle
+                                                                                 : nullptr;
+    rocblas_handle h = nullptr;
+    if (rocblas_create_handle(&h) != rocblas_status_success) return nullptr;
+    if (rocblas_set_stream(h, stream) != rocblas_status_success) {
+        (void)rocblas_destroy_handle(h);
+        return nullptr;
+    }
+    g_blas.push_back({dev, stream, h});
+    return h;
 }
 
 }  // namespace
@@ -940,8 +957,8 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     DeviceGuard on_dev(dev);
     if (!on_dev.ok) return DART_ERR_HIP;
     std::lock_guard<std::mutex> lock(g_blas_mu);
-    rocblas_handle blas = blas_handle(dev);
-    if (!blas || rocblas_set_stream(blas, stream) != rocblas_status_success) return DART_ERR_HIP;
+    rocblas_handle blas = blas_handle(dev, stream);
+    if (!blas) return DART_ERR_HIP;
     const uint16_t* h = static_cast<const uint16_t*>(hidden);
     const uint16_t* w = static_cast<const uint16_t*>(weight);
     char* ws = static_cast<char*>(workspace);
