@@ -145,11 +145,18 @@ def _torch():
     return torch
 
 
-def _stream_handle(stream):
+def _stream_handle(stream, device):
+    """The HIP stream a call enqueues on: for None the current stream of the
+    inputs' device (not of the current device); a torch stream, which must
+    belong to the inputs' device; or a raw hipStream_t handle, taken as given."""
     torch = _torch()
     if stream is None:
-        stream = torch.cuda.current_stream()
-    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        return torch.cuda.current_stream(device).cuda_stream
+    if hasattr(stream, "cuda_stream"):
+        if torch.device(stream.device) != torch.device(device):
+            raise ValueError(f"the stream is on {stream.device}, the inputs on {device}")
+        return stream.cuda_stream
+    return int(stream)
 
 
 def _ptr(t):
@@ -217,13 +224,13 @@ def dart_tok_stats(logits, target, logp=None, entropy=None, lse=None, stream=Non
     if inv_temp == 1.0:
         rc = load_library().dart_tok_stats(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
                                            logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
-                                           _stream_handle(stream))
+                                           _stream_handle(stream, dev))
         name = "dart_tok_stats"
     else:
         rc = load_library().dart_tok_stats_ex(logits.data_ptr(), dt, T, V, ld, target.data_ptr(),
                                               float(inv_temp), logp.data_ptr(),
                                               entropy.data_ptr(), lse.data_ptr(),
-                                              _stream_handle(stream))
+                                              _stream_handle(stream, dev))
         name = "dart_tok_stats_ex"
     if rc != DART_OK:
         raise DartError(name, rc)
@@ -248,7 +255,7 @@ def dart_step_select(entropy, step_offsets, rho, step_entropy=None, step_mask=No
     _check_vec("n_kept_steps", n_kept_steps, torch.int32, 1, dev)
     rc = load_library().dart_step_select(entropy.data_ptr(), T, step_offsets.data_ptr(), S,
                                          float(rho), step_entropy.data_ptr(), step_mask.data_ptr(),
-                                         n_kept_steps.data_ptr(), _stream_handle(stream))
+                                         n_kept_steps.data_ptr(), _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_step_select", rc)
     return step_entropy, step_mask, n_kept_steps
@@ -291,7 +298,7 @@ def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv
         logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(), step_offsets.data_ptr(), S,
         step_mask.data_ptr(), float(eps_low), float(eps_high), float(C), dlogits.data_ptr(),
         dlogits.stride(0), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes,
-        _stream_handle(stream))
+        _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd_bwd", rc)
     return loss, dlogits, tok_coef, stats
@@ -324,7 +331,7 @@ def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask
         T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(),
         step_offsets.data_ptr(), S, step_mask.data_ptr(), float(eps_low), float(eps_high),
         float(C), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes,
-        _stream_handle(stream))
+        _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd", rc)
     return loss, tok_coef, stats
@@ -363,7 +370,7 @@ def dart_tis_loss_fwd_ex(logp, logp_old, logp_rollout, adv, step_offsets, step_m
         T, logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(),
         None if DART_KL[kl] == 0 else logp_ref.data_ptr(), adv.data_ptr(),
         step_offsets.data_ptr(), S, step_mask.data_ptr(), ctypes.byref(cfg), loss.data_ptr(),
-        tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes, _stream_handle(stream))
+        tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes, _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd_ex", rc)
     return loss, tok_coef, stats
@@ -388,14 +395,14 @@ def dart_tis_grad(logits, target, logp, lse, tok_coef, dlogits=None, stream=None
     if inv_temp == 1.0 and not skip_zero_rows:
         rc = load_library().dart_tis_grad(
             logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
-            tok_coef.data_ptr(), dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+            tok_coef.data_ptr(), dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream, dev))
         name = "dart_tis_grad"
     else:
         rc = load_library().dart_tis_grad_ex(
             logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
             tok_coef.data_ptr(), float(inv_temp),
             DART_GRAD_SKIP_ZERO_ROWS if skip_zero_rows else 0, dlogits.data_ptr(),
-            dlogits.stride(0), _stream_handle(stream))
+            dlogits.stride(0), _stream_handle(stream, dev))
         name = "dart_tis_grad_ex"
     if rc != DART_OK:
         raise DartError(name, rc)
@@ -423,7 +430,7 @@ def dart_grpo_advantage(reward, traj_step_offsets, group_traj_offsets, step_offs
     rc = load_library().dart_grpo_advantage(
         reward.data_ptr(), n_traj, traj_step_offsets.data_ptr(), group_traj_offsets.data_ptr(), G,
         step_offsets.data_ptr(), S, T, adv.data_ptr(), _ptr(group_mean), _ptr(group_std),
-        _stream_handle(stream))
+        _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_grpo_advantage", rc)
     return adv, group_mean, group_std
@@ -446,7 +453,7 @@ def dart_step_select_groups(entropy, step_offsets, group_step_offsets, rho, step
     rc = load_library().dart_step_select_groups(
         entropy.data_ptr(), T, step_offsets.data_ptr(), S, group_step_offsets.data_ptr(), G,
         float(rho), step_entropy.data_ptr(), step_mask.data_ptr(), n_kept_steps.data_ptr(),
-        _stream_handle(stream))
+        _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_step_select_groups", rc)
     return step_entropy, step_mask, n_kept_steps
@@ -500,7 +507,7 @@ def dart_lmhead_tok_stats(hidden, weight, target, logp=None, entropy=None, lse=N
     rc = load_library().dart_lmhead_tok_stats(
         hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
         target.data_ptr(), logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
-        workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+        workspace.data_ptr(), workspace.numel(), _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_lmhead_tok_stats", rc)
     return logp, entropy, lse
@@ -543,7 +550,7 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
     rc = load_library().dart_lmhead_dlogits(
         hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
         target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-        dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream))
+        dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_lmhead_dlogits", rc)
     return dlogits
@@ -582,7 +589,7 @@ def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, c
             chunk_rows]
     if flags is not None:
         args += [chunk_cols, f]
-    args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream)]
+    args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream, dev)]
     rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
         raise DartError(name, rc)

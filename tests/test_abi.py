@@ -364,3 +364,19 @@ def test_lmhead_backward_plan():
                 assert cost <= -(-T // r2) * V + -(-V // c2) * T
     r, c = plan(152569, 152064)
     assert 8192 <= r <= 32768 and 8192 <= c <= 32768
+
+
+def test_stream_must_be_on_the_inputs_device():
+    """A torch stream of another device is refused before any call (kernels
+    would run on that device against these pointers); a raw handle is taken as
+    given."""
+    import torch
+
+    class FakeStream:
+        def __init__(self, device, handle):
+            self.device, self.cuda_stream = torch.device(device), handle
+
+    assert dart._stream_handle(FakeStream("cuda:0", 1234), torch.device("cuda:0")) == 1234
+    with pytest.raises(ValueError):
+        dart._stream_handle(FakeStream("cuda:1", 1234), torch.device("cuda:0"))
+    assert dart._stream_handle(5678, torch.device("cuda:0")) == 5678
