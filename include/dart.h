@@ -31,8 +31,14 @@
  *   start is 16-byte aligned (base aligned and ld * element size a multiple of
  *   16) take the vectorised path; other rows are still correct, only slower.
  * - Status codes: DART_OK; DART_ERR_INVALID_ARG for a bad scalar argument or a
- *   null required pointer (nothing is enqueued); DART_ERR_HIP when HIP reports a
- *   launch error. No call aborts or throws.
+ *   null required pointer (nothing is enqueued); DART_ERR_UNSUPPORTED, with
+ *   nothing enqueued, for sizes beyond what a launch can hold (a dispatch holds
+ *   at most 2^32 - 1 work-items): more than 67,108,863 steps (selection),
+ *   4,194,303 groups (per-group selection) or 16,777,215 groups (GRPO
+ *   advantage), more than 8,388,607 tiles of 256 x 256 logits or 268,435,455
+ *   rows (LM head); DART_ERR_HIP when HIP reports a launch error. No call
+ *   aborts or throws. The token statistics take any T up to INT32_MAX (rows
+ *   are launched 2^22 at a time).
  * - Results are deterministic: no atomics on any floating-point result, fixed
  *   reduction orders; identical rows at identical alignment give bit-identical
  *   entropies.

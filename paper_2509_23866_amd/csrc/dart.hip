@@ -236,6 +236,8 @@ __device__ __forceinline__ Triple triple_wave_reduce(Triple a) {
 // double-buffering does not.
 constexpr int kStatsThreads = 768;
 constexpr int kStatsUnroll = 4;
+constexpr int64_t kStatsMaxRows = int64_t(1) << 22;  // rows per launch of the statistics
+static_assert(kStatsMaxRows * kStatsThreads <= 0xFFFFFFFFll, "statistics grid");
 constexpr int kGradThreads = 128;
 constexpr int kGradUnroll = 2;
 constexpr int64_t kGradMaxBlocks = 1ll << 24;
@@ -1314,15 +1316,24 @@ dart_status_t dart_tok_stats_ex(const void* logits, dart_dtype_t dtype, int64_t 
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;
-    const dim3 grid((unsigned)T), block(kStatsThreads);
-    if (dtype == DART_BF16)
-        hipLaunchKernelGGL(
-            (tok_stats_kernel<DART_BF16, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
-            block, 0, stream, logits, V, ld, target, inv_temp, logp, entropy, lse);
-    else
-        hipLaunchKernelGGL(
-            (tok_stats_kernel<DART_F32, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
-            block, 0, stream, logits, V, ld, target, inv_temp, logp, entropy, lse);
+    // one workgroup per row, at most kStatsMaxRows rows per launch (a dispatch
+    // holds at most 2^32 - 1 work-items)
+    const size_t esz = elem_size(dtype);
+    for (int64_t r0 = 0; r0 < T; r0 += kStatsMaxRows) {
+        const int64_t rows = T - r0 < kStatsMaxRows ? T - r0 : kStatsMaxRows;
+        const void* lr = static_cast<const char*>(logits) + (size_t)r0 * (size_t)ld * esz;
+        const dim3 grid((unsigned)rows), block(kStatsThreads);
+        if (dtype == DART_BF16)
+            hipLaunchKernelGGL(
+                (tok_stats_kernel<DART_BF16, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
+                block, 0, stream, lr, V, ld, target + r0, inv_temp, logp + r0, entropy + r0,
+                lse + r0);
+        else
+            hipLaunchKernelGGL(
+                (tok_stats_kernel<DART_F32, kStatsThreads, kStatsUnroll, kPipe, kNtLoad>), grid,
+                block, 0, stream, lr, V, ld, target + r0, inv_temp, logp + r0, entropy + r0,
+                lse + r0);
+    }
     return launch_status();
 }
 
@@ -1342,6 +1353,7 @@ dart_status_t dart_step_select(const float* entropy, int64_t T, const int32_t* s
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Offsets, step_offsets, S, T}}); ck != DART_OK)
         return ck;
+    if (!grid_fits((S + kSelWaves - 1) / kSelWaves, kSelThreads)) return DART_ERR_UNSUPPORTED;
     if (T <= kSelLdsTokens && S <= kSelLdsKeys) {
         hipLaunchKernelGGL(step_select_kernel<true>, dim3(1), dim3(kSelThreads), 0, stream,
                            entropy, T, step_offsets, S, nullptr, rho, k, step_entropy, step_mask,
@@ -1365,6 +1377,8 @@ dart_status_t dart_step_select_groups(const float* entropy, int64_t T,
     if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll || G < 1 || G > S || G > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
     if (dart_kept_steps(S, rho) < 0) return DART_ERR_INVALID_ARG;
+    if (!grid_fits((S + kSelWaves - 1) / kSelWaves, kSelThreads) || !grid_fits(G, kSelThreads))
+        return DART_ERR_UNSUPPORTED;
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Offsets, step_offsets, S, T},
                      {dart_check::Item::Offsets, group_step_offsets, G, S}}); ck != DART_OK)
@@ -1387,6 +1401,7 @@ dart_status_t dart_grpo_advantage(const float* reward, int64_t n_traj,
     if (n_traj < 1 || G < 1 || G > n_traj || S < 1 || S > T || T > 0x7FFFFFFFll ||
         G > 0x7FFFFFFFll)
         return DART_ERR_INVALID_ARG;
+    if (!grid_fits(G, kAdvThreads)) return DART_ERR_UNSUPPORTED;
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Offsets, traj_step_offsets, n_traj, S},
                      {dart_check::Item::Offsets, group_traj_offsets, G, n_traj},

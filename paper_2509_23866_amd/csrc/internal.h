@@ -34,6 +34,12 @@ inline int stream_device(hipStream_t stream) {
     return dev;
 }
 
+// Whether a 1-D launch of blocks workgroups of threads work-items each fits
+// the dispatch (at most 2^32 - 1 work-items in the grid).
+inline bool grid_fits(int64_t blocks, int64_t threads) {
+    return blocks >= 0 && threads > 0 && blocks <= 0xFFFFFFFFll / threads;
+}
+
 // DART_OK when work on the stream may wait for the host (the stream is not
 // being captured into a graph), DART_ERR_UNSUPPORTED when it is being captured,
 // DART_ERR_HIP when HIP cannot tell.

@@ -660,7 +660,8 @@ dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, in
                              const float* coef, uint16_t* out, int64_t ld_out, int64_t vbase,
                              hipStream_t stream) {
     const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
-    if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
+    if (!grid_fits(nmt * nvt, LmCfg::THREADS) || ld_h > kMaxLd || ld_w > kMaxLd)
+        return DART_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
                        target, lse, logp, coef, out, ld_out, vbase, nmt, nvt);
@@ -723,7 +724,10 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
 
     if (workspace_bytes < dart_lmhead_stats_workspace_bytes(T, V)) return DART_ERR_INVALID_ARG;
     const int64_t nmt = (T + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
-    if (nmt * nvt > 0x7FFFFFFFll || ld_h > kMaxLd || ld_w > kMaxLd) return DART_ERR_UNSUPPORTED;
+    if (!grid_fits(nmt * nvt, LmCfg::THREADS) ||
+        !grid_fits((T + kMergeWaves - 1) / kMergeWaves, kMergeWaves * 64) || ld_h > kMaxLd ||
+        ld_w > kMaxLd)
+        return DART_ERR_UNSUPPORTED;
     float4* part = static_cast<float4*>(workspace);
     float* z_y = reinterpret_cast<float*>(part + T * nvt);
     hipLaunchKernelGGL(lmhead_stats_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)), dim3(LmCfg::THREADS),

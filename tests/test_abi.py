@@ -380,3 +380,22 @@ def test_stream_must_be_on_the_inputs_device():
     with pytest.raises(ValueError):
         dart._stream_handle(FakeStream("cuda:1", 1234), torch.device("cuda:0"))
     assert dart._stream_handle(5678, torch.device("cuda:0")) == 5678
+
+
+@pytest.mark.skipif("_gpu_visible()")
+def test_launch_limits_are_unsupported():
+    """Sizes whose launch would exceed 2^32 - 1 work-items are UNSUPPORTED,
+    decided on the host before anything is touched (fake pointers here)."""
+    lib = dart.load_library()
+    U = dart.DART_ERR_UNSUPPORTED
+    big = (1 << 31) - 1
+    # step selection: one wave per step, 1024-thread workgroups
+    assert lib.dart_step_select(P, big, P, 67108864, ctypes.c_double(0.5), P, P, P, None) == U
+    # per-group selection: one 1024-thread workgroup per group
+    assert lib.dart_step_select_groups(P, big, P, 1 << 23, P, 4194304, ctypes.c_double(0.5), P, P,
+                                       P, None) == U
+    # GRPO advantage: one 256-thread workgroup per group
+    assert lib.dart_grpo_advantage(P, 1 << 25, P, P, 16777216, P, 1 << 25, big, P, P, P, None) == U
+    # LM head: 8,388,608 tiles of 256 x 256
+    assert lib.dart_lmhead_tok_stats(P, big, 8, 8, P, 8, 8, P, P, P, P, P, (1 << 64) - 1,
+                                     None) == U

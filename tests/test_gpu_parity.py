@@ -11,6 +11,7 @@ output compared and the gradient compared element-wise on sampled rows.
 import numpy as np
 import pytest
 
+import oracle
 import synth
 from tests import _harness as H
 
@@ -147,3 +148,30 @@ def test_device_generator_matches_host():
         got = t[torch.from_numpy(rows).cuda()].cpu()
         got = got.numpy() if wl.dtype == "f32" else got.view(torch.int16).numpy().view(np.uint16)
         assert np.array_equal(got, sn.logits_rows_host(wl, rows))
+
+
+def test_tok_stats_rows_beyond_one_launch():
+    """2^22 + 999 rows of V = 8 bf16 logits, more rows than one launch of the
+    statistics takes: rows on both sides of row 2^22, the first and last rows
+    and a random sample against the oracle (tolerances of the named workloads)."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, V = (1 << 22) + 999, 8
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    logits = (torch.randn((T, V), device="cuda", generator=g) * 3.0).to(torch.bfloat16)
+    target = torch.randint(0, V, (T,), device="cuda", generator=g, dtype=torch.int32)
+    logp, ent, lse = dart.dart_tok_stats(logits, target)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(7)
+    rows = np.unique(np.r_[0, 1, (1 << 22) - 2, (1 << 22) - 1, 1 << 22, (1 << 22) + 1, T - 1,
+                           rng.integers(0, T, 200)])
+    idx = torch.from_numpy(rows).cuda()
+    z = logits[idx].view(torch.int16).cpu().numpy().view(np.uint16)
+    y = target[idx].cpu().numpy()
+    rlogp, rH, rlse = oracle.token_stats(z, y)
+    for got, ref, name in ((logp, rlogp, "logp"), (ent, rH, "entropy"), (lse, rlse, "lse")):
+        err = np.abs(got[idx].double().cpu().numpy() - ref)
+        assert err.max() <= 2e-4, (name, float(err.max()), rows[int(err.argmax())])
