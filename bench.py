@@ -277,6 +277,115 @@ def lmhead_variant(wl, dev, stream, target, coef, n):
     return out
 
 
+def _median_ms(fn, stream, dev, n):
+    """Median over n calls of fn(), each between its own pair of HIP events on
+    the stream, after one untimed call."""
+    import numpy as np
+    import torch
+
+    fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize(dev)
+    return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+
+def objective_variant(wl, dev, stream, logits, target, off, adv, lp_old, lp_roll, dlogits,
+                      default_step, n):
+    """The objective's variants on the same two passes (never the headline):
+    one whole step with inverse temperature 1.25 in both passes, the KL term
+    (k3 estimator, beta = 0.1) against the workload's reference log-probs,
+    step-mean aggregation and step-level (geometric-mean) ratios, beside the
+    default step; medians of n steps."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, V, S = wl.T, wl.V, wl.S
+    f = lambda k: torch.empty(k, dtype=torch.float32, device=dev)  # noqa: E731
+    logp, ent, lse, coef, sh, st = f(T), f(T), f(T), f(T), f(S), f(6)
+    mask = torch.empty(S, dtype=torch.uint8, device=dev)
+    nk = torch.empty(1, dtype=torch.int32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = torch.empty(dart.dart_tis_loss_workspace_bytes(T), dtype=torch.uint8, device=dev)
+    inv_temp = 1.25
+    dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream, inv_temp=inv_temp)
+    torch.cuda.synchronize(dev)
+    lp_ref = (logp.double() + torch.from_numpy(wl.ref_offset).to(dev)).float()
+
+    def step():
+        dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream, inv_temp=inv_temp)
+        dart.dart_step_select(ent, off, wl.rho, sh, mask, nk, stream=stream)
+        dart.dart_tis_loss_fwd_ex(logp, lp_old, lp_roll, adv, off, mask, wl.eps_low, wl.eps_high,
+                                  wl.C, logp_ref=lp_ref, kl="k3", beta=0.1,
+                                  aggregation="step_mean", ratio="step_geomean", loss=loss,
+                                  tok_coef=coef, stats=st, stream=stream, workspace=ws)
+        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream,
+                           inv_temp=inv_temp)
+
+    # the two steps alternate, so that both see the same clocks
+    import numpy as np
+
+    step()
+    default_step()
+    pairs = []
+    for _ in range(n):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        step()
+        ev[1].record(stream)
+        default_step()
+        ev[2].record(stream)
+        pairs.append(ev)
+    torch.cuda.synchronize(dev)
+    ms = float(np.median([e[0].elapsed_time(e[1]) for e in pairs]))
+    base = float(np.median([e[1].elapsed_time(e[2]) for e in pairs]))
+    return {"inv_temp": inv_temp, "kl": "k3", "beta": 0.1, "aggregation": "step_mean",
+            "ratio": "step_geomean", "ms_per_step": ms, "default_ms_per_step": base,
+            "logit_elements_per_s": T * V / (ms * 1e-3)}
+
+
+def groups_variant(wl, dev, stream, ent, off, n):
+    """The steps on either side of the path (never the headline): the
+    step-wise GRPO advantage and the per-group selection, with the workload's
+    steps cut into trajectories of at most 30 steps and task groups of 8
+    trajectories (the paper's episode cap and rollouts per task) and a seeded
+    0/1 reward per trajectory; medians of n calls, beside the one-group
+    selection of the headline step."""
+    import numpy as np
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    S, T = wl.S, wl.T
+    traj = np.r_[np.arange(0, S, 30), S].astype(np.int32)
+    n_traj = traj.size - 1
+    groups = np.r_[np.arange(0, n_traj, 8), n_traj].astype(np.int32)
+    G = groups.size - 1
+    reward = np.random.default_rng(wl.seed).integers(0, 2, n_traj).astype(np.float32)
+    dv = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    reward_d, traj_d, groups_d, gsteps_d = dv(reward), dv(traj), dv(groups), dv(traj[groups])
+    adv = torch.empty(T, dtype=torch.float32, device=dev)
+    gm, gs = (torch.empty(G, dtype=torch.float32, device=dev) for _ in range(2))
+    sh = torch.empty(S, dtype=torch.float32, device=dev)
+    mask = torch.empty(S, dtype=torch.uint8, device=dev)
+    nk = torch.empty(G, dtype=torch.int32, device=dev)
+    nk1 = torch.empty(1, dtype=torch.int32, device=dev)
+    grpo_ms = _median_ms(lambda: dart.dart_grpo_advantage(reward_d, traj_d, groups_d, off, T=T,
+                                                          adv=adv, group_mean=gm, group_std=gs,
+                                                          stream=stream), stream, dev, n)
+    sel_ms = _median_ms(lambda: dart.dart_step_select_groups(ent, off, gsteps_d, wl.rho, sh, mask,
+                                                             nk, stream=stream), stream, dev, n)
+    one_ms = _median_ms(lambda: dart.dart_step_select(ent, off, wl.rho, sh, mask, nk1,
+                                                      stream=stream), stream, dev, n)
+    return {"trajectories": n_traj, "groups": G, "grpo_advantage_us": grpo_ms * 1e3,
+            "step_select_groups_us": sel_ms * 1e3, "step_select_one_group_us": one_ms * 1e3}
+
+
 def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
     """One whole LM-head training step with bf16 gradients, two ways: fused
     (statistics, selection, loss and the blocked backward in its 512 MiB plan;
@@ -488,6 +597,11 @@ def main():
 
     if not wl.inplace and not args.no_variants:
         variants["hip_graph"] = graph_variant(step, stream, dev, args.steps)
+        variants["objective_variants"] = objective_variant(
+            wl, dev, stream, logits, target, off, adv, lp_old, lp_roll, dlogits, step,
+            min(args.steps, 20))
+    if not args.no_variants:
+        variants["groups"] = groups_variant(wl, dev, stream, ent, off, min(args.steps, 20))
     if not args.no_variants:
         variants["lmhead_fused"] = lmhead_variant(wl, dev, stream, target, coef,
                                                   min(args.steps, 10))
