@@ -36,7 +36,10 @@ def parse_args():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # a cold GPU runs its first ~25 steps up to 15% slower while its clocks
+    # ramp (per-step HIP events at vlm7b: 0.67 ms, then ~0.61, then ~0.585);
+    # 30 untimed steps (~20 ms) reach the steady state a training run sees
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="vlm7b",
                     choices=["tiny", "vlm7b", "microbatch", "longhorizon", "edge"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
