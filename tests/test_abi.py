@@ -399,3 +399,18 @@ def test_launch_limits_are_unsupported():
     # LM head: 8,388,608 tiles of 256 x 256
     assert lib.dart_lmhead_tok_stats(P, big, 8, 8, P, 8, 8, P, P, P, P, P, (1 << 64) - 1,
                                      None) == U
+
+
+def test_autograd_lmhead_plan():
+    """The LM-head autograd backward: the default plan with bf16 gradients, or
+    the caller's block and flags with bf16 gradients added; a block needs both
+    sizes."""
+    from paper_2509_23866_amd.autograd import lmhead_grad_plan
+
+    bf = dart.DART_LMHEAD_BF16_GRADS
+    assert lmhead_grad_plan(4096, 152064) == (4096, 65536, bf)
+    assert lmhead_grad_plan(300, 5000, 256, 1000, dart.DART_LMHEAD_SKIP_ZERO_ROWS) == \
+        (256, 1000, bf | dart.DART_LMHEAD_SKIP_ZERO_ROWS)
+    assert lmhead_grad_plan(300, 5000, 256, 1000) == (256, 1000, bf)
+    with pytest.raises(ValueError):
+        lmhead_grad_plan(300, 5000, 256, None)
