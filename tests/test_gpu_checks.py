@@ -159,3 +159,29 @@ def test_valid_inputs_unchanged(monkeypatch):
     for a, b in zip(*outs):
         assert torch.equal(a, b)
     assert int(outs[0][5].item()) == dart.dart_kept_steps(S, 0.6)
+
+
+def test_lmhead_backward_target(checks_on):
+    """The blocked LM-head backward with an out-of-range target id: INVALID_ARG
+    before anything is enqueued (the outputs keep their contents), with and
+    without row skipping."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 40, 64, 300
+    h = torch.randn(T, d, device="cuda").to(torch.bfloat16)
+    w = torch.randn(V, d, device="cuda").to(torch.bfloat16)
+    y = np.arange(T, dtype=np.int32)
+    f = lambda: torch.zeros(T, dtype=torch.float32, device="cuda")  # noqa: E731
+    lse, logp, coef = f(), f(), f() + 1e-2
+    y[7] = -1
+    for flags in (0, dart.DART_LMHEAD_SKIP_ZERO_ROWS):
+        dh = torch.full((T, d), 5.0, dtype=torch.float32, device="cuda")
+        dw = torch.full((V, d), 6.0, dtype=torch.float32, device="cuda")
+        with pytest.raises(dart.DartError) as e:
+            dart.dart_lmhead_backward_ex(h, w, _cuda(y), lse, logp, coef, chunk_rows=16,
+                                         chunk_cols=128, flags=flags, dhidden=dh, dweight=dw)
+        _invalid(e)
+        torch.cuda.synchronize()
+        assert bool(torch.all(dh == 5.0)) and bool(torch.all(dw == 6.0))
