@@ -20,8 +20,9 @@
 //                         and lse exactly as tok_stats_kernel defines them.
 //   lmhead_dlogits_kernel the same tile, its epilogue writing
 //                         dz = g (onehot - softmax) in bf16.
-// dart_lmhead_backward adds dh = dz W and dW = dz^T h per chunk of rows with
-// the ROCm BLAS library.
+// The backward forms dz block by block (rows x vocabulary entries, the blocked
+// entry point optionally over the rows with a non-zero coefficient only) and
+// adds dh = dz W and dW = dz^T h per block with the ROCm BLAS library.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <rocblas/rocblas.h>
@@ -416,8 +417,8 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
     }
 }
 
-// dlogits = g_t (onehot(y_t) - exp(z - lse_t)) for rows [0, M) of the chunk
-// (h and out already offset to the chunk's first row) and the V vocabulary
+// dlogits = g_t (onehot(y_t) - exp(z - lse_t)) for rows [0, M) of the block
+// (h and out already offset to the block's first row) and the V vocabulary
 // entries vbase .. vbase + V - 1 (w already offset to entry vbase), written in
 // bf16 (nearest even) to out [M, ld_out]: the gradient pass of the logits
 // path with the logits formed on the fly. The target element is
