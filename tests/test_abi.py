@@ -414,3 +414,17 @@ def test_autograd_lmhead_plan():
     assert lmhead_grad_plan(300, 5000, 256, 1000) == (256, 1000, bf)
     with pytest.raises(ValueError):
         lmhead_grad_plan(300, 5000, 256, None)
+
+
+def test_hip_builds_disable_packed_fp32():
+    """Every HIP compile of the package and of the generator's device twin
+    targets gfx950 with the packed-FP32 VALU forms disabled (the kernels are
+    plain scalar fp32 code)."""
+    from paper_2509_23866_amd import _build
+    import synth.native as sn
+
+    want = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+    for flags in (_build.HIPCC_FLAGS, sn.HIP_FLAGS):
+        flags = list(flags)
+        assert "--offload-arch=gfx950" in flags
+        assert any(flags[i:i + 4] == want for i in range(len(flags) - 3)), flags
