@@ -449,13 +449,16 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, rows, cols, flags):
     logp, _, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
     gdt = torch.bfloat16 if flags & _BF else torch.float32
     dh = torch.full((T, d + 4), 3.0, dtype=gdt, device="cuda")
-    dw = torch.full((V, d), 12345.0, dtype=gdt, device="cuda")  # overwritten
+    dwp = torch.full((V, d + 8), 7.0, dtype=gdt, device="cuda")  # rows padded by 8
+    dw = dwp[:, :d]
+    dw.fill_(12345.0)  # overwritten
     nb = dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, flags)
     ws = torch.full((nb,), 0x5A, dtype=torch.uint8, device="cuda")
     dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=rows, chunk_cols=cols,
                                  flags=flags, dhidden=dh[:, :d], dweight=dw, workspace=ws)
     torch.cuda.synchronize()
     assert torch.all(dh[:, d:] == 3.0), "dhidden padding was written"
+    assert torch.all(dwp[:, d:] == 7.0), "dweight padding was written"
     if flags & _SKIP:
         assert torch.all(dh[:, :d][torch.from_numpy(g == 0.0).cuda()] == 0.0)
     dzo = _own_dz(hd, wd, yd, lse, logp, _cuda(g))
