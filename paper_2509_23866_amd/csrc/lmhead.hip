@@ -53,7 +53,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // into LDS (vmcnt); lgkmcnt(0) retires its LDS reads; the empty asm
 // statements keep the compiler from moving memory accesses across it. Unlike
 // __syncthreads it carries no fence, which would wait for every load in flight.
-__device__ __forceinline__ void lds_ring_barrier() {
+[[maybe_unused]] __device__ __forceinline__ void lds_ring_barrier() {
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -179,7 +179,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
     // row. Each lane's source offsets within the tile are fixed for the whole
     // K loop (rows past M or N clamped to the last row), so a full slice's
     // load is a uniform base plus a per-lane 32-bit offset.
-    constexpr int CH = C::CH, BK = C::BK, PER = C::IA + C::IB;
+    constexpr int CH = C::CH, BK = C::BK;
     const int lrow = lane / CH, lslot = lane % CH;
     const char* a_tile = reinterpret_cast<const char*>(A + m0 * lda);
     const char* b_tile = reinterpret_cast<const char*>(B + n0 * ldb);
@@ -306,6 +306,9 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
         if (kt + 1 < nk) slice(std::integral_constant<int, 1>{}, kt + 1);
     }
     __syncthreads();
+#else
+    (void)A, (void)M, (void)lda, (void)B, (void)N, (void)ldb, (void)K, (void)m0, (void)n0;
+    (void)sm, (void)acc;
 #endif
 }
 
