@@ -175,3 +175,49 @@ def test_tok_stats_rows_beyond_one_launch():
     for got, ref, name in ((logp, rlogp, "logp"), (ent, rH, "entropy"), (lse, rlse, "lse")):
         err = np.abs(got[idx].double().cpu().numpy() - ref)
         assert err.max() <= 2e-4, (name, float(err.max()), rows[int(err.argmax())])
+
+
+@pytest.mark.timeout(600)
+def test_whole_path_beyond_the_grid_limits():
+    """T = 2^24 + 1000 rows of V = 8 bf16 logits in 1000 steps: the statistics
+    run in five launches of at most 2^22 rows, and the gradient pass has more
+    4 KB chunks (one per row) than its 2^24 workgroups, so it takes its
+    grid-stride loop. The whole path (policy_update) against the oracle: every
+    token's logp and entropy, the mask, the loss, and the gradient on rows
+    sampled across both limits."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, V, S = (1 << 24) + 1000, 8, 1000
+    rng = np.random.default_rng(24)
+    z32 = (rng.standard_normal((T, V), dtype=np.float32) * 3.0)
+    z = synth.f32_to_bf16_bits(z32)
+    del z32
+    target = rng.integers(0, V, T).astype(np.int32)
+    cuts = np.sort(rng.choice(np.arange(1, T), S - 1, replace=False))
+    off = np.r_[0, cuts, T].astype(np.int32)
+    adv = rng.standard_normal(T).astype(np.float32)
+    logp0, _, _ = oracle.token_stats(z, target)
+    lp_old = (logp0 + 0.05 * rng.standard_normal(T)).astype(np.float32)
+    lp_roll = (lp_old + 0.1 * rng.standard_normal(T)).astype(np.float32)
+    rho, eps_low, eps_high, C = 0.8, 0.2, 0.28, 2.0
+    ref = oracle.forward_backward(z, target, lp_old, lp_roll, adv, off, rho, eps_low, eps_high, C)
+    cuda = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    logits = cuda(z.view(np.int16)).view(torch.bfloat16)
+    out = dart.policy_update(logits, cuda(target), cuda(lp_old), cuda(lp_roll), cuda(adv),
+                             cuda(off), rho, eps_low, eps_high, C)
+    torch.cuda.synchronize()
+    assert np.abs(out["logp"].cpu().numpy() - ref["logp"]).max() <= 2e-4
+    assert np.abs(out["entropy"].cpu().numpy() - ref["H"]).max() <= 2e-4
+    assert np.array_equal(out["step_mask"].cpu().numpy(), ref["mask"])
+    L = float(out["loss"].cpu().item())
+    assert abs(L - ref["L"]) <= 1e-4 * abs(ref["L"])
+    rows = np.unique(np.r_[0, (1 << 22) - 1, 1 << 22, (1 << 24) - 1, 1 << 24, T - 1,
+                           rng.integers(0, T, 300)])
+    rows = rows[~ref["boundary"][rows]]
+    got = out["dlogits"][torch.from_numpy(rows).cuda()].view(torch.int16).cpu().numpy()
+    got = synth.bf16_bits_to_f32(got.view(np.uint16)).astype(np.float64)
+    want_bits = oracle.f64_to_bf16_bits(ref["dz"][rows])
+    want = synth.bf16_bits_to_f32(want_bits).astype(np.float64)
+    assert np.all(np.abs(got - want) <= oracle.bf16_ulp(want_bits))
