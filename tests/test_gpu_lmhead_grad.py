@@ -16,10 +16,11 @@ dhidden and dweight, each element two ways, with B = |dz| |W| (resp.
   bf16's 8-bit significand, and an ulp is at most 2 U relative), and the
   library sums in fp32: tolerance 3 U B + A B, with A = 2^-13 for the fp32
   sums;
-- against the exact product of the GPU's own bf16 dlogits (the same kernel's
-  output, bit for bit the values the backward multiplies): only the fp32 sums
-  differ, tolerance A B. This is the tight check: a block left out or added
-  twice, or a wrong offset, moves an element by far more than A B.
+- a consistency property of the GEMM stage, not a parity reference: against
+  the exact product of the GPU's own bf16 dlogits (the same kernel's output,
+  bit for bit the values the backward multiplies) only the fp32 sums differ,
+  tolerance A B; a block left out or added twice, or a wrong offset, moves an
+  element by far more than A B. Parity rests on the oracle comparison above.
 A bf16 gradient adds its own rounding, U |value| (round to nearest even)."""
 
 import math
