@@ -71,6 +71,39 @@ def test_small_shapes(case):
     _full_check(wl)
 
 
+def _random_case(seed):
+    """A seeded random configuration: 1-25 steps of 1-120 tokens, V from 1 to
+    40000 (often just off a multiple of 8 or of the 2048-element chunk), fp32 or
+    bf16, padded or misaligned rows, any rho, the wide or narrow ratio model,
+    C finite or infinite."""
+    rng = np.random.default_rng(1000 + seed)
+    lens = rng.integers(1, 121, int(rng.integers(1, 26)))
+    V = int(rng.choice([rng.integers(1, 64), rng.integers(64, 40001),
+                        8 * rng.integers(1, 5000) + rng.integers(-1, 2),
+                        2048 * rng.integers(1, 20) + rng.integers(-1, 2)]))
+    V = max(V, 1)
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    kw = dict(rho=float(rng.choice([0.0, 0.25, 0.5, 0.8, 1.0, rng.random()])),
+              C=float(rng.choice([1.0, 2.0, 5.0, float("inf")])),
+              ratio_spread=bool(rng.random() < 0.5), mix_kinds=bool(rng.random() < 0.5))
+    layout = dict(ld=None, misalign=0)
+    r = rng.random()
+    if r < 0.25:
+        layout["ld"] = V + int(rng.integers(1, 17))
+    elif r < 0.4:
+        layout["misalign"] = 1
+    return lens, V, dtype, kw, layout
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_shapes(seed):
+    """24 seeded random configurations through the whole path against the oracle."""
+    lens, V, dtype, kw, layout = _random_case(seed)
+    wl = synth.custom_workload(lens=lens, V=V, dtype=dtype, seed=500 + seed, **kw)
+    H.log(f"random case {seed}: S={lens.size} T={int(lens.sum())} V={V} {dtype} {kw} {layout}")
+    _full_check(wl, **layout)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("V,ld,misalign", [(4099, 4107, 0), (5000, 5003, 0), (777, 777, 1),
                                            (8200, 8203, 3)])
