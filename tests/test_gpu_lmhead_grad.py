@@ -506,3 +506,40 @@ def test_lmhead_backward_blockings_agree():
             a = xb.float().cpu().numpy().astype(np.float64)
             b = xf.cpu().numpy().astype(np.float64)
             assert np.all(np.abs(a - b) <= U * np.abs(b) + A * bound + 1e-37)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_lmhead_random_configurations(seed):
+    """16 seeded random LM-head problems: T in 1..300, d a multiple of 8 up
+    to 512, V in 1..5000, padded rows, random blocks of rows x vocabulary
+    entries and random flags; statistics, rows skipped exactly 0, and both
+    gradients against the oracle and the GPU's own dlogits."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    rng = np.random.default_rng(7000 + seed)
+    T, d, V = int(rng.integers(1, 301)), 8 * int(rng.integers(1, 65)), int(rng.integers(1, 5001))
+    pad = 8 * int(rng.integers(0, 3))
+    rows, cols = int(rng.integers(1, T + 65)), int(rng.integers(1, V + 300))
+    flags = int(rng.choice([0, _SKIP, _BF, _SKIP | _BF]))
+    h, w, y, g = _problem(T, d, V)
+    rlogp, rH, rlse = oracle.lmhead_token_stats(h, w, y)
+    dz64, dh64, dw64 = oracle.lmhead_grads(h, w, y, rlse, rlogp, g)
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    hd, wd, yd, gd = _dev_bf16(h, pad), _dev_bf16(w, pad), _cuda(y), _cuda(g)
+    logp, ent, lse = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    dh, dw = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=rows,
+                                          chunk_cols=cols, flags=flags)
+    dzo = _own_dz(hd, wd, yd, lse, logp, gd)
+    torch.cuda.synchronize()
+    assert np.abs(logp.cpu().numpy() - rlogp).max() <= 2e-4
+    assert np.abs(ent.cpu().numpy() - rH).max() <= 2e-4
+    if flags & _SKIP:
+        assert np.all(_as_f64(dh)[g == 0.0] == 0.0)
+    adz = np.abs(dz64)
+    bf = bool(flags & _BF)
+    rh = _check_grad(dh, dh64, dzo @ w64, adz @ np.abs(w64), "dhidden", bf16=bf)
+    rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight", bf16=bf)
+    H.log(f"lmhead random {seed}: T={T} d={d} V={V} pad={pad} block={rows}x{cols} "
+          f"flags={flags}: dh {rh:.2e} dW {rw:.2e}")
