@@ -146,7 +146,7 @@ def cpu_baseline(wl, threads, min_seconds=1.5, max_passes=20):
             "sample": f"{what}, float64 C oracle, OpenMP over rows; median of {len(times)} passes"}
 
 
-def graph_variant(step, stream, dev, n):
+def graph_variant(step, stream, dev, n, warm=30):
     """The same step captured once into a HIP graph and replayed n times back to
     back (one pair of events around the replays): the launch gaps a trainer
     that replays a captured step would see. Never the headline."""
@@ -161,7 +161,8 @@ def graph_variant(step, stream, dev, n):
     with torch.cuda.graph(g, stream=side):
         step(s=side)
     torch.cuda.synchronize(dev)
-    g.replay()
+    for _ in range(max(1, warm)):  # untimed replays: the same warm-up as the eager step
+        g.replay()
     torch.cuda.synchronize(dev)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -599,7 +600,7 @@ def main():
                                   "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
 
     if not wl.inplace and not args.no_variants:
-        variants["hip_graph"] = graph_variant(step, stream, dev, args.steps)
+        variants["hip_graph"] = graph_variant(step, stream, dev, args.steps, args.warmup)
         variants["objective_variants"] = objective_variant(
             wl, dev, stream, logits, target, off, adv, lp_old, lp_roll, dlogits, step,
             min(args.steps, 20))
