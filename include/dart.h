@@ -315,8 +315,20 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
                                     float* lse, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream);
 
-/* Bytes of workspace dart_lmhead_tok_stats needs (0 for T or V outside
- * [1, INT32_MAX]). Host only. */
+/* dart_lmhead_tok_stats for softmax(inv_temp * h W^T), as dart_tok_stats_ex
+ * is for materialised logits: each fp32 tile of z is multiplied by inv_temp
+ * before it is reduced, so lse, logp and entropy are those of inv_temp * z
+ * (inv_temp = 1 gives the bits of dart_lmhead_tok_stats). inv_temp: finite
+ * and > 0, else INVALID_ARG. Other arguments and errors as
+ * dart_lmhead_tok_stats. */
+dart_status_t dart_lmhead_tok_stats_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                       const void* weight, int64_t V, int64_t ld_w,
+                                       const int32_t* target, float inv_temp, float* logp,
+                                       float* entropy, float* lse, void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace dart_lmhead_tok_stats (and _ex) needs (0 for T or V
+ * outside [1, INT32_MAX]). Host only. */
 size_t dart_lmhead_stats_workspace_bytes(int64_t T, int64_t V);
 
 /* The gradient pass of the fused head, part one: dlogits of the logits
@@ -382,8 +394,14 @@ size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V);
 enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
 
 /* dart_lmhead_backward in blocks of chunk_rows rows x chunk_cols vocabulary
- * entries, with flags. dart_lmhead_backward(..., chunk_rows, ...) is this call
- * with chunk_cols = V and flags = 0.
+ * entries, with flags, at an inverse temperature. dart_lmhead_backward(...,
+ * chunk_rows, ...) is this call with inv_temp = 1, chunk_cols = V and
+ * flags = 0.
+ *
+ * inv_temp: the value given to dart_lmhead_tok_stats_ex for lse and logp
+ * (finite and > 0, else INVALID_ARG); the dlogits are
+ *   inv_temp * tok_coef[t] * (onehot(target[t])[v] - exp(inv_temp z_tv - lse[t]))
+ * as dart_tis_grad_ex defines them for materialised logits.
  *
  * Each block forms its dlogits (bf16, in the workspace), adds its share to
  * its rows of dhidden (summed over the vocabulary blocks) and to its entries'
@@ -431,10 +449,11 @@ enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
 dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                       const void* weight, int64_t V, int64_t ld_w,
                                       const int32_t* target, const float* lse, const float* logp,
-                                      const float* tok_coef, void* dhidden, int64_t ld_dh,
-                                      void* dweight, int64_t ld_dw, int64_t chunk_rows,
-                                      int64_t chunk_cols, uint32_t flags, void* workspace,
-                                      size_t workspace_bytes, hipStream_t stream);
+                                      const float* tok_coef, float inv_temp, void* dhidden,
+                                      int64_t ld_dh, void* dweight, int64_t ld_dw,
+                                      int64_t chunk_rows, int64_t chunk_cols, uint32_t flags,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
 
 /* Bytes of workspace dart_lmhead_backward_ex needs (host only; 0 for bad
  * arguments or flags). The parts, each starting 256-byte aligned: the dlogits

@@ -304,18 +304,21 @@ def lmhead_logits(h_bits, w_bits):
     return np.ascontiguousarray(bf16_bits_to_f64(h_bits) @ bf16_bits_to_f64(w_bits).T)
 
 
-def lmhead_token_stats(h_bits, w_bits, target, nthreads=None):
-    """(logp, H, lse) of softmax(h W^T) per row, in float64 (Sec. 4.3, Eq. 1 on
-    the logits of the LM head)."""
-    return token_stats(lmhead_logits(h_bits, w_bits), target, nthreads=nthreads)
+def lmhead_token_stats(h_bits, w_bits, target, nthreads=None, inv_temp=1.0):
+    """(logp, H, lse) of softmax(inv_temp h W^T) per row, in float64 (Sec. 4.3,
+    Eq. 1 on the logits of the LM head; inv_temp is an inverse sampling
+    temperature, 1 in the paper, App. A.4)."""
+    return token_stats(lmhead_logits(h_bits, w_bits), target, nthreads=nthreads,
+                       inv_temp=inv_temp)
 
 
-def lmhead_grads(h_bits, w_bits, target, lse, logp, g, nthreads=None):
+def lmhead_grads(h_bits, w_bits, target, lse, logp, g, nthreads=None, inv_temp=1.0):
     """Gradients of the loss through the LM head, given the per-token
-    coefficient g = dL/dlogp: dz = g (onehot - p) [T, V] (the logits gradient),
-    dh = dz W [T, d] and dW = dz^T h [V, d], all in float64."""
+    coefficient g = dL/dlogp: dz = inv_temp g (onehot - p) [T, V] (the gradient
+    of the logits h W^T, p = softmax(inv_temp h W^T)), dh = dz W [T, d] and
+    dW = dz^T h [V, d], all in float64."""
     z = lmhead_logits(h_bits, w_bits)
-    dz = dlogits(z, target, lse, logp, g, nthreads=nthreads)
+    dz = dlogits(z, target, lse, logp, g, nthreads=nthreads, inv_temp=inv_temp)
     h = bf16_bits_to_f64(h_bits)
     w = bf16_bits_to_f64(w_bits)
     return dz, dz @ w, dz.T @ h

@@ -38,7 +38,8 @@ DART_LMHEAD_BF16_GRADS = 4
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
-            "dart_lmhead_tok_stats", "dart_lmhead_stats_workspace_bytes", "dart_lmhead_dlogits",
+            "dart_lmhead_tok_stats", "dart_lmhead_tok_stats_ex", "dart_lmhead_stats_workspace_bytes",
+            "dart_lmhead_dlogits",
             "dart_lmhead_backward", "dart_lmhead_backward_workspace_bytes",
             "dart_lmhead_backward_ex", "dart_lmhead_backward_ex_workspace_bytes", "dart_kept_steps",
             "dart_status_string")
@@ -106,6 +107,10 @@ def load_library():
         lib.dart_lmhead_tok_stats.restype = ctypes.c_int
         lib.dart_lmhead_tok_stats.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
                                               _P, ctypes.c_size_t, _P]
+        lib.dart_lmhead_tok_stats_ex.restype = ctypes.c_int
+        lib.dart_lmhead_tok_stats_ex.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P,
+                                                 ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t,
+                                                 _P]
         lib.dart_lmhead_stats_workspace_bytes.restype = ctypes.c_size_t
         lib.dart_lmhead_stats_workspace_bytes.argtypes = [_I64, _I64]
         lib.dart_lmhead_dlogits.restype = ctypes.c_int
@@ -118,8 +123,8 @@ def load_library():
         lib.dart_lmhead_backward_workspace_bytes.argtypes = [_I64, _I64]
         lib.dart_lmhead_backward_ex.restype = ctypes.c_int
         lib.dart_lmhead_backward_ex.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P,
-                                                _P, _P, _I64, _P, _I64, _I64, _I64,
-                                                ctypes.c_uint32, _P, ctypes.c_size_t, _P]
+                                                _P, ctypes.c_float, _P, _I64, _P, _I64, _I64,
+                                                _I64, ctypes.c_uint32, _P, ctypes.c_size_t, _P]
         lib.dart_lmhead_backward_ex_workspace_bytes.restype = ctypes.c_size_t
         lib.dart_lmhead_backward_ex_workspace_bytes.argtypes = [_I64, _I64, _I64, _I64, _I64,
                                                                 ctypes.c_uint32]
@@ -480,6 +485,17 @@ def dart_lmhead_tok_stats(hidden, weight, target, logp=None, entropy=None, lse=N
     materialising the logits: hidden [T, d] and weight [V, d] bfloat16 (d a
     multiple of 8). ``workspace``: "auto" (allocated here) or a uint8 device
     tensor of dart_lmhead_stats_workspace_bytes(T, V) bytes."""
+    return _lmhead_tok_stats(None, hidden, weight, target, logp, entropy, lse, workspace, stream)
+
+
+def dart_lmhead_tok_stats_ex(hidden, weight, target, inv_temp, logp=None, entropy=None,
+                             lse=None, workspace="auto", stream=None):
+    """dart_lmhead_tok_stats of softmax(inv_temp * hidden @ weight^T)."""
+    return _lmhead_tok_stats(float(inv_temp), hidden, weight, target, logp, entropy, lse,
+                             workspace, stream)
+
+
+def _lmhead_tok_stats(inv_temp, hidden, weight, target, logp, entropy, lse, workspace, stream):
     torch = _torch()
     _matrix_bf16("hidden", hidden)
     dev = hidden.device
@@ -504,12 +520,17 @@ def dart_lmhead_tok_stats(hidden, weight, target, logp=None, entropy=None, lse=N
     if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8
             or workspace.device != dev or not workspace.is_contiguous()):
         raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
-    rc = load_library().dart_lmhead_tok_stats(
-        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
-        target.data_ptr(), logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(),
-        workspace.data_ptr(), workspace.numel(), _stream_handle(stream, dev))
+    args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+            target.data_ptr()]
+    name = "dart_lmhead_tok_stats"
+    if inv_temp is not None:
+        args.append(inv_temp)
+        name += "_ex"
+    args += [logp.data_ptr(), entropy.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
+             workspace.numel(), _stream_handle(stream, dev)]
+    rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
-        raise DartError("dart_lmhead_tok_stats", rc)
+        raise DartError(name, rc)
     return logp, entropy, lse
 
 
@@ -557,7 +578,7 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
 
 
 def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, chunk_rows,
-                     chunk_cols, dhidden, dweight, workspace, stream):
+                     chunk_cols, dhidden, dweight, workspace, stream, inv_temp=1.0):
     torch = _torch()
     dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
     f = 0 if flags is None else int(flags)
@@ -584,9 +605,11 @@ def _lmhead_backward(name, flags, hidden, weight, target, lse, logp, tok_coef, c
             or workspace.device != dev or not workspace.is_contiguous()):
         raise ValueError("workspace must be a contiguous uint8 tensor on the device of the inputs")
     args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
-            target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-            dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0),
-            chunk_rows]
+            target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr()]
+    if flags is not None:
+        args.append(float(inv_temp))
+    args += [dhidden.data_ptr(), dhidden.stride(0), dweight.data_ptr(), dweight.stride(0),
+             chunk_rows]
     if flags is not None:
         args += [chunk_cols, f]
     args += [workspace.data_ptr(), workspace.numel(), _stream_handle(stream, dev)]
@@ -609,9 +632,11 @@ def dart_lmhead_backward(hidden, weight, target, lse, logp, tok_coef, chunk_rows
 
 def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk_rows=None,
                             chunk_cols=None, flags=0, dhidden=None, dweight=None,
-                            workspace="auto", stream=None):
+                            workspace="auto", stream=None, inv_temp=1.0):
     """dart_lmhead_backward in blocks of chunk_rows rows x chunk_cols vocabulary
-    entries (both None: lmhead_backward_plan's block), with flags (bitwise or):
+    entries (both None: lmhead_backward_plan's block), at inverse temperature
+    inv_temp (lse and logp from dart_lmhead_tok_stats_ex at the same value),
+    with flags (bitwise or):
     DART_LMHEAD_BF16_GRADS: dhidden and dweight in bfloat16;
     DART_LMHEAD_SKIP_ZERO_ROWS: the GEMMs over the rows with tok_coef != 0 only
     (the call synchronises the stream once).
@@ -624,7 +649,7 @@ def dart_lmhead_backward_ex(hidden, weight, target, lse, logp, tok_coef, chunk_r
         raise ValueError("give both chunk_rows and chunk_cols, or neither")
     return _lmhead_backward("dart_lmhead_backward_ex", int(flags), hidden, weight, target, lse,
                             logp, tok_coef, chunk_rows, chunk_cols, dhidden, dweight, workspace,
-                            stream)
+                            stream, inv_temp)
 
 
 def lmhead_backward_plan(T: int, V: int, budget_bytes: int = 512 << 20):

@@ -6,7 +6,9 @@
 // entropy, the target's log-prob of Eq. 1) for logits z = h W^T, where h [T, d]
 // are the final hidden states of the T action tokens and W [V, d] the LM-head
 // weight of the policy (the 7B VLM of Sec. 5.1); the gradient is the chain
-// rule of Eq. 2's loss through them.
+// rule of Eq. 2's loss through them. Both kernels scale the fp32 tile by an
+// inverse sampling temperature before the epilogue (1 in the paper, App. A.4;
+// multiplying by 1 changes no bit).
 //
 //   lmhead_stats_kernel   one 256 x 256 tile of z per workgroup on MFMA
 //                         (v_mfma_f32_32x32x16_bf16, fp32 accumulation), K = d
@@ -330,7 +332,7 @@ template <class C>
 __global__ void __launch_bounds__(C::THREADS)
 lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
                     const uint16_t* __restrict__ w, int64_t V, int64_t ldw, int64_t d,
-                    const int32_t* __restrict__ target, int64_t nmt, int64_t nvt,
+                    const int32_t* __restrict__ target, float scale, int64_t nmt, int64_t nvt,
                     float4* __restrict__ part, float* __restrict__ z_y) {
     __shared__ typename C::Smem sm;
     int64_t mt, vt;
@@ -352,7 +354,8 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
-                    if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
+                    if (row >= 0 && row < C::EPI)
+                        sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v] * scale;
                 }
         __syncthreads();
         // P threads per row; thread p takes the 16-byte pieces p, p + P, ...
@@ -420,12 +423,13 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
     }
 }
 
-// dlogits = g_t (onehot(y_t) - exp(z - lse_t)) for rows [0, M) of the block
+// dlogits = s g_t (onehot(y_t) - exp(s z - lse_t)) (s = scale, the inverse
+// temperature; lse_t that of s z) for rows [0, M) of the block
 // (h and out already offset to the block's first row) and the V vocabulary
 // entries vbase .. vbase + V - 1 (w already offset to entry vbase), written in
 // bf16 (nearest even) to out [M, ld_out]: the gradient pass of the logits
 // path with the logits formed on the fly. The target element is
-// g_t * -expm1(logp_t), accurate when p_y -> 1. The fp32 tile is staged
+// s g_t * -expm1(logp_t), accurate when p_y -> 1. The fp32 tile is staged
 // through LDS so that each row leaves as 16-byte vectors.
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
@@ -433,8 +437,8 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
                       const uint16_t* __restrict__ w, int64_t V, int64_t ldw, int64_t d,
                       const int32_t* __restrict__ target, const float* __restrict__ lse,
                       const float* __restrict__ logp, const float* __restrict__ coef,
-                      uint16_t* __restrict__ out, int64_t ld_out, int64_t vbase, int64_t nmt,
-                      int64_t nvt) {
+                      float scale, uint16_t* __restrict__ out, int64_t ld_out, int64_t vbase,
+                      int64_t nmt, int64_t nvt) {
     __shared__ typename C::Smem sm;
     int64_t mt, vt;
     tile_of_block(nmt, nvt, mt, vt);
@@ -455,15 +459,17 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
-                    if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
+                    if (row >= 0 && row < C::EPI)
+                        sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v] * scale;
                 }
         // per-row constants: -g, -lse log2(e), the target's gradient
-        // g (-expm1(logp)) (accurate when p_y -> 1), the target's column here
+        // g (-expm1(logp)) (accurate when p_y -> 1), the target's column here;
+        // g carries the inverse temperature (the chain rule through scale z)
         if (tid < C::EPI) {
             const int64_t t = m0 + e0 + tid;
             float4 rp = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
             if (t < M) {
-                const float g = coef[t];
+                const float g = coef[t] * scale;
                 const int64_t yrel = (int64_t)target[t] - vbase - n0;
                 rp = make_float4(-g, -lse[t] * 1.4426950408889634f, g * -expm1f(logp[t]),
                                  __int_as_float(yrel >= 0 && yrel < C::BN ? (int)yrel : -1));
@@ -661,14 +667,14 @@ bool bad_lmhead_args(const void* hidden, int64_t T, int64_t d, int64_t ld_h, con
 dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, int64_t ld_h,
                              const uint16_t* weight, int64_t V, int64_t ld_w,
                              const int32_t* target, const float* lse, const float* logp,
-                             const float* coef, uint16_t* out, int64_t ld_out, int64_t vbase,
-                             hipStream_t stream) {
+                             const float* coef, float scale, uint16_t* out, int64_t ld_out,
+                             int64_t vbase, hipStream_t stream) {
     const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
     if (!grid_fits(nmt * nvt, LmCfg::THREADS) || ld_h > kMaxLd || ld_w > kMaxLd)
         return DART_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
-                       target, lse, logp, coef, out, ld_out, vbase, nmt, nvt);
+                       target, lse, logp, coef, scale, out, ld_out, vbase, nmt, nvt);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
@@ -713,12 +719,13 @@ size_t dart_lmhead_stats_workspace_bytes(int64_t T, int64_t V) {
     return (size_t)T * (size_t)vocab_tiles(V) * sizeof(float4) + (size_t)T * sizeof(float);
 }
 
-dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
-                                    const void* weight, int64_t V, int64_t ld_w,
-                                    const int32_t* target, float* logp, float* entropy,
-                                    float* lse, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream) {
+dart_status_t dart_lmhead_tok_stats_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                       const void* weight, int64_t V, int64_t ld_w,
+                                       const int32_t* target, float inv_temp, float* logp,
+                                       float* entropy, float* lse, void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
     if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!(inv_temp > 0.f) || isinf(inv_temp)) return DART_ERR_INVALID_ARG;
     if (!target || !logp || !entropy || !lse || !workspace ||
         reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
@@ -737,12 +744,21 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
     hipLaunchKernelGGL(lmhead_stats_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)), dim3(LmCfg::THREADS),
                        0, stream,
                        static_cast<const uint16_t*>(hidden), T, ld_h,
-                       static_cast<const uint16_t*>(weight), V, ld_w, d, target, nmt, nvt, part,
-                       z_y);
+                       static_cast<const uint16_t*>(weight), V, ld_w, d, target, inv_temp, nmt,
+                       nvt, part, z_y);
     hipLaunchKernelGGL(lmhead_merge_kernel, dim3((unsigned)((T + kMergeWaves - 1) / kMergeWaves)),
                        dim3(kMergeWaves * 64), 0, stream, part, z_y, T, nvt, V, target, logp,
                        entropy, lse);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
+}
+
+dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                    const void* weight, int64_t V, int64_t ld_w,
+                                    const int32_t* target, float* logp, float* entropy,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    return dart_lmhead_tok_stats_ex(hidden, T, d, ld_h, weight, V, ld_w, target, 1.f, logp,
+                                    entropy, lse, workspace, workspace_bytes, stream);
 }
 
 dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
@@ -760,7 +776,7 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
 
     return launch_dlogits(static_cast<const uint16_t*>(hidden), T, d, ld_h,
                           static_cast<const uint16_t*>(weight), V, ld_w, target, lse, logp,
-                          tok_coef, static_cast<uint16_t*>(dlogits), ld_out, 0, stream);
+                          tok_coef, 1.f, static_cast<uint16_t*>(dlogits), ld_out, 0, stream);
 }
 
 size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {
@@ -882,7 +898,8 @@ void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& ds
 dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
                             int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
                             const int32_t* target, const float* lse, const float* logp,
-                            const float* coef, const Grad& dh, const Grad& dw, int64_t R,
+                            const float* coef, float scale, const Grad& dh, const Grad& dw,
+                            int64_t R,
                             int64_t C, uint16_t* dz, float* acc_h, float* acc_w,
                             hipStream_t stream) {
     if (R > T) R = T;
@@ -899,7 +916,7 @@ dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, i
             const uint16_t* wc = w + c0 * ld_w;
             const dart_status_t st =
                 launch_dlogits(hr, rows, d, ld_h, wc, cols, ld_w, target + r0, lse + r0,
-                               logp + r0, coef + r0, dz, ld_dz, c0, stream);
+                               logp + r0, coef + r0, scale, dz, ld_dz, c0, stream);
             if (st != DART_OK) return st;
             if (!gemm_dh(blas, dz, ld_dz, rows, cols, wc, ld_w, d, c0 > 0,
                          Grad{sum_h.row(r0), sum_h.ld, sum_h.bf16}) ||
@@ -936,11 +953,13 @@ size_t dart_lmhead_backward_ex_workspace_bytes(int64_t T, int64_t d, int64_t V,
 dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                       const void* weight, int64_t V, int64_t ld_w,
                                       const int32_t* target, const float* lse, const float* logp,
-                                      const float* tok_coef, void* dhidden, int64_t ld_dh,
-                                      void* dweight, int64_t ld_dw, int64_t chunk_rows,
-                                      int64_t chunk_cols, uint32_t flags, void* workspace,
-                                      size_t workspace_bytes, hipStream_t stream) {
+                                      const float* tok_coef, float inv_temp, void* dhidden,
+                                      int64_t ld_dh, void* dweight, int64_t ld_dw,
+                                      int64_t chunk_rows, int64_t chunk_cols, uint32_t flags,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
     if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!(inv_temp > 0.f) || isinf(inv_temp)) return DART_ERR_INVALID_ARG;
     if (!target || !lse || !logp || !tok_coef || !dhidden || !dweight || !workspace)
         return DART_ERR_INVALID_ARG;
     if (ld_dh < d || ld_dw < d || chunk_rows < 1 || chunk_cols < 1 ||
@@ -975,8 +994,8 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     float* acc_h = P.acc_h ? reinterpret_cast<float*>(ws + P.acch) : nullptr;
     const Grad dh{dhidden, ld_dh, P.bf16}, dw{dweight, ld_dw, P.bf16};
     if (!P.skip)
-        return backward_core(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef, dh,
-                             dw, P.rows, P.cols, dz, acc_h, acc_w, stream);
+        return backward_core(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef,
+                             inv_temp, dh, dw, P.rows, P.cols, dz, acc_h, acc_w, stream);
 
     // rows with a zero coefficient have dz = 0: they add nothing to dW and
     // their rows of dh are 0, so the GEMMs run over the other rows only
@@ -1011,7 +1030,7 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
         return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
     }
     const dart_status_t st =
-        backward_core(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c,
+        backward_core(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c, inv_temp,
                       Grad{dh_c, d, false}, dw, P.rows, P.cols, dz, nullptr, acc_w, stream);
     if (st != DART_OK) return st;
     const unsigned nb = (unsigned)(n < kRowBlocks ? n : kRowBlocks);
@@ -1031,8 +1050,8 @@ dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int
                                    float* dweight, int64_t ld_dw, int64_t chunk_rows,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
     return dart_lmhead_backward_ex(hidden, T, d, ld_h, weight, V, ld_w, target, lse, logp,
-                                   tok_coef, dhidden, ld_dh, dweight, ld_dw, chunk_rows, V, 0u,
-                                   workspace, workspace_bytes, stream);
+                                   tok_coef, 1.f, dhidden, ld_dh, dweight, ld_dw, chunk_rows, V,
+                                   0u, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -218,6 +218,20 @@ def _lm_args(**kw):
 def test_lmhead_stats_rejects(kw):
     lib = dart.load_library()
     assert lib.dart_lmhead_tok_stats(*_lm_args(**kw)) == dart.DART_ERR_INVALID_ARG
+    a = _lm_args(**kw)
+    assert lib.dart_lmhead_tok_stats_ex(*a[:8], 1.0, *a[8:]) == dart.DART_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("inv_temp", [0.0, -1.0, float("inf"), float("nan"), -0.0])
+def test_lmhead_inverse_temperature_rejects(inv_temp):
+    """An inverse temperature that is not finite and positive, with every other
+    argument valid, is INVALID_ARG for the statistics and the backward."""
+    lib = dart.load_library()
+    a = _lm_args()
+    assert lib.dart_lmhead_tok_stats_ex(*a[:8], inv_temp, *a[8:]) == dart.DART_ERR_INVALID_ARG
+    assert (lib.dart_lmhead_backward_ex(*_lm_bwd_ex_args(inv_temp=inv_temp))
+            == dart.DART_ERR_INVALID_ARG)
 
 
 def test_lmhead_workspace_bytes():
@@ -286,9 +300,9 @@ def test_lmhead_leading_dimension_limit():
     assert lib.dart_lmhead_dlogits(*_lm_grad_args(ld_w=big)) == dart.DART_ERR_UNSUPPORTED
 
 
-def _lm_bwd_ex_args(flags=0, chunk_cols=300, **kw):
+def _lm_bwd_ex_args(flags=0, chunk_cols=300, inv_temp=1.0, **kw):
     a = _lm_bwd_args(**kw)[:-1]
-    return a[:16] + [chunk_cols, flags] + a[16:] + [None]
+    return a[:11] + [inv_temp] + a[11:16] + [chunk_cols, flags] + a[16:] + [None]
 
 
 @pytest.mark.skipif("_gpu_visible()")

@@ -88,12 +88,15 @@ def _as_f64(x):
 
 
 def _check_grad(got, ref, own, bound, name, bf16=False):
-    """got against the oracle's exact product ref (3 U B + A B) and against the
-    exact product own of the GPU's own bf16 dlogits (A B); a bf16 output adds
-    U |value| to both. Returns the largest error against ref in units of B."""
+    """got against the oracle's exact product ref (3 U B + A B) and, unless own
+    is None, against the exact product own of the GPU's own bf16 dlogits (A B);
+    a bf16 output adds U |value| to both. Returns the largest error against ref
+    in units of B."""
     got = _as_f64(got)
-    for what, target, tol in (("oracle", ref, (3 * U + A) * bound),
-                              ("own dlogits", own, A * bound)):
+    checks = [("oracle", ref, (3 * U + A) * bound)]
+    if own is not None:
+        checks.append(("own dlogits", own, A * bound))
+    for what, target, tol in checks:
         if bf16:
             tol = tol + U * np.abs(target)
         err = np.abs(got - target)
@@ -469,6 +472,64 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, rows, cols, flags):
     rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight", bf16=bf)
     H.log(f"lmhead backward_ex T={T} d={d} V={V} block={rows}x{cols} flags={flags}: "
           f"dh {rh:.2e} dW {rw:.2e}")
+
+
+@pytest.mark.parametrize("T,d,V,pad,rows,cols,flags,inv_temp", [
+    (129, 72, 127, 8, 129, 64, _BF, 0.7),
+    (300, 512, 16384, 0, 300, 4096, 0, 1.6),
+    (257, 3584, 2000, 0, 100, 2000, _BF, 1.3),
+    (1100, 136, 2000, 8, 300, 700, _SKIP | _BF, 0.5),
+])
+def test_lmhead_inverse_temperature(T, d, V, pad, rows, cols, flags, inv_temp):
+    """Statistics and gradients of softmax(inv_temp h W^T) (the _ex entry
+    points) against the oracle at the same inverse temperature: logp, H and lse
+    to the tolerances of the logits path, dhidden and dweight to 3 U B + A B
+    with the factor inv_temp inside dz."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    h, w, y, g = _problem(T, d, V)
+    ref = oracle.lmhead_token_stats(h, w, y, inv_temp=inv_temp)
+    _, dh64, dw64 = oracle.lmhead_grads(h, w, y, ref[2], ref[0], g, inv_temp=inv_temp)
+    dz64 = oracle.dlogits(oracle.lmhead_logits(h, w), y, ref[2], ref[0], g, inv_temp=inv_temp)
+    h64, w64 = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
+    hd, wd, yd = _dev_bf16(h, pad), _dev_bf16(w, pad), _cuda(y)
+    logp, ent, lse = dart.dart_lmhead_tok_stats_ex(hd, wd, yd, inv_temp)
+    got = [x.cpu().numpy().astype(np.float64) for x in (logp, ent, lse)]
+    err = [float(np.abs(a - b).max()) for a, b in zip(got, ref)]
+    assert err[0] <= H.LOGP_TOL and err[1] <= H.H_TOL and err[2] <= H.LOGP_TOL, err
+    dh, dw = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=rows,
+                                          chunk_cols=cols, flags=flags, inv_temp=inv_temp)
+    torch.cuda.synchronize()
+    adz = np.abs(dz64)
+    bf = bool(flags & _BF)
+    rh = _check_grad(dh, dh64, None, adz @ np.abs(w64), "dhidden", bf16=bf)
+    rw = _check_grad(dw, dw64, None, adz.T @ np.abs(h64), "dweight", bf16=bf)
+    H.log(f"lmhead inv_temp={inv_temp} T={T} d={d} V={V} block={rows}x{cols} flags={flags}: "
+          f"stats {max(err):.2e} dh {rh:.2e} dW {rw:.2e}")
+
+
+def test_lmhead_inverse_temperature_one_is_the_plain_call():
+    """At inv_temp = 1 the _ex statistics and the backward give the bits of the
+    calls without a temperature."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 300, 136, 2000
+    h, w, y, g = _problem(T, d, V)
+    hd, wd, yd, gd = _dev_bf16(h), _dev_bf16(w), _cuda(y), _cuda(g)
+    plain = dart.dart_lmhead_tok_stats(hd, wd, yd)
+    ex = dart.dart_lmhead_tok_stats_ex(hd, wd, yd, 1.0)
+    for a, b in zip(plain, ex):
+        assert torch.equal(a, b)
+    logp, _, lse = plain
+    ref = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
+    got = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128, chunk_cols=V,
+                                       inv_temp=1.0)
+    for a, b in zip(ref, got):
+        assert torch.equal(a, b)
 
 
 def test_lmhead_backward_blockings_agree():

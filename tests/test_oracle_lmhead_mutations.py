@@ -43,6 +43,10 @@ def _dz_with_next_rows_lse(z, target, lse, logp, g, **k):
     return _dlogits(z, target, np.roll(np.asarray(lse), 1), logp, g, **k)
 
 
+def _dz_without_temperature_factor(z, target, lse, logp, g, inv_temp=1.0, **k):
+    return _dlogits(z, target, lse, logp, g, inv_temp=inv_temp, **k) / inv_temp
+
+
 MUTATIONS = {
     "bf16_widening_off_by_one_bit": ("bf16_bits_to_f64", _widen_off_by_one_bit),
     "weight_read_as_d_by_v": ("lmhead_logits", _weight_read_as_d_by_v),
@@ -50,6 +54,7 @@ MUTATIONS = {
     "dlogits_negated": ("dlogits", _dz_negated),
     "dlogits_without_onehot": ("dlogits", _dz_without_target_term),
     "dlogits_with_other_rows_lse": ("dlogits", _dz_with_next_rows_lse),
+    "dlogits_without_temperature_factor": ("dlogits", _dz_without_temperature_factor),
 }
 
 
@@ -58,8 +63,9 @@ def _pins():
     out = [("zero_weight", pins.test_zero_weight_gives_uniform_rows),
            ("one_hot_weight", pins.test_one_hot_weight_rows_select_hidden_features),
            ("rank_one", pins.test_rank_one_closed_form)]
-    out += [(f"finite_differences[{s}]", (lambda s=s: pins.test_grads_finite_differences(s)))
-            for s in range(3)]
+    out += [(f"finite_differences[{s}-{it}]",
+             (lambda s=s, it=it: pins.test_grads_finite_differences(s, it)))
+            for s, it in ((0, 1.0), (1, 1.0), (2, 1.0), (3, 0.7))]
     return out
 
 

@@ -93,12 +93,14 @@ def test_matches_mini_oracle_dot_products(seed):
         assert abs(lse[t] - mini_stats[t][2]) <= 1e-12
 
 
-@pytest.mark.parametrize("seed", range(3))
-def test_grads_finite_differences(seed):
+@pytest.mark.parametrize("seed,inv_temp", [(0, 1.0), (1, 1.0), (2, 1.0), (3, 0.7), (4, 1.6)])
+def test_grads_finite_differences(seed, inv_temp):
     """Central differences of the loss (through the LM head, the statistics and
     the clipped TIS surrogate, with the mask and TIS weights fixed) with
     respect to every hidden-state and weight entry match dh = dz W and
-    dW = dz^T h; ratios are kept away from the clip bounds."""
+    dW = dz^T h; ratios are kept away from the clip bounds. At an inverse
+    temperature the differenced loss takes softmax(inv_temp h W^T), formed in
+    the pure-Python statistics, so the factor the chain rule adds is pinned."""
     rng = np.random.default_rng(70 + seed)
     T, d, V = 5, 6, 9
     h = gaussian_bits(seed, 9, T, d, 1.0)
@@ -108,17 +110,17 @@ def test_grads_finite_differences(seed):
     mask = np.array([1, 1], np.uint8) if seed % 2 == 0 else np.array([0, 1], np.uint8)
     A = rng.normal(0, 1, T).astype(np.float32)
     eps_low, eps_high, C = 0.2, 0.28, 1.5
-    logp0, _, lse0 = oracle.lmhead_token_stats(h, w, y)
+    logp0, _, lse0 = oracle.lmhead_token_stats(h, w, y, inv_temp=inv_temp)
     r_target = rng.choice([0.6, 0.95, 1.1, 1.5], T)
     lp_old = (logp0 - np.log(r_target)).astype(np.float32)
     lp_roll = (lp_old + rng.normal(0, 0.5, T)).astype(np.float32)
     res = oracle.tis_loss(logp0, lp_old, lp_roll, A, off, mask, eps_low, eps_high, C)
-    _, dh, dW = oracle.lmhead_grads(h, w, y, lse0, logp0, res["g"])
+    _, dh, dW = oracle.lmhead_grads(h, w, y, lse0, logp0, res["g"], inv_temp=inv_temp)
 
     hf, wf = oracle.bf16_bits_to_f64(h), oracle.bf16_bits_to_f64(w)
 
     def L_of(hh, ww):
-        rows = (hh @ ww.T).tolist()
+        rows = (inv_temp * (hh @ ww.T)).tolist()
         st = mini.token_stats(rows, y.tolist())
         L, _ = mini.loss_and_coef([s[0] for s in st], lp_old.astype(np.float64).tolist(),
                                   lp_roll.astype(np.float64).tolist(), A.astype(np.float64).tolist(),
