@@ -16,6 +16,9 @@ only marshal tensors and scale the [T] coefficient.
                                    offsets, rho, eps_low, eps_high, C)
     loss.backward()          # hidden.grad, weight.grad (bfloat16)
 
+Both take inv_temp (default 1, the paper's value): the policy is then
+softmax(inv_temp z), as for dart_tok_stats_ex and dart_tis_grad_ex.
+
 The LM-head backward writes its gradients in bfloat16 directly and, unless
 told otherwise, forms the dlogits in the blocks of rows x vocabulary entries
 that lmhead_backward_plan picks for a 512 MiB workspace.
@@ -23,7 +26,7 @@ that lmhead_backward_plan picks for a 512 MiB workspace.
 
 import torch
 
-from . import (DART_LMHEAD_BF16_GRADS, dart_lmhead_backward_ex, dart_lmhead_tok_stats,
+from . import (DART_LMHEAD_BF16_GRADS, dart_lmhead_backward_ex, dart_lmhead_tok_stats_ex,
                dart_step_select, dart_tis_grad, dart_tis_loss_fwd, dart_tok_stats,
                lmhead_backward_plan)
 
@@ -48,19 +51,20 @@ class DartPolicyLoss(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
-                eps_high, C):
+                eps_high, C, inv_temp):
         logits = logits.detach()
-        logp, ent, lse = dart_tok_stats(logits, target)
+        logp, ent, lse = dart_tok_stats(logits, target, inv_temp=inv_temp)
         loss, coef = _loss(logp, ent, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
                            eps_high, C)
+        ctx.inv_temp = inv_temp
         ctx.save_for_backward(logits, target, logp, lse, coef)
         return loss
 
     @staticmethod
     def backward(ctx, grad):
         logits, target, logp, lse, coef = ctx.saved_tensors
-        dz = dart_tis_grad(logits, target, logp, lse, _scaled(coef, grad))
-        return (dz,) + (None,) * 9
+        dz = dart_tis_grad(logits, target, logp, lse, _scaled(coef, grad), inv_temp=ctx.inv_temp)
+        return (dz,) + (None,) * 10
 
 
 class DartLmHeadPolicyLoss(torch.autograd.Function):
@@ -69,13 +73,14 @@ class DartLmHeadPolicyLoss(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, hidden, weight, target, logp_old, logp_rollout, adv, step_offsets, rho,
-                eps_low, eps_high, C, chunk_rows, chunk_cols, flags):
+                eps_low, eps_high, C, chunk_rows, chunk_cols, flags, inv_temp):
         hidden, weight = hidden.detach(), weight.detach()
-        logp, ent, lse = dart_lmhead_tok_stats(hidden, weight, target)
+        logp, ent, lse = dart_lmhead_tok_stats_ex(hidden, weight, target, inv_temp)
         loss, coef = _loss(logp, ent, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
                            eps_high, C)
         ctx.plan = lmhead_grad_plan(hidden.shape[0], weight.shape[0], chunk_rows, chunk_cols,
                                     flags)
+        ctx.inv_temp = inv_temp
         ctx.save_for_backward(hidden, weight, target, logp, lse, coef)
         return loss
 
@@ -84,8 +89,9 @@ class DartLmHeadPolicyLoss(torch.autograd.Function):
         hidden, weight, target, logp, lse, coef = ctx.saved_tensors
         rows, cols, flags = ctx.plan
         dh, dw = dart_lmhead_backward_ex(hidden, weight, target, lse, logp, _scaled(coef, grad),
-                                         chunk_rows=rows, chunk_cols=cols, flags=flags)
-        return (dh, dw) + (None,) * 12
+                                         chunk_rows=rows, chunk_cols=cols, flags=flags,
+                                         inv_temp=ctx.inv_temp)
+        return (dh, dw) + (None,) * 13
 
 
 def lmhead_grad_plan(T, V, chunk_rows=None, chunk_cols=None, flags=None):
@@ -100,18 +106,18 @@ def lmhead_grad_plan(T, V, chunk_rows=None, chunk_cols=None, flags=None):
 
 
 def dart_policy_loss(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
-                     eps_high, C):
+                     eps_high, C, inv_temp=1.0):
     """Differentiable DART loss of the logits (see the module docstring)."""
     return DartPolicyLoss.apply(logits, target, logp_old, logp_rollout, adv, step_offsets, rho,
-                                eps_low, eps_high, C)
+                                eps_low, eps_high, C, float(inv_temp))
 
 
 def dart_lmhead_policy_loss(hidden, weight, target, logp_old, logp_rollout, adv, step_offsets,
                             rho, eps_low, eps_high, C, chunk_rows=None, chunk_cols=None,
-                            flags=None):
+                            flags=None, inv_temp=1.0):
     """Differentiable DART loss of the LM head's inputs (see the module
     docstring); chunk_rows, chunk_cols and flags as for dart_lmhead_backward_ex
     (no block: the default plan)."""
     return DartLmHeadPolicyLoss.apply(hidden, weight, target, logp_old, logp_rollout, adv,
                                       step_offsets, rho, eps_low, eps_high, C, chunk_rows,
-                                      chunk_cols, flags)
+                                      chunk_cols, flags, float(inv_temp))

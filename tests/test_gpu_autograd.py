@@ -110,3 +110,58 @@ def test_lmhead_policy_loss_autograd_matches_direct(rows, cols, flags):
         _, dw32 = dart.dart_lmhead_backward(h, w, y, lse, logp, coef, chunk_rows=256)
         torch.cuda.synchronize()
         assert torch.equal(wx.grad.view(torch.int16), dw32.to(torch.bfloat16).view(torch.int16))
+
+
+def test_autograd_inverse_temperature_matches_direct():
+    """At an inverse temperature both wrappers give the bits of the direct
+    calls at that temperature (whose parity with the oracle is tested on its
+    own): the loss and the gradient of the logits, and the loss and the bf16
+    gradients of the LM head's inputs."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+    from paper_2509_23866_amd.autograd import (dart_lmhead_policy_loss, dart_policy_loss,
+                                               lmhead_grad_plan)
+
+    it = 1.4
+    logits, target, off, adv, rng = _workload()
+    logp, ent, lse = dart.dart_tok_stats(logits, target, inv_temp=it)
+    lp_old = logp + _cuda(rng.normal(0, 0.05, logp.numel()).astype(np.float32))
+    lp_roll = lp_old + _cuda(rng.normal(0, 0.1, logp.numel()).astype(np.float32))
+    _, mask, _ = dart.dart_step_select(ent, off, 0.8)
+    loss_ref, coef, _ = dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, 0.2, 0.28,
+                                               2.0)
+    dz_ref = dart.dart_tis_grad(logits, target, logp, lse, coef, inv_temp=it)
+    x = logits.clone().requires_grad_(True)
+    loss = dart_policy_loss(x, target, lp_old, lp_roll, adv, off, 0.8, 0.2, 0.28, 2.0, inv_temp=it)
+    loss.backward()
+    torch.cuda.synchronize()
+    assert loss.item() == loss_ref.item()
+    assert torch.equal(x.grad.view(torch.int16), dz_ref.view(torch.int16))
+
+    T, d, V, S = 600, 256, 5000, 10
+    h = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    w = torch.empty((V, d), dtype=torch.bfloat16, device="cuda")
+    sn.fill_gaussian_device(h, 11, STREAM_HIDDEN, 1.0)
+    sn.fill_gaussian_device(w, 11, STREAM_WEIGHT, 3.0 / math.sqrt(d))
+    y = _cuda(rng.integers(0, V, T).astype(np.int32))
+    off = _cuda(np.linspace(0, T, S + 1).astype(np.int32))
+    adv = _cuda(rng.normal(0, 1, T).astype(np.float32))
+    logp, ent, lse = dart.dart_lmhead_tok_stats_ex(h, w, y, it)
+    lp_old = logp + _cuda(rng.normal(0, 0.05, T).astype(np.float32))
+    lp_roll = lp_old + _cuda(rng.normal(0, 0.1, T).astype(np.float32))
+    _, mask, _ = dart.dart_step_select(ent, off, 0.7)
+    loss_ref, coef, _ = dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, 0.2, 0.28,
+                                               2.0)
+    r, c, f = lmhead_grad_plan(T, V)
+    dh_ref, dw_ref = dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=r,
+                                                  chunk_cols=c, flags=f, inv_temp=it)
+    hx = h.clone().requires_grad_(True)
+    wx = w.clone().requires_grad_(True)
+    loss = dart_lmhead_policy_loss(hx, wx, y, lp_old, lp_roll, adv, off, 0.7, 0.2, 0.28, 2.0,
+                                   inv_temp=it)
+    loss.backward()
+    torch.cuda.synchronize()
+    assert loss.item() == loss_ref.item()
+    assert torch.equal(hx.grad.view(torch.int16), dh_ref.view(torch.int16))
+    assert torch.equal(wx.grad.view(torch.int16), dw_ref.view(torch.int16))
