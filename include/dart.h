@@ -353,6 +353,18 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
                                   const float* tok_coef, void* dlogits, int64_t ld_out,
                                   hipStream_t stream);
 
+/* dart_lmhead_dlogits at inverse temperature inv_temp (the value given to
+ * dart_lmhead_tok_stats_ex for lse and logp):
+ *   dlogits[t, v] = inv_temp * tok_coef[t] * (onehot(target[t])[v] - exp(inv_temp z_tv - lse[t]))
+ * as dart_tis_grad_ex defines it for materialised logits (inv_temp = 1 gives
+ * the bits of dart_lmhead_dlogits). inv_temp: finite and > 0, else
+ * INVALID_ARG. Other arguments and errors as dart_lmhead_dlogits. */
+dart_status_t dart_lmhead_dlogits_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                     const void* weight, int64_t V, int64_t ld_w,
+                                     const int32_t* target, const float* lse, const float* logp,
+                                     const float* tok_coef, float inv_temp, void* dlogits,
+                                     int64_t ld_out, hipStream_t stream);
+
 /* The gradient pass of the fused head, whole: the gradients of the loss with
  * respect to the hidden states and the LM-head weight,
  *   dhidden = dlogits W        [T, d]

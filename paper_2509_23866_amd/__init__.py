@@ -39,7 +39,7 @@ EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart
             "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
             "dart_lmhead_tok_stats", "dart_lmhead_tok_stats_ex", "dart_lmhead_stats_workspace_bytes",
-            "dart_lmhead_dlogits",
+            "dart_lmhead_dlogits", "dart_lmhead_dlogits_ex",
             "dart_lmhead_backward", "dart_lmhead_backward_workspace_bytes",
             "dart_lmhead_backward_ex", "dart_lmhead_backward_ex_workspace_bytes", "dart_kept_steps",
             "dart_status_string")
@@ -116,6 +116,9 @@ def load_library():
         lib.dart_lmhead_dlogits.restype = ctypes.c_int
         lib.dart_lmhead_dlogits.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
                                             _P, _I64, _P]
+        lib.dart_lmhead_dlogits_ex.restype = ctypes.c_int
+        lib.dart_lmhead_dlogits_ex.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P,
+                                               _P, ctypes.c_float, _P, _I64, _P]
         lib.dart_lmhead_backward.restype = ctypes.c_int
         lib.dart_lmhead_backward.argtypes = [_P, _I64, _I64, _I64, _P, _I64, _I64, _P, _P, _P, _P,
                                              _P, _I64, _P, _I64, _I64, _P, ctypes.c_size_t, _P]
@@ -558,9 +561,12 @@ def _lmhead_common(hidden, weight, target, lse, logp, tok_coef):
     return dev, T, d, weight.shape[0]
 
 
-def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=None, stream=None):
+def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=None, stream=None,
+                        inv_temp=None):
     """bfloat16 [T, V] dlogits = tok_coef (onehot - softmax(hidden @ weight^T)), the
-    logits recomputed on the matrix cores; lse and logp from dart_lmhead_tok_stats."""
+    logits recomputed on the matrix cores; lse and logp from dart_lmhead_tok_stats.
+    With inv_temp (dart_lmhead_dlogits_ex): inv_temp tok_coef (onehot -
+    softmax(inv_temp hidden @ weight^T)), lse and logp from dart_lmhead_tok_stats_ex."""
     torch = _torch()
     dev, T, d, V = _lmhead_common(hidden, weight, target, lse, logp, tok_coef)
     if dlogits is None:
@@ -568,12 +574,16 @@ def dart_lmhead_dlogits(hidden, weight, target, lse, logp, tok_coef, dlogits=Non
     _matrix_bf16("dlogits", dlogits, dev)
     if tuple(dlogits.shape) != (T, V):
         raise ValueError(f"dlogits must have shape ({T}, {V})")
-    rc = load_library().dart_lmhead_dlogits(
-        hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
-        target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr(),
-        dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream, dev))
+    args = [hidden.data_ptr(), T, d, hidden.stride(0), weight.data_ptr(), V, weight.stride(0),
+            target.data_ptr(), lse.data_ptr(), logp.data_ptr(), tok_coef.data_ptr()]
+    name = "dart_lmhead_dlogits"
+    if inv_temp is not None:
+        args.append(float(inv_temp))
+        name += "_ex"
+    args += [dlogits.data_ptr(), dlogits.stride(0), _stream_handle(stream, dev)]
+    rc = getattr(load_library(), name)(*args)
     if rc != DART_OK:
-        raise DartError("dart_lmhead_dlogits", rc)
+        raise DartError(name, rc)
     return dlogits
 
 

@@ -761,12 +761,13 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
                                     entropy, lse, workspace, workspace_bytes, stream);
 }
 
-dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
-                                  const void* weight, int64_t V, int64_t ld_w,
-                                  const int32_t* target, const float* lse, const float* logp,
-                                  const float* tok_coef, void* dlogits, int64_t ld_out,
-                                  hipStream_t stream) {
+dart_status_t dart_lmhead_dlogits_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                     const void* weight, int64_t V, int64_t ld_w,
+                                     const int32_t* target, const float* lse, const float* logp,
+                                     const float* tok_coef, float inv_temp, void* dlogits,
+                                     int64_t ld_out, hipStream_t stream) {
     if (bad_lmhead_args(hidden, T, d, ld_h, weight, V, ld_w)) return DART_ERR_INVALID_ARG;
+    if (!(inv_temp > 0.f) || isinf(inv_temp)) return DART_ERR_INVALID_ARG;
     if (!target || !lse || !logp || !tok_coef || !dlogits || ld_out < V || ld_out % 8 ||
         reinterpret_cast<uintptr_t>(dlogits) % 16)
         return DART_ERR_INVALID_ARG;
@@ -776,7 +777,16 @@ dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int6
 
     return launch_dlogits(static_cast<const uint16_t*>(hidden), T, d, ld_h,
                           static_cast<const uint16_t*>(weight), V, ld_w, target, lse, logp,
-                          tok_coef, 1.f, static_cast<uint16_t*>(dlogits), ld_out, 0, stream);
+                          tok_coef, inv_temp, static_cast<uint16_t*>(dlogits), ld_out, 0, stream);
+}
+
+dart_status_t dart_lmhead_dlogits(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
+                                  const void* weight, int64_t V, int64_t ld_w,
+                                  const int32_t* target, const float* lse, const float* logp,
+                                  const float* tok_coef, void* dlogits, int64_t ld_out,
+                                  hipStream_t stream) {
+    return dart_lmhead_dlogits_ex(hidden, T, d, ld_h, weight, V, ld_w, target, lse, logp, tok_coef,
+                                  1.f, dlogits, ld_out, stream);
 }
 
 size_t dart_lmhead_backward_workspace_bytes(int64_t chunk_rows, int64_t V) {

@@ -232,6 +232,8 @@ def test_lmhead_inverse_temperature_rejects(inv_temp):
     assert lib.dart_lmhead_tok_stats_ex(*a[:8], inv_temp, *a[8:]) == dart.DART_ERR_INVALID_ARG
     assert (lib.dart_lmhead_backward_ex(*_lm_bwd_ex_args(inv_temp=inv_temp))
             == dart.DART_ERR_INVALID_ARG)
+    g = _lm_grad_args()
+    assert lib.dart_lmhead_dlogits_ex(*g[:11], inv_temp, *g[11:]) == dart.DART_ERR_INVALID_ARG
 
 
 def test_lmhead_workspace_bytes():
@@ -259,6 +261,8 @@ def _lm_grad_args(**kw):
 def test_lmhead_dlogits_rejects(kw):
     lib = dart.load_library()
     assert lib.dart_lmhead_dlogits(*_lm_grad_args(**kw)) == dart.DART_ERR_INVALID_ARG
+    g = _lm_grad_args(**kw)
+    assert lib.dart_lmhead_dlogits_ex(*g[:11], 1.0, *g[11:]) == dart.DART_ERR_INVALID_ARG
 
 
 def _lm_bwd_args(**kw):

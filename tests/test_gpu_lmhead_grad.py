@@ -483,8 +483,9 @@ def test_lmhead_backward_ex_modes(T, d, V, pad, rows, cols, flags):
 def test_lmhead_inverse_temperature(T, d, V, pad, rows, cols, flags, inv_temp):
     """Statistics and gradients of softmax(inv_temp h W^T) (the _ex entry
     points) against the oracle at the same inverse temperature: logp, H and lse
-    to the tolerances of the logits path, dhidden and dweight to 3 U B + A B
-    with the factor inv_temp inside dz."""
+    to the tolerances of the logits path, dz within 1 bf16 ulp, dhidden and
+    dweight to 3 U B + A B with the factor inv_temp inside dz (and to A B
+    against the GPU's own dz, the consistency property of the GEMM stage)."""
     import torch
 
     import paper_2509_23866_amd as dart
@@ -499,15 +500,21 @@ def test_lmhead_inverse_temperature(T, d, V, pad, rows, cols, flags, inv_temp):
     got = [x.cpu().numpy().astype(np.float64) for x in (logp, ent, lse)]
     err = [float(np.abs(a - b).max()) for a, b in zip(got, ref)]
     assert err[0] <= H.LOGP_TOL and err[1] <= H.H_TOL and err[2] <= H.LOGP_TOL, err
+    buf = torch.empty((T, (V + 7) // 8 * 8), dtype=torch.bfloat16, device="cuda")
+    dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, _cuda(g), dlogits=buf[:, :V],
+                             inv_temp=inv_temp)
+    torch.cuda.synchronize()
+    ulps = H.check_dz(_bits(buf[:, :V]), dz64, "bf16")
+    dzo = buf[:, :V].double().cpu().numpy()
     dh, dw = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, _cuda(g), chunk_rows=rows,
                                           chunk_cols=cols, flags=flags, inv_temp=inv_temp)
     torch.cuda.synchronize()
     adz = np.abs(dz64)
     bf = bool(flags & _BF)
-    rh = _check_grad(dh, dh64, None, adz @ np.abs(w64), "dhidden", bf16=bf)
-    rw = _check_grad(dw, dw64, None, adz.T @ np.abs(h64), "dweight", bf16=bf)
+    rh = _check_grad(dh, dh64, dzo @ w64, adz @ np.abs(w64), "dhidden", bf16=bf)
+    rw = _check_grad(dw, dw64, dzo.T @ h64, adz.T @ np.abs(h64), "dweight", bf16=bf)
     H.log(f"lmhead inv_temp={inv_temp} T={T} d={d} V={V} block={rows}x{cols} flags={flags}: "
-          f"stats {max(err):.2e} dh {rh:.2e} dW {rw:.2e}")
+          f"stats {max(err):.2e} dz {ulps:.2f} ulp dh {rh:.2e} dW {rw:.2e}")
 
 
 def test_lmhead_inverse_temperature_one_is_the_plain_call():
@@ -525,6 +532,9 @@ def test_lmhead_inverse_temperature_one_is_the_plain_call():
     for a, b in zip(plain, ex):
         assert torch.equal(a, b)
     logp, _, lse = plain
+    z1 = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd)
+    z2 = dart.dart_lmhead_dlogits(hd, wd, yd, lse, logp, gd, inv_temp=1.0)
+    assert torch.equal(z1.view(torch.int16), z2.view(torch.int16))
     ref = dart.dart_lmhead_backward(hd, wd, yd, lse, logp, gd, chunk_rows=128)
     got = dart.dart_lmhead_backward_ex(hd, wd, yd, lse, logp, gd, chunk_rows=128, chunk_cols=V,
                                        inv_temp=1.0)
