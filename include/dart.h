@@ -152,6 +152,35 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
  * T < 1 or T > INT32_MAX). Host only. */
 size_t dart_tis_loss_workspace_bytes(int64_t T);
 
+/* dart_tis_loss_fwd_bwd for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation, checks, kernels and results, bit for bit,
+ * with the loss workspace taken from a fixed array in the library's device
+ * memory instead of a caller argument. The call allocates nothing and calls
+ * no allocating routine.
+ *   Arguments: as for dart_tis_loss_fwd_bwd, without workspace and
+ *              workspace_bytes. The caller still owns every input and output.
+ *   Scratch:   40,976 bytes per GPU (the largest loss workspace), held
+ *              from the first call on that GPU until the process ends; it
+ *              covers every T the call accepts (T <= INT32_MAX), and its
+ *              contents on entry do not matter.
+ *   Races:     every call on one GPU uses that GPU's one array, so calls that
+ *              may run at the same time on one GPU (two streams, two host
+ *              threads) race and give undefined results: order them on one
+ *              stream, or use dart_tis_loss_fwd_bwd with a workspace each.
+ * Errors: those of dart_tis_loss_fwd_bwd; UNSUPPORTED if T needs more scratch
+ * than the array holds (not reachable for T <= INT32_MAX); HIP if the array's
+ * device address cannot be obtained. */
+dart_status_t dart_tis_loss_fwd_bwd_noalloc(const void* logits, dart_dtype_t dtype, int64_t T,
+                                            int64_t V, int64_t ld, const int32_t* target,
+                                            const float* logp, const float* lse,
+                                            const float* logp_old, const float* logp_rollout,
+                                            const float* adv, const int32_t* step_offsets,
+                                            int64_t S, const uint8_t* step_mask, float eps_low,
+                                            float eps_high, float C, void* dlogits, int64_t ld_out,
+                                            double* loss, float* tok_coef, float* stats,
+                                            hipStream_t stream);
+
 /* The two halves of dart_tis_loss_fwd_bwd, for callers that want the loss
  * without the gradient, or that time the two kernels separately.
  * dart_tis_loss_fwd computes loss, tok_coef and stats exactly as above (the

@@ -36,7 +36,8 @@ DART_LMHEAD_SKIP_ZERO_ROWS = 1
 DART_LMHEAD_BF16_GRADS = 4
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
-            "dart_tis_grad", "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
+            "dart_tis_grad", "dart_tis_loss_fwd_bwd_noalloc",
+            "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
             "dart_lmhead_tok_stats", "dart_lmhead_tok_stats_ex", "dart_lmhead_stats_workspace_bytes",
             "dart_lmhead_dlogits", "dart_lmhead_dlogits_ex",
@@ -80,6 +81,10 @@ def load_library():
             _P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P,
             ctypes.c_float, ctypes.c_float, ctypes.c_float, _P, _I64, _P, _P, _P, _P,
             ctypes.c_size_t, _P]
+        lib.dart_tis_loss_fwd_bwd_noalloc.restype = ctypes.c_int
+        lib.dart_tis_loss_fwd_bwd_noalloc.argtypes = [
+            _P, ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P,
+            ctypes.c_float, ctypes.c_float, ctypes.c_float, _P, _I64, _P, _P, _P, _P]
         lib.dart_tis_loss_fwd.restype = ctypes.c_int
         lib.dart_tis_loss_fwd.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, ctypes.c_float,
                                           ctypes.c_float, ctypes.c_float, _P, _P, _P, _P,
@@ -309,6 +314,47 @@ def dart_tis_loss_fwd_bwd(logits, target, logp, lse, logp_old, logp_rollout, adv
         _stream_handle(stream, dev))
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd_bwd", rc)
+    return loss, dlogits, tok_coef, stats
+
+
+def dart_tis_loss_fwd_bwd_noalloc(logits, target, logp, lse, logp_old, logp_rollout, adv,
+                                  step_offsets, step_mask, eps_low, eps_high, C, dlogits=None,
+                                  loss=None, tok_coef=None, stats=None, with_stats=True,
+                                  stream=None):
+    """dart_tis_loss_fwd_bwd with the loss workspace in the library's fixed
+    per-GPU scratch array (the C call allocates nothing; outputs not given are
+    allocated here by torch). Calls on one GPU that may overlap race."""
+    torch = _torch()
+    dt, T, V, ld = _logits_meta(logits)
+    dev = logits.device
+    S = step_offsets.numel() - 1
+    _check_vec("target", target, torch.int32, T, dev)
+    for n, v in (("logp", logp), ("lse", lse), ("logp_old", logp_old),
+                 ("logp_rollout", logp_rollout), ("adv", adv)):
+        _check_vec(n, v, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    if dlogits is None:
+        dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+    if (dlogits.dtype != logits.dtype or dlogits.dim() != 2 or tuple(dlogits.shape) != (T, V)
+            or dlogits.stride(1) != 1 or dlogits.device != dev):
+        raise ValueError("dlogits must match logits in dtype and shape, with contiguous rows")
+    loss = torch.empty(1, dtype=torch.float64, device=dev) if loss is None else loss
+    tok_coef = torch.empty(T, dtype=torch.float32, device=dev) if tok_coef is None else tok_coef
+    if stats is None and with_stats:
+        stats = torch.empty(4, dtype=torch.float32, device=dev)
+    _check_vec("loss", loss, torch.float64, 1, dev)
+    _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
+    if stats is not None:
+        _check_vec("stats", stats, torch.float32, 4, dev)
+    rc = load_library().dart_tis_loss_fwd_bwd_noalloc(
+        logits.data_ptr(), dt, T, V, ld, target.data_ptr(), logp.data_ptr(), lse.data_ptr(),
+        logp_old.data_ptr(), logp_rollout.data_ptr(), adv.data_ptr(), step_offsets.data_ptr(), S,
+        step_mask.data_ptr(), float(eps_low), float(eps_high), float(C), dlogits.data_ptr(),
+        dlogits.stride(0), loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats),
+        _stream_handle(stream, dev))
+    if rc != DART_OK:
+        raise DartError("dart_tis_loss_fwd_bwd_noalloc", rc)
     return loss, dlogits, tok_coef, stats
 
 

@@ -26,6 +26,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "internal.h"
@@ -1278,7 +1279,58 @@ bool bad_workspace(const void* workspace, size_t bytes, int64_t T) {
            reinterpret_cast<uintptr_t>(workspace) % sizeof(double) != 0;
 }
 
+// Host-side argument rules of dart_tis_loss_fwd_bwd (both halves), workspace
+// aside: true when the call must return DART_ERR_INVALID_ARG.
+bool bad_fwd_bwd_args(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V, int64_t ld,
+                      const int32_t* target, const float* logp, const float* lse,
+                      const float* logp_old, const float* logp_rollout, const float* adv,
+                      const int32_t* step_offsets, int64_t S, const uint8_t* step_mask,
+                      float eps_low, float eps_high, float C, const void* dlogits, int64_t ld_out,
+                      const double* loss, const float* tok_coef) {
+    if (!logits || !target || !lse || !dlogits) return true;
+    if (bad_dtype(dtype) || V < 1 || ld < V || ld_out < V) return true;
+    const size_t es = elem_size(dtype);
+    if (reinterpret_cast<uintptr_t>(logits) % es || reinterpret_cast<uintptr_t>(dlogits) % es)
+        return true;
+    if (!logp || !logp_old || !logp_rollout || !adv || !step_offsets || !step_mask || !loss ||
+        !tok_coef)
+        return true;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return true;
+    if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return true;
+    return bad_overlap(logits, ld, dlogits, ld_out, T, V, es);
+}
+
 }  // namespace
+
+// Scratch of dart_tis_loss_fwd_bwd_noalloc: the loss kernels' per-workgroup
+// partial sums and the kept counts, sized for the largest many-workgroup
+// launch (kCoefMaxBlocks workgroups, 40,976 bytes), so every T fits. Each
+// device holds its own copy for the life of the process. Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in for
+// the symbol): the device address comes from hipGetSymbolAddress, once per
+// device, with that device current.
+constexpr int64_t kNoAllocScratchDoubles = coef_workspace_doubles(kCoefMaxBlocks);
+constexpr size_t kNoAllocScratchBytes = (size_t)kNoAllocScratchDoubles * sizeof(double);
+static __device__ __align__(256) double scratch[kNoAllocScratchDoubles];
+
+constexpr int kMaxScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The device address of dev's scratch array (null on a HIP error or a device
+// index beyond kMaxScratchDevices).
+static void* device_scratch(int dev) {
+    if (dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        DeviceGuard on_dev(dev);
+        if (!on_dev.ok) return nullptr;
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
 
 extern "C" {
 
@@ -1552,6 +1604,35 @@ dart_status_t dart_tis_loss_fwd_bwd(const void* logits, dart_dtype_t dtype, int6
     if (st != DART_OK) return st;
     return dart_tis_grad(logits, dtype, T, V, ld, target, logp, lse, tok_coef, dlogits, ld_out,
                          stream);
+}
+
+
+dart_status_t dart_tis_loss_fwd_bwd_noalloc(const void* logits, dart_dtype_t dtype, int64_t T,
+                                            int64_t V, int64_t ld, const int32_t* target,
+                                            const float* logp, const float* lse,
+                                            const float* logp_old, const float* logp_rollout,
+                                            const float* adv, const int32_t* step_offsets,
+                                            int64_t S, const uint8_t* step_mask, float eps_low,
+                                            float eps_high, float C, void* dlogits, int64_t ld_out,
+                                            double* loss, float* tok_coef, float* stats,
+                                            hipStream_t stream) {
+    // host-side rules first: a bad argument is reported before any HIP call
+    if (bad_fwd_bwd_args(logits, dtype, T, V, ld, target, logp, lse, logp_old, logp_rollout, adv,
+                         step_offsets, S, step_mask, eps_low, eps_high, C, dlogits, ld_out, loss,
+                         tok_coef))
+        return DART_ERR_INVALID_ARG;
+    // the workspace this T needs must fit the scratch array (always true for
+    // T <= INT32_MAX: the many-workgroup launch is capped at kCoefMaxBlocks)
+    if (dart_tis_loss_workspace_bytes(T) > kNoAllocScratchBytes) return DART_ERR_UNSUPPORTED;
+    const int dev = stream_device(stream);
+    if (dev < 0) return DART_ERR_HIP;
+    void* ws = device_scratch(dev);
+    if (!ws) return DART_ERR_HIP;
+    // every argument rule of dart_tis_loss_fwd_bwd applies unchanged
+    return dart_tis_loss_fwd_bwd(logits, dtype, T, V, ld, target, logp, lse, logp_old,
+                                 logp_rollout, adv, step_offsets, S, step_mask, eps_low, eps_high,
+                                 C, dlogits, ld_out, loss, tok_coef, stats, ws,
+                                 kNoAllocScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -120,6 +120,23 @@ def test_tis_loss_rejects(kw):
     assert lib.dart_tis_loss_fwd_bwd(*_tis_args(**kw), None) == dart.DART_ERR_INVALID_ARG
 
 
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(logits=0), dict(target=0), dict(logp=0), dict(lse=0), dict(lp_old=0), dict(lp_roll=0),
+    dict(adv=0), dict(off=0), dict(mask=0), dict(dlogits=0), dict(loss=0), dict(coef=0),
+    dict(T=0), dict(T=1 << 31), dict(V=0), dict(ld=7), dict(ld_out=7), dict(S=0), dict(S=5),
+    dict(dtype=3), dict(eps_low=-0.1), dict(eps_high=float("nan")), dict(C=0.0),
+    dict(C=float("nan")), dict(dlogits=P + 2), dict(dlogits=P, ld_out=9),
+    dict(dlogits=(1 << 20) + 1),
+])
+def test_tis_loss_noalloc_rejects_before_any_hip_call(kw):
+    """The no-allocation entry point applies dart_tis_loss_fwd_bwd's host rules
+    before it looks up its scratch array (no GPU here: a HIP call would fail)."""
+    lib = dart.load_library()
+    args = _tis_args(**kw)[:-2]  # no workspace arguments
+    assert lib.dart_tis_loss_fwd_bwd_noalloc(*args, None) == dart.DART_ERR_INVALID_ARG
+
+
 def test_workspace_bytes():
     """kParts = 5 doubles per workgroup of 1024 tokens (at most 1024
     workgroups), then N and K."""
