@@ -43,10 +43,16 @@ def parse_args():
     ap.add_argument("--workload", default="vlm7b",
                     choices=["tiny", "vlm7b", "microbatch", "longhorizon", "edge"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-threads", type=int, default=0, help="0 = the process's CPU affinity (max 16)")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="0 = the CPU share of one GPU (16 cores) or the process's affinity if smaller")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the separately reported variants and the copy ceiling "
                          "(profiling runs of the headline step)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="measure only --workload, not the other workloads first "
+                         "(profiling runs of the headline step)")
+    ap.add_argument("--no-lmhead", action="store_true",
+                    help="leave the fused LM-head variant out")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed steps, run one plain device copy of this many MiB "
                          "(torch copy kernel) so that hardware counters can be scaled by it")
@@ -59,20 +65,10 @@ def kernel_source_hash():
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload):
-    """HBM bytes per launch of the dominant kernel from the committed PMC
-    summary, if it was taken on the current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", f"{DOMINANT}_{workload}_traffic.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as fh:
-        rec = json.load(fh)
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
-        return None
-    return rec.get("hbm_bytes_per_launch")
-
-
 CPU_SAMPLE_MAX_ROWS = 8192
+# host cores one GPU's share of the machine provides: the oracle baseline runs
+# that many OpenMP threads (fewer if the process's affinity is smaller)
+CPU_SHARE = 16
 
 
 def _steps_prefix(wl, max_rows):
@@ -451,24 +447,37 @@ def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
             "block": [rows, cols]}
 
 
-def main():
-    args = parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the library has no multi-GPU path; "
-              "run with --gpus 1.", file=sys.stderr)
-        return 2
+SWEEP_ORDER = ("tiny", "edge", "microbatch", "longhorizon")
 
+
+def measured_profile(kernel, workload, variant=""):
+    """The committed PMC record of a kernel at a workload (``variant``: e.g.
+    "skip" for the read-skipping gradient), if it was taken on the current
+    kernel source (else None)."""
+    name = f"{kernel}_{workload}{'_' + variant if variant else ''}_traffic.json"
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec
+
+
+def measure_workload(wl, args, dev, headline):
+    """One workload: inputs generated in HBM, W untimed steps, K timed steps
+    back to back, K more steps with events around each kernel, the
+    read-skipping gradient and the statistics pass alone, and a plain
+    elementwise copy of the same bytes. With ``headline`` also the variants
+    that are reported only for the headline workload. Returns a dict of
+    results; every buffer is freed on return."""
     import numpy as np
     import torch
 
     import paper_2509_23866_amd as dart
-    import synth
     import synth.native as sn
 
-    wl = synth.make_workload(args.workload)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
     esize = 4 if wl.dtype == "f32" else 2
     T, V, S = wl.T, wl.V, wl.S
@@ -512,7 +521,7 @@ def main():
         if ev:
             ev[3].record(s)
 
-    if args.calib_copy_mib:
+    if headline and args.calib_copy_mib:
         # a plain elementwise kernel that reads and writes exactly this many
         # bytes (a same-dtype copy_ would go to the DMA engine, not a kernel)
         n = args.calib_copy_mib * (1 << 20) // 2
@@ -570,43 +579,52 @@ def main():
         step(evs[i])
     torch.cuda.synchronize(dev)
 
-    # separately reported variants (never the headline): the gradient pass with
-    # zero-coefficient rows written without reading them, and the statistics
-    # pass alone (the forward-only recompute of pi_old's log-probs)
+    # separately reported variants (never the headline value): the gradient
+    # pass with zero-coefficient rows written without reading them, and the
+    # statistics pass alone (the forward-only recompute of pi_old's log-probs)
     variants = {}
-    if not wl.inplace and not args.no_variants:
+    if not args.no_variants:
         zero_rows = float((coef == 0).float().mean().item())
-        ev_v = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        skip_out = torch.empty_like(logits) if wl.inplace else dlogits
+        ev_v = [[ev_new() for _ in range(2)] for _ in range(args.steps)]
         for i in range(args.steps):
             ev_v[i][0].record(stream)
-            dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream,
-                               skip_zero_rows=True)
+            dart.dart_tis_grad(pristine if wl.inplace else logits, target, logp, lse, coef,
+                               skip_out, stream=stream, skip_zero_rows=True)
             ev_v[i][1].record(stream)
         torch.cuda.synchronize(dev)
+        del skip_out
         skip_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_v]))
+        model_bytes = (2.0 - zero_rows) * T * V * esize
+        rec = measured_profile(DOMINANT, wl.name, "skip")
+        meas = rec.get("hbm_bytes_per_launch") if rec else None
         variants["grad_skip_zero_rows"] = {
             "zero_row_fraction": zero_rows, "grad_ms": skip_ms,
-            "hbm_bytes_per_launch": (1.0 - zero_rows) * T * V * esize + T * V * esize,
-            "achieved_GBps": ((1.0 - zero_rows) + 1.0) * T * V * esize / (skip_ms * 1e-3) / 1e9}
-    if not args.no_variants:
-        ev_s = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+            "model_bytes_per_launch": model_bytes,
+            "hbm_bytes_per_launch_measured": meas,
+            "measured_over_model": (meas / model_bytes) if meas else None,
+            "achieved_GBps": (meas if meas else model_bytes) / (skip_ms * 1e-3) / 1e9,
+            "bytes_source": (f"rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE: {rec['summary']}" if rec
+                             else "model (2 - f) T V b; no counter record on this source")}
+        ev_s = [[ev_new() for _ in range(2)] for _ in range(args.steps)]
         for i in range(args.steps):
             ev_s[i][0].record(stream)
-            dart.dart_tok_stats(logits, target, logp, ent, lse, stream=stream)
+            dart.dart_tok_stats(pristine if wl.inplace else logits, target, logp, ent, lse,
+                                stream=stream)
             ev_s[i][1].record(stream)
         torch.cuda.synchronize(dev)
         stats_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev_s]))
         variants["stats_only"] = {"ms": stats_ms, "logit_elements_per_s": T * V / (stats_ms * 1e-3),
                                   "achieved_GBps": T * V * esize / (stats_ms * 1e-3) / 1e9}
 
-    if not wl.inplace and not args.no_variants:
+    if headline and not wl.inplace and not args.no_variants:
         variants["hip_graph"] = graph_variant(step, stream, dev, args.steps, args.warmup)
         variants["objective_variants"] = objective_variant(
             wl, dev, stream, logits, target, off, adv, lp_old, lp_roll, dlogits, step,
             min(args.steps, 20))
-    if not args.no_variants:
+    if headline and not args.no_variants:
         variants["groups"] = groups_variant(wl, dev, stream, ent, off, min(args.steps, 20))
-    if not args.no_variants:
+    if headline and not args.no_variants and not args.no_lmhead:
         variants["lmhead_fused"] = lmhead_variant(wl, dev, stream, target, coef,
                                                   min(args.steps, 10))
 
@@ -614,59 +632,130 @@ def main():
     # reading and writing the same T x V bytes as the gradient pass
     copy_ceiling = None
     if not args.no_variants:
+        src_c = pristine if wl.inplace else logits
         copy_ev = [(ev_new(), ev_new()) for _ in range(min(args.steps, 10))]
-        torch.mul(logits, 1.0, out=dlogits)  # first launch loads the kernel's code
+        torch.mul(src_c, 1.0, out=dlogits)  # first launch loads the kernel's code
         for a, b in copy_ev:
             a.record(stream)
-            torch.mul(logits, 1.0, out=dlogits)
+            torch.mul(src_c, 1.0, out=dlogits)
             b.record(stream)
         torch.cuda.synchronize(dev)
         copy_ms = float(np.median([a.elapsed_time(b) for a, b in copy_ev]))
         copy_gbs = 2 * T * V * esize / (copy_ms * 1e-3) / 1e9
         copy_ceiling = {"kernel": "torch elementwise multiply by 1 (T x V read + write)",
                         "ms": copy_ms, "GBps": copy_gbs, "frac": copy_gbs / HBM_PEAK_GBS}
-        if pristine is not None:
-            logits.copy_(pristine)
 
     k1_ms = [e[0].elapsed_time(e[1]) for e in evs]
     mid_ms = [e[1].elapsed_time(e[2]) for e in evs]
     grad_ms = [e[2].elapsed_time(e[3]) for e in evs]
     elems = T * V
-    value = elems / (ms_per_step * 1e-3)
-    grad_s = float(np.mean(grad_ms)) * 1e-3
     grad_bytes = 2 * elems * esize
-    achieved = grad_bytes / grad_s / 1e9
-    traffic = measured_traffic(args.workload)
+    achieved = grad_bytes / (float(np.mean(grad_ms)) * 1e-3) / 1e9
+    rec = measured_profile(DOMINANT, wl.name)
+    out = {
+        "wl": wl, "T": T, "V": V, "S": S, "dtype": wl.dtype, "in_place": wl.inplace,
+        "logits_bytes": elems * esize, "ms_per_step": ms_per_step,
+        "value": elems / (ms_per_step * 1e-3),
+        "hbm_frac_step": (3 * elems * esize / (ms_per_step * 1e-3) / 1e9) / HBM_PEAK_GBS,
+        "kernel_ms": {"tok_stats_kernel": float(np.mean(k1_ms)),
+                      "tis_grad_kernel": float(np.mean(grad_ms)),
+                      "step_select+tis_loss_fwd": float(np.mean(mid_ms))},
+        "tok_stats_GBps": elems * esize / (float(np.mean(k1_ms)) * 1e-3) / 1e9,
+        "roofline": {"kernel": DOMINANT, "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": rec.get("hbm_bytes_per_launch") if rec else None,
+                     "algorithmic_bytes_per_launch": grad_bytes},
+        "variants": variants, "copy_ceiling": copy_ceiling, "timing": timing,
+    }
+    del logits, pristine, dlogits
+    torch.cuda.synchronize(dev)
+    torch.cuda.empty_cache()
+    return out
+
+
+def workload_summary(r, cpu):
+    """The per-workload record of the JSON line's ``workloads`` object."""
+    v = r["variants"]
+    return {
+        "T": r["T"], "V": r["V"], "S": r["S"], "dtype": r["dtype"], "in_place": r["in_place"],
+        "ms_per_step": r["ms_per_step"], "logit_elements_per_s": r["value"],
+        "hbm_frac_step": r["hbm_frac_step"], "kernel_ms": r["kernel_ms"],
+        "tis_grad_GBps": r["roofline"]["achieved"], "tis_grad_frac": r["roofline"]["frac"],
+        "tis_grad_traffic": r["roofline"]["traffic"], "tok_stats_GBps": r["tok_stats_GBps"],
+        "grad_skip_zero_rows": v.get("grad_skip_zero_rows"),
+        "stats_only_GBps": (v.get("stats_only") or {}).get("achieved_GBps"),
+        "copy_ceiling_GBps": (r["copy_ceiling"] or {}).get("GBps"),
+        "timing": r["timing"], "cpu_baseline": cpu,
+    }
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the library has no multi-GPU path; "
+              "run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    affinity = len(os.sched_getaffinity(0))
+    threads = args.cpu_threads or min(CPU_SHARE, affinity)
+
+    # every other workload first (in the same process; each one's buffers are
+    # freed before the next), then the headline workload
+    sweep = {}
+    if not args.headline_only:
+        for name in SWEEP_ORDER:
+            if name == args.workload:
+                continue
+            wl = synth.make_workload(name)
+            print(f"[bench] workload {name}: T={wl.T} V={wl.V}", file=sys.stderr, flush=True)
+            r = measure_workload(wl, args, dev, headline=False)
+            cpu = None if args.no_cpu_baseline else cpu_baseline(wl, threads)
+            sweep[name] = workload_summary(r, cpu)
+
+    wl = synth.make_workload(args.workload)
+    print(f"[bench] headline {wl.name}: T={wl.T} V={wl.V}", file=sys.stderr, flush=True)
+    r = measure_workload(wl, args, dev, headline=True)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(wl, threads)
+    if cpu is not None:
+        cpu["affinity_cores"] = affinity
+    workloads = {**sweep, wl.name: workload_summary(r, cpu)}
+    workloads = {k: workloads[k] for k in ("tiny", "vlm7b", "microbatch", "longhorizon", "edge")
+                 if k in workloads}
 
     line = {
         "metric": METRIC,
-        "value": value,
+        "value": r["value"],
         "unit": "logit elements/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": r["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded counter-based generator; shapes of the workload description)",
-        "config": {"workload": f"{wl.name}: {wl.description}", "T": T, "V": V, "S": S,
+        "config": {"workload": f"{wl.name}: {wl.description}", "T": wl.T, "V": wl.V, "S": wl.S,
                    "rho": wl.rho, "eps_low": wl.eps_low, "eps_high": wl.eps_high, "C": wl.C,
-                   "in_place": wl.inplace, "logits_bytes": elems * esize},
-        "hbm_frac_step": (3 * elems * esize / (ms_per_step * 1e-3) / 1e9) / HBM_PEAK_GBS,
-        "kernel_ms": {"tok_stats_kernel": float(np.mean(k1_ms)), "tis_grad_kernel": float(np.mean(grad_ms)),
-                      "step_select+tis_loss_fwd": float(np.mean(mid_ms))},
-        "roofline": {"kernel": DOMINANT, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "algorithmic_bytes_per_launch": grad_bytes},
-        "variants": variants,
-        "copy_ceiling": copy_ceiling,
-        "timing": timing,
+                   "in_place": wl.inplace, "logits_bytes": r["logits_bytes"]},
+        "hbm_frac_step": r["hbm_frac_step"],
+        "kernel_ms": r["kernel_ms"],
+        "roofline": r["roofline"],
+        "variants": r["variants"],
+        "copy_ceiling": r["copy_ceiling"],
+        "timing": r["timing"],
+        "workloads": workloads,
+        "workloads_order": ([k for k in SWEEP_ORDER if k in sweep] + [wl.name]),
     }
-    if not args.no_cpu_baseline:
-        threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
-        line["cpu_baseline"] = cpu_baseline(wl, threads)
+    if cpu is not None:
+        line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
     return 0
 

@@ -21,18 +21,22 @@ def test_traffic_only_for_the_measured_source():
     sys.path.insert(0, ROOT)
     import bench
 
-    for wl in ("vlm7b", "longhorizon"):
-        path = os.path.join(ROOT, "profiles", f"tis_grad_kernel_{wl}_traffic.json")
-        with open(path) as fh:
+    names = [n for n in os.listdir(os.path.join(ROOT, "profiles")) if n.endswith("_traffic.json")]
+    assert names
+    for name in names:
+        with open(os.path.join(ROOT, "profiles", name)) as fh:
             rec = json.load(fh)
-        got = bench.measured_traffic(wl)
+        wl, variant = rec["workload"], rec.get("variant", "")
+        got = bench.measured_profile(rec["kernel"], wl, variant)
         if rec["kernel_source_sha256_16"] == bench.kernel_source_hash():
-            assert got == rec["hbm_bytes_per_launch"]
-            # within 0.1% of the algorithmic bytes: no re-reads
-            assert abs(got / rec["algorithmic_bytes_per_launch"] - 1.0) < 1e-3
+            assert got == rec
+            if not variant:
+                # within 0.1% of the algorithmic bytes: no re-reads
+                assert abs(rec["hbm_bytes_per_launch"] / rec["algorithmic_bytes_per_launch"]
+                           - 1.0) < 1e-3
         else:
             assert got is None
-    assert bench.measured_traffic("tiny") is None
+    assert bench.measured_profile(bench.DOMINANT, "tiny", "no-such-variant") is None
 
 
 def test_cpu_baseline_sample_is_whole_steps():
