@@ -15,8 +15,8 @@
  * - Array arguments are DEVICE pointers unless a comment says otherwise. The
  *   caller owns every buffer; the library allocates no memory and keeps no
  *   state between calls, so concurrent calls on different streams are safe
- *   (the one exception, dart_lmhead_backward, keeps a ROCm BLAS handle per
- *   device and stream and serialises its own calls).
+ *   (dart_tis_loss_fwd_bwd_noalloc, which has a fixed scratch array per
+ *   device, says how its calls may overlap).
  * - Every call is asynchronous on `stream` (0 = the null stream): it checks its
  *   scalar arguments on the host, enqueues its kernels and returns. Outputs are
  *   valid once the stream is synchronised. Device data (target ids in range,
@@ -400,7 +400,7 @@ dart_status_t dart_lmhead_dlogits_ex(const void* hidden, int64_t T, int64_t d, i
  *   dweight = dlogits^T h      [V, d]
  * with dlogits as dart_lmhead_dlogits defines it. The rows are taken
  * chunk_rows at a time: the chunk's dlogits go to the workspace in bfloat16,
- * then two GEMMs of the ROCm BLAS library (bf16 inputs, fp32 accumulation and
+ * then two GEMMs on the matrix cores (bf16 inputs, fp32 accumulation and
  * output) form the chunk's rows of dhidden and add its share to dweight, so the
  * [T, V] dlogits never exist whole.
  *   dhidden:    [T, ld_dh] float32 output, row-major; ld_dh >= d.
@@ -411,14 +411,11 @@ dart_status_t dart_lmhead_dlogits_ex(const void* hidden, int64_t T, int64_t d, i
  *               dart_lmhead_backward_workspace_bytes(min(chunk_rows, T), V)
  *               bytes, 16-byte aligned, owned by the caller; contents on entry
  *               do not matter.
- * The first call on a device and stream creates a BLAS handle for them (the
- * library allocates its own memory then, including a device workspace that two
- * streams must not share); the handle lives until the process ends, and calls
- * into this function are serialised while they enqueue. Errors: as for
- * dart_lmhead_dlogits, INVALID_ARG also for a null output, bad ld_dh/ld_dw,
- * chunk_rows < 1 or a workspace that is too small; UNSUPPORTED for a leading
- * dimension above INT32_MAX (the BLAS library's limit); HIP when the BLAS
- * library reports an error. */
+ * Errors: as for dart_lmhead_dlogits, INVALID_ARG also for a null output, bad
+ * ld_dh/ld_dw, chunk_rows < 1 or a workspace that is too small; UNSUPPORTED
+ * for a leading dimension (ld_h, ld_w, ld_dh, ld_dw, or the dlogits block's
+ * ceil8 of its vocabulary entries) above 2^22 elements, where the tiles'
+ * 32-bit row offsets end; HIP when a launch fails. */
 dart_status_t dart_lmhead_backward(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                    const void* weight, int64_t V, int64_t ld_w,
                                    const int32_t* target, const float* lse, const float* logp,
@@ -466,13 +463,12 @@ enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
  * dhidden are 0. The call gathers the other rows (hidden rows, target, lse,
  * logp, tok_coef) into the workspace, runs the blocked backward over those
  * rows only, and scatters their dhidden rows back; the rows it skipped are set
- * to 0. The result equals the dense call's up to the order of the BLAS
- * library's fp32 sums. Because the GEMM sizes depend on how many rows are
+ * to 0. The result equals the dense call's up to the order of the GEMMs'
+ * fp32 sums. Because the GEMM sizes depend on how many rows are
  * kept, the call copies that count to the host and synchronises the stream
  * once: on a stream that is being captured into a graph it returns
  * DART_ERR_UNSUPPORTED with nothing enqueued. Without this flag the call is
- * asynchronous and can be captured into a HIP graph (the BLAS library's
- * kernels included).
+ * asynchronous and can be captured into a HIP graph.
  *
  *   dhidden:    [T, ld_dh] output, float32, or bfloat16 with
  *               DART_LMHEAD_BF16_GRADS; ld_dh >= d.

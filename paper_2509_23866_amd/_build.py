@@ -19,8 +19,7 @@ HIPCC_FLAGS = [
 
 
 def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
-    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, *SRCS, "-o", out,
-           "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"]
+    cmd = ["hipcc", *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, *SRCS, "-o", out]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -24,13 +24,13 @@
 //                         dz = g (onehot - softmax) in bf16.
 // The backward forms dz block by block (rows x vocabulary entries, the blocked
 // entry point optionally over the rows with a non-zero coefficient only) and
-// adds dh = dz W and dW = dz^T h per block with the ROCm BLAS library.
+// adds dh = dz W and dW = dz^T h per block with lmhead_bwd_gemm_kernel (the
+// same MFMA tile, its operands stored with K as their row index read through
+// LDS transpose loads).
 #include <hip/hip_runtime.h>
 #include <math.h>
-#include <rocblas/rocblas.h>
 #include <stdint.h>
 
-#include <mutex>
 #include <type_traits>
 #include <vector>
 
@@ -559,6 +559,373 @@ lmhead_merge_kernel(const float4* __restrict__ part, const float* __restrict__ z
     logp[t] = sx < ey ? -log1pf(sx / ey) : xy - ln_s;
 }
 
+// ---------------------------------------------------------------------------
+// Backward GEMMs on the matrix cores: C[M, N] (+)= A B with B stored [K][N]
+// (N contiguous), for dh = dz W (A = the dz block read along its rows, K
+// contiguous; B = the block's rows of W) and dW = dz^T h (A = the dz block
+// read down its columns, M contiguous; B = the block's rows of h). The tile,
+// waves, K slices and LDS ring are those of the forward tile; what differs is
+// how an operand stored with K as its row index reaches the MFMA.
+//
+// Such an operand's slice sits in LDS as BK rows of 256 elements (its k rows
+// as they are stored), chunk c (8 elements, 16 bytes) of row k in slot
+// c ^ (4 (k mod 4)). The MFMA wants, in lane l, 8 consecutive k of one column;
+// ds_read_b64_tr_b16 transposes 4 x 16 blocks within each 16 lanes: lane l
+// receives element l % 4 of the 8 bytes that lane 16 (l / 16) + 4 j + (l % 16) / 4
+// loaded, for j = 0..3 (whatever addresses the lanes gave). So lane L of a
+// group points at row k0 + L / 4, columns 4 (L % 4) .. + 3 of its group's 16
+// columns, and receives column L at rows k0 .. k0 + 3; two such reads give the
+// 8 k of one MFMA operand. In one read, the 32 lanes of a half-wave take 4
+// rows x 32 columns; the swizzle puts the 4 rows' chunks in 16 distinct bank
+// quads (gfx950: 64 banks of 4 bytes), so the reads do not conflict.
+// ---------------------------------------------------------------------------
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4* lds_s16x4_ptr;
+
+// Elements of one transposed operand row in LDS (the tile width).
+constexpr int kTw = 256;
+static_assert(LmCfg::BM == kTw && LmCfg::BN == kTw, "transposed rows are one tile wide");
+
+// Slot of chunk c of row k of a transposed operand tile.
+__device__ __forceinline__ int tr_slot(int c, int k) { return c ^ (4 * (k & 3)); }
+
+// acc = this wave's part of C[m0:m0+BM, n0:n0+BN] = A B over k in [0, K).
+// A_KMAJ: A(m, k) = A[m lda + k], else A(m, k) = A[k lda + m]. B(k, n) =
+// B[k ldb + n]. Rows and columns past M, N clamp to the last chunk that
+// exists (their results are not stored); k past K is zero in LDS (also inside
+// a chunk that straddles K), so the stored row padding up to a multiple of 8
+// may hold anything. lda >= ceil8(K) (A_KMAJ) or ceil8(M), ldb >= ceil8(N);
+// rows 16-byte aligned. Layout of acc as in gemm_tile. Ends on a barrier with
+// no loads in flight.
+template <class C, bool A_KMAJ>
+__device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, int64_t lda,
+                                              const uint16_t* __restrict__ B, int64_t ldb,
+                                              int64_t M, int64_t N, int64_t K, int64_t m0,
+                                              int64_t n0, typename C::Smem& sm,
+                                              f32x16 (&acc)[C::TM][C::TN]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    static_assert(C::BK == 64 && C::BM == kTw && C::BN == kTw, "backward tile");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    constexpr int CH = C::CH, BK = C::BK;
+    // transposed operands: one load instruction fills 2 rows of 32 chunks
+    constexpr int TQ = BK / 2 / C::WAVES;  // load instructions per wave and slice
+    static_assert(TQ * 2 * C::WAVES == BK, "transposed rows per wave");
+    const int trow = lane >> 5, tslot = lane & 31;
+    const int64_t nk = (K + BK - 1) / BK;
+
+    // per-lane byte offsets of the loads, fixed for the whole K loop (the
+    // slice's base moves); the last chunk that exists: columns < ceil8(len)
+    auto tr_col = [&](int q, int64_t t0, int64_t len) -> int64_t {
+        const int k = (q * C::WAVES + wave) * 2 + trow;
+        const int64_t col = t0 + 8 * tr_slot(tslot, k);
+        const int64_t last = (len + 7) / 8 * 8 - 8;
+        return (col < last ? col : last) - t0;
+    };
+    uint32_t aoff[A_KMAJ ? C::IA : TQ], boff[TQ];
+    const int lrow = lane / CH, lslot = lane % CH;
+    if constexpr (A_KMAJ) {
+#pragma unroll
+        for (int q = 0; q < C::IA; ++q) {
+            const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+            aoff[q] = (uint32_t)(((min(m0 + r, M - 1) - m0) * lda + (lslot ^ swz<CH>(r)) * 8) * 2);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < TQ; ++q)
+            aoff[q] = (uint32_t)((((q * C::WAVES + wave) * 2 + trow) * lda + tr_col(q, m0, M)) * 2);
+    }
+#pragma unroll
+    for (int q = 0; q < TQ; ++q)
+        boff[q] = (uint32_t)((((q * C::WAVES + wave) * 2 + trow) * ldb + tr_col(q, n0, N)) * 2);
+
+    auto lds_a = [&](int buf, int q) {
+        constexpr int per = A_KMAJ ? C::LROWS * BK : 2 * kTw;  // elements per instruction
+        return &sm.in.a[buf][0][0] + (q * C::WAVES + wave) * per;
+    };
+    auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][0][0] + (q * C::WAVES + wave) * 2 * kTw; };
+
+    auto issue = [&](int64_t kt, int buf) {
+        if ((kt + 1) * BK <= K) {
+            if constexpr (A_KMAJ) {
+                const char* a = reinterpret_cast<const char*>(A + m0 * lda + kt * BK);
+#pragma unroll
+                for (int q = 0; q < C::IA; ++q)
+                    __builtin_amdgcn_global_load_lds(a + aoff[q], lds_a(buf, q), 16, 0, 0);
+            } else {
+                const char* a = reinterpret_cast<const char*>(A + kt * BK * lda + m0);
+#pragma unroll
+                for (int q = 0; q < TQ; ++q)
+                    __builtin_amdgcn_global_load_lds(a + aoff[q], lds_a(buf, q), 16, 0, 0);
+            }
+            const char* b = reinterpret_cast<const char*>(B + kt * BK * ldb + n0);
+#pragma unroll
+            for (int q = 0; q < TQ; ++q)
+                __builtin_amdgcn_global_load_lds(b + boff[q], lds_b(buf, q), 16, 0, 0);
+        } else {
+            // the last, partial slice: k rows clamped to K - 1, k chunks to
+            // the last that exists (zeroed after landing)
+            if constexpr (A_KMAJ) {
+#pragma unroll
+                for (int q = 0; q < C::IA; ++q) {
+                    const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
+                    const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, (K + 7) / 8 * 8 - 8);
+                    __builtin_amdgcn_global_load_lds(A + min(m0 + r, M - 1) * lda + k,
+                                                     lds_a(buf, q), 16, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < TQ; ++q) {
+                    const int64_t k = min(kt * BK + (q * C::WAVES + wave) * 2 + trow, K - 1);
+                    __builtin_amdgcn_global_load_lds(A + k * lda + m0 + tr_col(q, m0, M),
+                                                     lds_a(buf, q), 16, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int64_t k = min(kt * BK + (q * C::WAVES + wave) * 2 + trow, K - 1);
+                __builtin_amdgcn_global_load_lds(B + k * ldb + n0 + tr_col(q, n0, N),
+                                                 lds_b(buf, q), 16, 0, 0);
+            }
+        }
+    };
+    // the partial last slice: k >= K set to 0 in both operands
+    auto zero_tail = [&](int64_t kt, int buf) {
+        const int kv = (int)(K - kt * BK);  // valid k in this slice, 1 .. BK-1
+        uint16_t* a = &sm.in.a[buf][0][0];
+        uint16_t* b = &sm.in.b[buf][0][0];
+        for (int e = tid; e < BK * kTw; e += C::THREADS) {
+            const int k = e / kTw;  // transposed layouts: row k
+            if (k >= kv) {
+                b[e] = 0;
+                if constexpr (!A_KMAJ) a[e] = 0;
+            }
+            if constexpr (A_KMAJ) {
+                // [BM][BK] rows with swizzled chunks: element e is row e / BK,
+                // slot (e % BK) / 8, holding chunk slot ^ swz(row)
+                const int r = e / BK, s = (e % BK) / 8;
+                const int kk = ((s ^ swz<CH>(r)) * 8) + (e % 8);
+                if (kk >= kv) a[e] = 0;
+            }
+        }
+    };
+
+    // MFMA operand offsets. A (K-major): as gemm_tile. Transposed: lane l
+    // points at row ks*16 + 8 (l / 32) + 4 h + (l / 4) % 4 and columns
+    // mb + 16 ((l / 16) % 2) + 4 (l % 4) of its 32-column block mb (a multiple
+    // of 32, so the chunk is (mb / 8) | ((l / 16) % 2) * 2 | (l % 4) / 2).
+    const int kq = (lane >> 2) & 3;
+    const int tr_lane_row = 8 * (lane >> 5) + kq;
+    const int tr_delta = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+    auto tr_off = [&](int mb) -> uint32_t {
+        const int slot = ((mb / 8) ^ (4 * kq)) | tr_delta;
+        return (uint32_t)(tr_lane_row * kTw * 2 + slot * 16 + 8 * (lane & 1));
+    };
+    uint32_t rda[A_KMAJ ? C::KSTEPS : C::TM], rdb[C::TN];
+    if constexpr (A_KMAJ) {
+#pragma unroll
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            const int c = ks * 2 + (lane >> 5), ra = wr + (lane & 31);
+            rda[ks] = (uint32_t)(ra * BK + (c ^ swz<CH>(ra)) * 8) * 2;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i) rda[i] = tr_off(wr + i * C::RS);
+    }
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) rdb[j] = tr_off(wc + j * 32);
+
+    auto tr_pair = [&](const char* base, uint32_t off, int ks) -> bf16x8 {
+        const int k0 = ks * 16 * kTw * 2;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4_ptr)(base + off + k0));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4_ptr)(base + off + k0 + 4 * kTw * 2));
+        typedef short s16x8 __attribute__((ext_vector_type(8)));
+        const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, v);
+    };
+    bf16x8 af[2][C::TM], bfr[2][C::TN];
+    auto read_step = [&](auto bufc, int ks, int set) {
+        constexpr int buf = decltype(bufc)::value;
+        const char* ba = reinterpret_cast<const char*>(&sm.in.a[buf][0][0]);
+        const char* bb = reinterpret_cast<const char*>(&sm.in.b[buf][0][0]);
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i) {
+            if constexpr (A_KMAJ)
+                af[set][i] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4*>(ba + rda[ks] + i * C::RS * BK * 2));
+            else
+                af[set][i] = tr_pair(ba, rda[i], ks);
+        }
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j) bfr[set][j] = tr_pair(bb, rdb[j], ks);
+    };
+    auto mfmas = [&](int set) {
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][i], bfr[set][j],
+                                                                    acc[i][j], 0, 0, 0);
+    };
+    auto slice = [&](auto bufc, int64_t kt) {
+        constexpr int buf = decltype(bufc)::value;
+        wait_vmcnt<0>();
+        lds_ring_barrier();
+        if ((K % BK) && kt == nk - 1) {
+            zero_tail(kt, buf);
+            lds_ring_barrier();
+        }
+        if (kt + 1 < nk) issue(kt + 1, buf ^ 1);
+        read_step(bufc, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            const int cs = ks & 1;
+            if (ks < C::KSTEPS - 1) read_step(bufc, ks + 1, cs ^ 1);
+            mfmas(cs);
+        }
+    };
+    if (nk > 0) issue(0, 0);
+    for (int64_t kt = 0; kt < nk; kt += 2) {
+        slice(std::integral_constant<int, 0>{}, kt);
+        if (kt + 1 < nk) slice(std::integral_constant<int, 1>{}, kt + 1);
+    }
+    __syncthreads();
+#else
+    (void)A, (void)lda, (void)B, (void)ldb, (void)M, (void)N, (void)K, (void)m0, (void)n0;
+    (void)sm, (void)acc;
+#endif
+}
+
+// One GEMM of the backward: C[M, N] (+)= A B with gemm_tile_bwd's operands,
+// written to out [M, ldc] (fp32, or bf16 bits rounded to nearest even); vec:
+// out 16-byte aligned and ldc a multiple of 16 bytes' worth of elements.
+struct BwdGemm {
+    const uint16_t* A;
+    int64_t lda;
+    const uint16_t* B;
+    int64_t ldb;
+    int64_t M, N, K;
+    void* out;
+    int64_t ldc;
+    int vec;
+    int64_t nmt, nnt;  // tiles
+};
+
+// Output modes of a backward GEMM: fp32 written, fp32 added to, bf16 written.
+enum BwdOut { kOutF32 = 0, kOutF32Acc = 1, kOutBf16 = 2 };
+
+// Logical tile of the workgroup with index b among the nb workgroups of one
+// GEMM whose first workgroup sits on XCD 0 (workgroup i of a launch runs on
+// XCD i % 8): each XCD takes a contiguous run of logical tiles, column tile
+// fastest, so the tiles that share a row block of A run together on one XCD
+// and read it from that XCD's L2.
+__device__ __forceinline__ void tile_of_block_nfast(int64_t b, int64_t nmt, int64_t nnt,
+                                                    int64_t& mt, int64_t& nt) {
+    const int64_t nb = nmt * nnt, q = nb / 8, rr = nb % 8;
+    const int64_t x = b % 8, sl = b / 8;
+    const int64_t lg = x * q + min(x, rr) + sl;
+    nt = lg % nnt;
+    mt = lg / nnt;
+}
+
+// Tile b of GEMM g: the MFMA tile, then the fp32 result through LDS, 128 rows
+// at a time, so that each row leaves as 16-byte vectors (vec), else one
+// element at a time.
+template <class C, bool A_KMAJ, int OUT>
+__device__ __forceinline__ void bwd_gemm_tile(const BwdGemm& g, int64_t b, typename C::Smem& sm) {
+    using OutT = typename std::conditional<OUT == kOutBf16, uint16_t, float>::type;
+    constexpr bool ACC = OUT == kOutF32Acc;
+    int64_t mt, nt;
+    tile_of_block_nfast(b, g.nmt, g.nnt, mt, nt);
+    const int64_t m0 = mt * C::BM, n0 = nt * C::BN;
+    const int64_t M = g.M, N = g.N;
+    f32x16 acc[C::TM][C::TN];
+    gemm_tile_bwd<C, A_KMAJ>(g.A, g.lda, g.B, g.ldb, M, N, g.K, m0, n0, sm, acc);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
+    constexpr bool F32 = OUT != kOutBf16;
+    constexpr int EPV = F32 ? 4 : 8;  // elements per 16-byte vector
+    constexpr int VPR = C::BN / EPV;  // vectors per tile row
+    OutT* out = static_cast<OutT*>(g.out);
+#pragma unroll
+    for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
+        if (e0) __syncthreads();
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
+                    if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
+                }
+        __syncthreads();
+        for (int e = tid; e < C::EPI * VPR; e += C::THREADS) {
+            const int r = e / VPR, cv = e % VPR;
+            const int64_t m = m0 + e0 + r, n = n0 + (int64_t)cv * EPV;
+            if (m >= M || n >= N) continue;
+            const float* src = &sm.c[r][cv * EPV];
+            OutT* dst = out + m * g.ldc + n;
+            if (g.vec && n + EPV <= N) {
+                if constexpr (F32) {
+                    float4 x = *reinterpret_cast<const float4*>(src);
+                    if constexpr (ACC) {
+                        const float4 o = *reinterpret_cast<const float4*>(dst);
+                        x.x += o.x, x.y += o.y, x.z += o.z, x.w += o.w;
+                    }
+                    *reinterpret_cast<float4*>(dst) = x;
+                } else {
+                    const float4 lo = *reinterpret_cast<const float4*>(src);
+                    const float4 hi = *reinterpret_cast<const float4*>(src + 4);
+                    u32x4 pk;
+                    pk.x = pack_bf16x2(lo.x, lo.y);
+                    pk.y = pack_bf16x2(lo.z, lo.w);
+                    pk.z = pack_bf16x2(hi.x, hi.y);
+                    pk.w = pack_bf16x2(hi.z, hi.w);
+                    *reinterpret_cast<u32x4*>(dst) = pk;
+                }
+            } else {
+                for (int q = 0; q < EPV && n + q < N; ++q) {
+                    if constexpr (F32)
+                        dst[q] = ACC ? dst[q] + src[q] : src[q];
+                    else
+                        dst[q] = bf16_bits(src[q]);
+                }
+            }
+        }
+    }
+}
+
+// The two GEMMs of one backward block in one launch: dh = dz W (dz read
+// along its rows) on the first n_dh workgroups (a multiple of 8; those past
+// dh's tiles return at once), dW = dz^T h (dz read down its columns) on the
+// rest. dh has few tiles with a long sum (a block's rows x d) and dW many
+// with a short one, so dW's tiles fill the compute units that dh leaves
+// free, and both start from the dz block just written.
+template <class C, int DH_OUT, int DW_OUT>
+__global__ void __launch_bounds__(C::THREADS)
+lmhead_bwd_gemms_kernel(BwdGemm dh, BwdGemm dw, int64_t n_dh) {
+    __shared__ typename C::Smem sm;
+    const int64_t b = blockIdx.x;
+    if (b < n_dh) {
+        if (b < dh.nmt * dh.nnt) bwd_gemm_tile<C, true, DH_OUT>(dh, b, sm);
+    } else {
+        bwd_gemm_tile<C, false, DW_OUT>(dw, b - n_dh, sm);
+    }
+}
+
 int64_t vocab_tiles(int64_t V) { return (V + LmCfg::BN - 1) / LmCfg::BN; }
 
 // Rows whose coefficient is not 0, in increasing order: map[0 .. n) and
@@ -676,38 +1043,6 @@ dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, in
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
                        target, lse, logp, coef, scale, out, ld_out, vbase, nmt, nvt);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
-}
-
-// One rocBLAS handle per device and stream, created on the first call on that
-// stream and kept until the process ends. A handle owns a device workspace that
-// some of the library's kernels use, so two streams never share one: their
-// GEMMs may run at the same time. Calls are serialised by the mutex (the
-// lookup, and the enqueueing on one handle).
-std::mutex g_blas_mu;
-struct BlasEntry {
-    int dev;
-    hipStream_t stream;
-    rocblas_handle handle;
-};
-std::vector<BlasEntry> g_blas;
-
-// The handle of (dev, stream), bound to that stream; dev must be current (a
-// handle belongs to the device current when it is created). The caller holds
-// g_blas_mu.
-rocblas_handle blas_handle(int dev, hipStream_t stream) {
-    for (const BlasEntry& e : g_blas)
-        if (e.dev == dev && e.stream == stream)
-            // the stream may be a new one at the address of a destroyed one
-            return rocblas_set_stream(e.handle, stream) == rocblas_status_success ? e.handle
-                                                                                 : nullptr;
-    rocblas_handle h = nullptr;
-    if (rocblas_create_handle(&h) != rocblas_status_success) return nullptr;
-    if (rocblas_set_stream(h, stream) != rocblas_status_success) {
-        (void)rocblas_destroy_handle(h);
-        return nullptr;
-    }
-    g_blas.push_back({dev, stream, h});
-    return h;
 }
 
 }  // namespace
@@ -861,34 +1196,60 @@ struct Grad {
     }
 };
 
-// rocBLAS is column-major: a row-major [R, C] matrix with row stride ld is
-// its column-major [C, R] transpose with leading dimension ld. Both products
-// take bf16 inputs and accumulate in fp32; accumulate adds to the output.
-// dh[rows, d] (+)= dz[rows, K] W[K, d]   <=>   dh^T = W^T dz^T
-bool gemm_dh(rocblas_handle blas, const uint16_t* dz, int64_t ld_dz, int64_t rows, int64_t K,
-             const uint16_t* w, int64_t ld_w, int64_t d, bool accumulate, const Grad& out) {
-    const float one = 1.f, zero = 0.f;
-    const rocblas_datatype ot = out.bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
-    return rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)d,
-                           (rocblas_int)rows, (rocblas_int)K, &one, w, rocblas_datatype_bf16_r,
-                           (rocblas_int)ld_w, dz, rocblas_datatype_bf16_r, (rocblas_int)ld_dz,
-                           accumulate ? &one : &zero, out.p, ot, (rocblas_int)out.ld, out.p, ot,
-                           (rocblas_int)out.ld, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
-                           0, 0) == rocblas_status_success;
+// The GEMM description of one backward output (out.p at the block's first
+// row); mode: kOutF32, kOutF32Acc or kOutBf16.
+BwdGemm make_bwd_gemm(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb, int64_t M,
+                      int64_t N, int64_t K, const Grad& out) {
+    BwdGemm g;
+    g.A = A, g.lda = lda, g.B = B, g.ldb = ldb, g.M = M, g.N = N, g.K = K;
+    g.out = out.p, g.ldc = out.ld;
+    const size_t esz = out.bf16 ? 2 : 4;
+    g.vec = reinterpret_cast<uintptr_t>(out.p) % 16 == 0 && (out.ld * esz) % 16 == 0;
+    g.nmt = (M + LmCfg::BM - 1) / LmCfg::BM;
+    g.nnt = (N + LmCfg::BN - 1) / LmCfg::BN;
+    return g;
 }
 
-// dW[cols, d] (+)= dz[K, cols]^T h[K, d]   <=>   dW^T = h^T dz
-bool gemm_dw(rocblas_handle blas, const uint16_t* h, int64_t ld_h, int64_t K, const uint16_t* dz,
-             int64_t ld_dz, int64_t cols, int64_t d, bool accumulate, const Grad& out) {
-    const float one = 1.f, zero = 0.f;
-    const rocblas_datatype ot = out.bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
-    return rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
-                           (rocblas_int)d, (rocblas_int)cols, (rocblas_int)K, &one, h,
-                           rocblas_datatype_bf16_r, (rocblas_int)ld_h, dz, rocblas_datatype_bf16_r,
-                           (rocblas_int)ld_dz, accumulate ? &one : &zero, out.p, ot,
-                           (rocblas_int)out.ld, out.p, ot, (rocblas_int)out.ld,
-                           rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0,
-                           0) == rocblas_status_success;
+int out_mode(const Grad& out, bool accumulate) {
+    return out.bf16 ? kOutBf16 : accumulate ? kOutF32Acc : kOutF32;
+}
+
+template <int DH, int DW>
+void launch_bwd_gemms_t(const BwdGemm& dh, const BwdGemm& dw, int64_t n_dh, int64_t blocks,
+                        hipStream_t stream) {
+    hipLaunchKernelGGL((lmhead_bwd_gemms_kernel<LmCfg, DH, DW>), dim3((unsigned)blocks),
+                       dim3(LmCfg::THREADS), 0, stream, dh, dw, n_dh);
+}
+
+template <int DH>
+void launch_bwd_gemms_dw(int dw_mode, const BwdGemm& dh, const BwdGemm& dw, int64_t n_dh,
+                         int64_t blocks, hipStream_t stream) {
+    if (dw_mode == kOutF32) launch_bwd_gemms_t<DH, kOutF32>(dh, dw, n_dh, blocks, stream);
+    else if (dw_mode == kOutF32Acc) launch_bwd_gemms_t<DH, kOutF32Acc>(dh, dw, n_dh, blocks, stream);
+    else launch_bwd_gemms_t<DH, kOutBf16>(dh, dw, n_dh, blocks, stream);
+}
+
+// One block's dh[rows, d] (+)= dz[rows, cols] W[cols, d] and
+// dW[cols, d] (+)= dz[rows, cols]^T h[rows, d], in one launch. A bf16 output
+// is never added to (sums over blocks go through fp32).
+dart_status_t launch_bwd_gemms(const uint16_t* dz, int64_t ld_dz, int64_t rows, int64_t cols,
+                               const uint16_t* w, int64_t ld_w, const uint16_t* h, int64_t ld_h,
+                               int64_t d, const Grad& dh_out, bool dh_acc, const Grad& dw_out,
+                               bool dw_acc, hipStream_t stream) {
+    if ((dh_out.bf16 && dh_acc) || (dw_out.bf16 && dw_acc)) return DART_ERR_INVALID_ARG;
+    if (ld_dz > kMaxLd || ld_w > kMaxLd || ld_h > kMaxLd || dh_out.ld > kMaxLd ||
+        dw_out.ld > kMaxLd)
+        return DART_ERR_UNSUPPORTED;
+    const BwdGemm dh = make_bwd_gemm(dz, ld_dz, w, ld_w, rows, d, cols, dh_out);
+    const BwdGemm dw = make_bwd_gemm(dz, ld_dz, h, ld_h, cols, d, rows, dw_out);
+    const int64_t n_dh = (dh.nmt * dh.nnt + 7) / 8 * 8;
+    const int64_t blocks = n_dh + dw.nmt * dw.nnt;
+    if (!grid_fits(blocks, LmCfg::THREADS)) return DART_ERR_UNSUPPORTED;
+    const int dhm = out_mode(dh_out, dh_acc), dwm = out_mode(dw_out, dw_acc);
+    if (dhm == kOutF32) launch_bwd_gemms_dw<kOutF32>(dwm, dh, dw, n_dh, blocks, stream);
+    else if (dhm == kOutF32Acc) launch_bwd_gemms_dw<kOutF32Acc>(dwm, dh, dw, n_dh, blocks, stream);
+    else launch_bwd_gemms_dw<kOutBf16>(dwm, dh, dw, n_dh, blocks, stream);
+    return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
 void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& dst,
@@ -905,7 +1266,7 @@ void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& ds
 // or, for a bf16 output that more than one block adds to, into acc_h ([T, d])
 // or acc_w ([V, d]) and is rounded to bf16 once at the end; an output that
 // one block writes is that GEMM's fp32 result rounded once.
-dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, int64_t d,
+dart_status_t backward_core(const uint16_t* h, int64_t T, int64_t d,
                             int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
                             const int32_t* target, const float* lse, const float* logp,
                             const float* coef, float scale, const Grad& dh, const Grad& dw,
@@ -928,11 +1289,11 @@ dart_status_t backward_core(rocblas_handle blas, const uint16_t* h, int64_t T, i
                 launch_dlogits(hr, rows, d, ld_h, wc, cols, ld_w, target + r0, lse + r0,
                                logp + r0, coef + r0, scale, dz, ld_dz, c0, stream);
             if (st != DART_OK) return st;
-            if (!gemm_dh(blas, dz, ld_dz, rows, cols, wc, ld_w, d, c0 > 0,
-                         Grad{sum_h.row(r0), sum_h.ld, sum_h.bf16}) ||
-                !gemm_dw(blas, hr, ld_h, rows, dz, ld_dz, cols, d, r0 > 0,
-                         Grad{sum_w.row(c0), sum_w.ld, sum_w.bf16}))
-                return DART_ERR_HIP;
+            const dart_status_t sg = launch_bwd_gemms(
+                dz, ld_dz, rows, cols, wc, ld_w, hr, ld_h, d,
+                Grad{sum_h.row(r0), sum_h.ld, sum_h.bf16}, c0 > 0,
+                Grad{sum_w.row(c0), sum_w.ld, sum_w.bf16}, r0 > 0, stream);
+            if (sg != DART_OK) return sg;
         }
     }
     if (via_h) launch_to_bf16(acc_h, T, d, dh, stream);
@@ -975,9 +1336,9 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     if (ld_dh < d || ld_dw < d || chunk_rows < 1 || chunk_cols < 1 ||
         (flags & ~kBackwardFlags) || reinterpret_cast<uintptr_t>(workspace) % 16)
         return DART_ERR_INVALID_ARG;
-    // the BLAS library takes 32-bit sizes and leading dimensions
-    const int64_t kI32 = 0x7FFFFFFFll;
-    if (ld_h > kI32 || ld_w > kI32 || ld_dh > kI32 || ld_dw > kI32) return DART_ERR_UNSUPPORTED;
+    // the MFMA tiles address rows by 32-bit offsets from a tile's first row
+    if (ld_h > kMaxLd || ld_w > kMaxLd || ld_dh > kMaxLd || ld_dw > kMaxLd)
+        return DART_ERR_UNSUPPORTED;
     const BackwardPlan P = plan_backward(T, d, V, chunk_rows, chunk_cols, flags);
     if (P.total == 0) return DART_ERR_UNSUPPORTED;
     if (workspace_bytes < P.total) return DART_ERR_INVALID_ARG;
@@ -988,14 +1349,6 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;
 
-    const int dev = stream_device(stream);
-    if (dev < 0) return DART_ERR_HIP;
-    // the stream's device is current while the BLAS library works
-    DeviceGuard on_dev(dev);
-    if (!on_dev.ok) return DART_ERR_HIP;
-    std::lock_guard<std::mutex> lock(g_blas_mu);
-    rocblas_handle blas = blas_handle(dev, stream);
-    if (!blas) return DART_ERR_HIP;
     const uint16_t* h = static_cast<const uint16_t*>(hidden);
     const uint16_t* w = static_cast<const uint16_t*>(weight);
     char* ws = static_cast<char*>(workspace);
@@ -1004,7 +1357,7 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     float* acc_h = P.acc_h ? reinterpret_cast<float*>(ws + P.acch) : nullptr;
     const Grad dh{dhidden, ld_dh, P.bf16}, dw{dweight, ld_dw, P.bf16};
     if (!P.skip)
-        return backward_core(blas, h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef,
+        return backward_core(h, T, d, ld_h, w, V, ld_w, target, lse, logp, tok_coef,
                              inv_temp, dh, dw, P.rows, P.cols, dz, acc_h, acc_w, stream);
 
     // rows with a zero coefficient have dz = 0: they add nothing to dW and
@@ -1040,7 +1393,7 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
         return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
     }
     const dart_status_t st =
-        backward_core(blas, h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c, inv_temp,
+        backward_core(h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c, inv_temp,
                       Grad{dh_c, d, false}, dw, P.rows, P.cols, dz, nullptr, acc_w, stream);
     if (st != DART_OK) return st;
     const unsigned nb = (unsigned)(n < kRowBlocks ? n : kRowBlocks);

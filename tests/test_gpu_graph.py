@@ -133,7 +133,7 @@ def test_synchronising_modes_refused_under_capture(monkeypatch):
 @pytest.mark.parametrize("rows,cols,bf16", [(256, 300, False), (100, 128, True)])
 def test_lmhead_step_graph_replays_match_eager(rows, cols, bf16):
     """The fused LM-head step (statistics, selection, loss, blocked backward
-    with its library GEMMs) captured once: every replay gives the eager bits,
+    with its GEMMs) captured once: every replay gives the eager bits,
     with eager work and synchronisations between replays."""
     import torch
 

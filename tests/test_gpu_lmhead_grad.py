@@ -39,7 +39,7 @@ from tests import _harness as H
 pytestmark = pytest.mark.gpu
 
 U = 2.0 ** -8   # unit roundoff of bf16
-A = 2.0 ** -13  # fp32 summation by the BLAS library, relative to the sum of |terms|
+A = 2.0 ** -13  # fp32 summation in the GEMMs, relative to the sum of |terms|
 
 
 def _dev_bf16(bits, pad=0):
@@ -573,7 +573,7 @@ def test_lmhead_backward_blockings_agree():
     for bf, fp in zip(bfs, outs):
         for xb, xf, (_, bound) in zip(bf, fp, refs):
             # one rounding of the fp32 sum, up to the fp32 summation order of
-            # the library's kernels for bf16 and fp32 outputs
+            # the GEMM kernels for bf16 and fp32 outputs
             a = xb.float().cpu().numpy().astype(np.float64)
             b = xf.cpu().numpy().astype(np.float64)
             assert np.all(np.abs(a - b) <= U * np.abs(b) + A * bound + 1e-37)

@@ -77,11 +77,11 @@ def _lm_run(p, stream, rows, cols, flags):
 
 
 def test_lmhead_two_streams_interleaved():
-    """The LM-head statistics and blocked backward (library GEMMs included) of
-    two problems interleaved on two streams, each bit-identical to its own run
-    alone: the streams use separate BLAS handles, so no library workspace is
-    shared. One problem has few rows against a long vocabulary (a small GEMM
-    output over a long sum, where the library may split the sum)."""
+    """The LM-head statistics and blocked backward (its GEMMs included) of two
+    problems interleaved on two streams, each bit-identical to its own run
+    alone: the library keeps no state between calls, so nothing is shared. One
+    problem has few rows against a long vocabulary (a small GEMM output over a
+    long sum)."""
     import torch
 
     pa = _lm_problem(3, 64, 256, 20000)
