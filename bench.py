@@ -51,6 +51,9 @@ def parse_args():
     ap.add_argument("--headline-only", action="store_true",
                     help="measure only --workload, not the other workloads first "
                          "(profiling runs of the headline step)")
+    ap.add_argument("--skip-rows-step", action="store_true",
+                    help="the step's gradient pass skips reading rows with a zero coefficient "
+                         "(profiling runs of the read-skipping gradient; not the headline)")
     ap.add_argument("--no-lmhead", action="store_true",
                     help="leave the fused LM-head variant out")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -517,7 +520,8 @@ def measure_workload(wl, args, dev, headline):
                                loss, coef, stats, stream=s, workspace=workspace)
         if ev:
             ev[2].record(s)
-        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=s)
+        dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=s,
+                           skip_zero_rows=args.skip_rows_step)
         if ev:
             ev[3].record(s)
 
@@ -652,9 +656,11 @@ def measure_workload(wl, args, dev, headline):
     grad_bytes = 2 * elems * esize
     achieved = grad_bytes / (float(np.mean(grad_ms)) * 1e-3) / 1e9
     rec = measured_profile(DOMINANT, wl.name)
+    zero_frac = float((coef == 0).float().mean().item())
     out = {
         "wl": wl, "T": T, "V": V, "S": S, "dtype": wl.dtype, "in_place": wl.inplace,
         "logits_bytes": elems * esize, "ms_per_step": ms_per_step,
+        "zero_row_fraction": zero_frac,
         "value": elems / (ms_per_step * 1e-3),
         "hbm_frac_step": (3 * elems * esize / (ms_per_step * 1e-3) / 1e9) / HBM_PEAK_GBS,
         "kernel_ms": {"tok_stats_kernel": float(np.mean(k1_ms)),
@@ -744,8 +750,10 @@ def main():
         "data": "synthetic (seeded counter-based generator; shapes of the workload description)",
         "config": {"workload": f"{wl.name}: {wl.description}", "T": wl.T, "V": wl.V, "S": wl.S,
                    "rho": wl.rho, "eps_low": wl.eps_low, "eps_high": wl.eps_high, "C": wl.C,
-                   "in_place": wl.inplace, "logits_bytes": r["logits_bytes"]},
+                   "in_place": wl.inplace, "logits_bytes": r["logits_bytes"],
+                   "grad_skip_zero_rows_step": bool(args.skip_rows_step)},
         "hbm_frac_step": r["hbm_frac_step"],
+        "zero_row_fraction": r["zero_row_fraction"],
         "kernel_ms": r["kernel_ms"],
         "roofline": r["roofline"],
         "variants": r["variants"],
