@@ -51,6 +51,17 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// A buffer resource over [base, base + bytes) (bytes capped at 2^32 - 1): raw
+// loads past its end return zero. Dword 3 selects 32-bit data, untyped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* base, int64_t bytes) {
+    const uint32_t n = bytes > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+
+__device__ __forceinline__ __attribute__((address_space(3))) void* lds_ptr(void* p) {
+    return (__attribute__((address_space(3))) void*)p;
+}
+
 // Workgroup barrier of the LDS ring: the caller has waited for its own loads
 // into LDS (vmcnt); lgkmcnt(0) retires its LDS reads; the empty asm
 // statements keep the compiler from moving memory accesses across it. Unlike
@@ -154,8 +165,8 @@ __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
 
 // acc = this wave's part of the tile A[m0:m0+BM, :] B[n0:n0+BN, :]^T (A [M, K]
 // and B [N, K] row-major bf16, rows 16-byte aligned, K % 8 == 0). Rows past M
-// or N read clamped copies of the last row (their results are not used); K
-// past the end is zeroed in LDS. Layout of acc[i][j]: value v of lane l is
+// or N read as zero (their results are not used); K past the end is zeroed in
+// LDS. Layout of acc[i][j]: value v of lane l is
 // tile row (wave / WN) * 32 + i * RS + (v/4)*8 + (l/32)*4 + v%4, column
 // (wave % WN) * BN/WN + j*32 + l%32. Ends on a barrier with no loads in
 // flight, so the caller may reuse the LDS.
@@ -178,54 +189,42 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
 
     // One load instruction fills LROWS rows x CH slots (1 KB): lane l writes
     // slot l % CH of row r0 + l / CH, i.e. chunk (l % CH) ^ swz(row) of that
-    // row. Each lane's source offsets within the tile are fixed for the whole
-    // K loop (rows past M or N clamped to the last row), so a full slice's
-    // load is a uniform base plus a per-lane 32-bit offset.
+    // row. The loads are buffer loads into LDS: each operand's tile rows are a
+    // buffer resource whose range ends at the matrix's last element, so rows
+    // past M or N read as zero (their results are not used). A lane's byte
+    // offset within its instruction's rows is the same for every instruction
+    // and slice (the swizzle repeats every 16 rows, and the rows of one
+    // instruction of every wave together are a multiple of that), so one VGPR
+    // serves all of an operand's loads; the instruction's rows and the slice
+    // enter as a scalar offset.
     constexpr int CH = C::CH, BK = C::BK;
     const int lrow = lane / CH, lslot = lane % CH;
-    const char* a_tile = reinterpret_cast<const char*>(A + m0 * lda);
-    const char* b_tile = reinterpret_cast<const char*>(B + n0 * ldb);
-    uint32_t aoff[C::IA], boff[C::IB];
-#pragma unroll
-    for (int q = 0; q < C::IA; ++q) {
-        const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-        aoff[q] = (uint32_t)(((min(m0 + r, M - 1) - m0) * lda + (lslot ^ swz<CH>(r)) * 8) * 2);
-    }
-#pragma unroll
-    for (int q = 0; q < C::IB; ++q) {
-        const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-        boff[q] = (uint32_t)(((min(n0 + r, N - 1) - n0) * ldb + (lslot ^ swz<CH>(r)) * 8) * 2);
-    }
+    static_assert((C::WAVES * C::LROWS) % (16 / CH * CH) == 0, "swizzle period");
+    const int r_lane = wave * C::LROWS + lrow;  // row of the lane in instruction 0
+    const uint32_t voff_a = (uint32_t)((r_lane * lda + (lslot ^ swz<CH>(r_lane)) * 8) * 2);
+    const uint32_t voff_b = (uint32_t)((r_lane * ldb + (lslot ^ swz<CH>(r_lane)) * 8) * 2);
+    const uint32_t qstride_a = (uint32_t)(C::WAVES * C::LROWS * lda * 2);
+    const uint32_t qstride_b = (uint32_t)(C::WAVES * C::LROWS * ldb * 2);
+    const __amdgpu_buffer_rsrc_t rsrc_a = tile_rsrc(A + m0 * lda, (M - m0) * lda * 2);
+    const __amdgpu_buffer_rsrc_t rsrc_b = tile_rsrc(B + n0 * ldb, (N - n0) * ldb * 2);
     auto lds_a = [&](int buf, int q) { return &sm.in.a[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
     auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
     const int64_t nk = (K + BK - 1) / BK;
-    // slice kt into buffer buf; a slice that ends past K clamps each chunk's
-    // column to K - 8 (those chunks are zeroed after landing)
+    // slice kt into buffer buf; a slice that ends past K reads chunks past K
+    // (in the row padding, the next row or, at the end, as zero) that are
+    // zeroed after landing
     auto issue = [&](int64_t kt, int buf) {
-        if ((kt + 1) * BK <= K) {
-            const int64_t kb = kt * BK * 2;
+        const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
-            for (int q = 0; q < C::IA; ++q)
-                __builtin_amdgcn_global_load_lds(a_tile + kb + aoff[q], lds_a(buf, q), 16, 0, 0);
+        for (int q = 0; q < C::IA; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_a, lds_ptr(lds_a(buf, q)), 16, voff_a,
+                                                    kb + q * qstride_a, 0, 0);
 #pragma unroll
-            for (int q = 0; q < C::IB; ++q)
-                __builtin_amdgcn_global_load_lds(b_tile + kb + boff[q], lds_b(buf, q), 16, 0, 0);
-        } else {
-#pragma unroll
-            for (int q = 0; q < C::IA; ++q) {
-                const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-                const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, K - 8);
-                __builtin_amdgcn_global_load_lds(A + min(m0 + r, M - 1) * lda + k, lds_a(buf, q), 16, 0, 0);
-            }
-#pragma unroll
-            for (int q = 0; q < C::IB; ++q) {
-                const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-                const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, K - 8);
-                __builtin_amdgcn_global_load_lds(B + min(n0 + r, N - 1) * ldb + k, lds_b(buf, q), 16, 0, 0);
-            }
-        }
+        for (int q = 0; q < C::IB; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_b, lds_ptr(lds_b(buf, q)), 16, voff_b,
+                                                    kb + q * qstride_b, 0, 0);
     };
-    // a partial last slice: zero the chunks past K (they hold clamped copies)
+    // a partial last slice: zero the chunks past K
     auto zero_tail = [&](int64_t kt, int buf) {
         const u32x4 z = {0u, 0u, 0u, 0u};
         for (int e = tid; e < (C::BM + C::BN) * CH; e += C::THREADS) {
@@ -302,11 +301,16 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
             }
         }
     };
+    // the loop body has no condition on the accumulators: an odd last slice
+    // runs after it (a conditional second slice in the body made the compiler
+    // copy every accumulator at the join)
     issue(0, 0);
-    for (int64_t kt = 0; kt < nk; kt += 2) {
+    int64_t kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
         slice(std::integral_constant<int, 0>{}, kt);
-        if (kt + 1 < nk) slice(std::integral_constant<int, 1>{}, kt + 1);
+        slice(std::integral_constant<int, 1>{}, kt + 1);
     }
+    if (kt < nk) slice(std::integral_constant<int, 0>{}, kt);
     __syncthreads();
 #else
     (void)A, (void)M, (void)lda, (void)B, (void)N, (void)ldb, (void)K, (void)m0, (void)n0;
@@ -592,12 +596,12 @@ __device__ __forceinline__ int tr_slot(int c, int k) { return c ^ (4 * (k & 3));
 
 // acc = this wave's part of C[m0:m0+BM, n0:n0+BN] = A B over k in [0, K).
 // A_KMAJ: A(m, k) = A[m lda + k], else A(m, k) = A[k lda + m]. B(k, n) =
-// B[k ldb + n]. Rows and columns past M, N clamp to the last chunk that
-// exists (their results are not stored); k past K is zero in LDS (also inside
-// a chunk that straddles K), so the stored row padding up to a multiple of 8
-// may hold anything. lda >= ceil8(K) (A_KMAJ) or ceil8(M), ldb >= ceil8(N);
-// rows 16-byte aligned. Layout of acc as in gemm_tile. Ends on a barrier with
-// no loads in flight.
+// B[k ldb + n]. Rows and columns past M, N read zero or whatever lies there
+// in the matrices (their results are not stored); k past K is zero in LDS
+// (also inside a chunk that straddles K), so the stored row padding up to a
+// multiple of 8 may hold anything. lda >= ceil8(K) (A_KMAJ) or ceil8(M),
+// ldb >= ceil8(N); rows 16-byte aligned. Layout of acc as in gemm_tile. Ends
+// on a barrier with no loads in flight.
 template <class C, bool A_KMAJ>
 __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, int64_t lda,
                                               const uint16_t* __restrict__ B, int64_t ldb,
@@ -623,30 +627,36 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
     const int trow = lane >> 5, tslot = lane & 31;
     const int64_t nk = (K + BK - 1) / BK;
 
-    // per-lane byte offsets of the loads, fixed for the whole K loop (the
-    // slice's base moves); the last chunk that exists: columns < ceil8(len)
-    auto tr_col = [&](int q, int64_t t0, int64_t len) -> int64_t {
-        const int k = (q * C::WAVES + wave) * 2 + trow;
-        const int64_t col = t0 + 8 * tr_slot(tslot, k);
-        const int64_t last = (len + 7) / 8 * 8 - 8;
-        return (col < last ? col : last) - t0;
-    };
-    uint32_t aoff[A_KMAJ ? C::IA : TQ], boff[TQ];
+    // Buffer loads into LDS, as in gemm_tile: one per-lane offset VGPR per
+    // operand, the instruction's rows and the slice as scalar offsets (or,
+    // for a transposed operand, the slice in the resource base). A transposed
+    // operand's resource ends at the last element of row K - 1 that exists
+    // (columns < ceil8(len)), so k rows past K read as zero; chunks past len
+    // within a row read the row padding or the next row (their results are
+    // not stored).
     const int lrow = lane / CH, lslot = lane % CH;
+    static_assert((C::WAVES * C::LROWS) % (16 / CH * CH) == 0, "swizzle period");
+    static_assert(C::WAVES % 2 == 0, "transposed swizzle period");
+    const int tr_k = wave * 2 + trow;  // transposed row of the lane in instruction 0
+    const int tr_c = 8 * tr_slot(tslot, tr_k);
+    uint32_t voff_a, qstride_a;
     if constexpr (A_KMAJ) {
-#pragma unroll
-        for (int q = 0; q < C::IA; ++q) {
-            const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-            aoff[q] = (uint32_t)(((min(m0 + r, M - 1) - m0) * lda + (lslot ^ swz<CH>(r)) * 8) * 2);
-        }
+        const int r_lane = wave * C::LROWS + lrow;
+        voff_a = (uint32_t)((r_lane * lda + (lslot ^ swz<CH>(r_lane)) * 8) * 2);
+        qstride_a = (uint32_t)(C::WAVES * C::LROWS * lda * 2);
     } else {
-#pragma unroll
-        for (int q = 0; q < TQ; ++q)
-            aoff[q] = (uint32_t)((((q * C::WAVES + wave) * 2 + trow) * lda + tr_col(q, m0, M)) * 2);
+        voff_a = (uint32_t)((tr_k * lda + tr_c) * 2);
+        qstride_a = (uint32_t)(C::WAVES * 2 * lda * 2);
     }
-#pragma unroll
-    for (int q = 0; q < TQ; ++q)
-        boff[q] = (uint32_t)((((q * C::WAVES + wave) * 2 + trow) * ldb + tr_col(q, n0, N)) * 2);
+    const uint32_t voff_b = (uint32_t)((tr_k * ldb + tr_c) * 2);
+    const uint32_t qstride_b = (uint32_t)(C::WAVES * 2 * ldb * 2);
+    const __amdgpu_buffer_rsrc_t rsrc_ak = tile_rsrc(A + m0 * lda, (M - m0) * lda * 2);
+    // resource of a transposed operand's slice kt: rows kt*BK .. K-1 from column t0
+    auto tr_rsrc = [&](const uint16_t* X, int64_t ld, int64_t t0, int64_t len, int64_t kt) {
+        const int64_t first = kt * BK * ld + t0;
+        const int64_t end = (K - 1) * ld + (len + 7) / 8 * 8;
+        return tile_rsrc(X + first, (end - first) * 2);
+    };
 
     auto lds_a = [&](int buf, int q) {
         constexpr int per = A_KMAJ ? C::LROWS * BK : 2 * kTw;  // elements per instruction
@@ -655,67 +665,36 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
     auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][0][0] + (q * C::WAVES + wave) * 2 * kTw; };
 
     auto issue = [&](int64_t kt, int buf) {
-        if ((kt + 1) * BK <= K) {
-            if constexpr (A_KMAJ) {
-                const char* a = reinterpret_cast<const char*>(A + m0 * lda + kt * BK);
+        if constexpr (A_KMAJ) {
+            const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
-                for (int q = 0; q < C::IA; ++q)
-                    __builtin_amdgcn_global_load_lds(a + aoff[q], lds_a(buf, q), 16, 0, 0);
-            } else {
-                const char* a = reinterpret_cast<const char*>(A + kt * BK * lda + m0);
-#pragma unroll
-                for (int q = 0; q < TQ; ++q)
-                    __builtin_amdgcn_global_load_lds(a + aoff[q], lds_a(buf, q), 16, 0, 0);
-            }
-            const char* b = reinterpret_cast<const char*>(B + kt * BK * ldb + n0);
+            for (int q = 0; q < C::IA; ++q)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_ak, lds_ptr(lds_a(buf, q)), 16,
+                                                        voff_a, kb + q * qstride_a, 0, 0);
+        } else {
+            const __amdgpu_buffer_rsrc_t ra = tr_rsrc(A, lda, m0, M, kt);
 #pragma unroll
             for (int q = 0; q < TQ; ++q)
-                __builtin_amdgcn_global_load_lds(b + boff[q], lds_b(buf, q), 16, 0, 0);
-        } else {
-            // the last, partial slice: k rows clamped to K - 1, k chunks to
-            // the last that exists (zeroed after landing)
-            if constexpr (A_KMAJ) {
-#pragma unroll
-                for (int q = 0; q < C::IA; ++q) {
-                    const int r = (q * C::WAVES + wave) * C::LROWS + lrow;
-                    const int64_t k = min(kt * BK + (lslot ^ swz<CH>(r)) * 8, (K + 7) / 8 * 8 - 8);
-                    __builtin_amdgcn_global_load_lds(A + min(m0 + r, M - 1) * lda + k,
-                                                     lds_a(buf, q), 16, 0, 0);
-                }
-            } else {
-#pragma unroll
-                for (int q = 0; q < TQ; ++q) {
-                    const int64_t k = min(kt * BK + (q * C::WAVES + wave) * 2 + trow, K - 1);
-                    __builtin_amdgcn_global_load_lds(A + k * lda + m0 + tr_col(q, m0, M),
-                                                     lds_a(buf, q), 16, 0, 0);
-                }
-            }
-#pragma unroll
-            for (int q = 0; q < TQ; ++q) {
-                const int64_t k = min(kt * BK + (q * C::WAVES + wave) * 2 + trow, K - 1);
-                __builtin_amdgcn_global_load_lds(B + k * ldb + n0 + tr_col(q, n0, N),
-                                                 lds_b(buf, q), 16, 0, 0);
-            }
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, lds_ptr(lds_a(buf, q)), 16, voff_a,
+                                                        q * qstride_a, 0, 0);
         }
+        const __amdgpu_buffer_rsrc_t rb = tr_rsrc(B, ldb, n0, N, kt);
+#pragma unroll
+        for (int q = 0; q < TQ; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, lds_ptr(lds_b(buf, q)), 16, voff_b,
+                                                    q * qstride_b, 0, 0);
     };
-    // the partial last slice: k >= K set to 0 in both operands
+    // the partial last slice of a K-major A: k >= K set to 0, also inside the
+    // chunk that straddles K (transposed operands read zero rows there)
     auto zero_tail = [&](int64_t kt, int buf) {
         const int kv = (int)(K - kt * BK);  // valid k in this slice, 1 .. BK-1
         uint16_t* a = &sm.in.a[buf][0][0];
-        uint16_t* b = &sm.in.b[buf][0][0];
         for (int e = tid; e < BK * kTw; e += C::THREADS) {
-            const int k = e / kTw;  // transposed layouts: row k
-            if (k >= kv) {
-                b[e] = 0;
-                if constexpr (!A_KMAJ) a[e] = 0;
-            }
-            if constexpr (A_KMAJ) {
-                // [BM][BK] rows with swizzled chunks: element e is row e / BK,
-                // slot (e % BK) / 8, holding chunk slot ^ swz(row)
-                const int r = e / BK, s = (e % BK) / 8;
-                const int kk = ((s ^ swz<CH>(r)) * 8) + (e % 8);
-                if (kk >= kv) a[e] = 0;
-            }
+            // [BM][BK] rows with swizzled chunks: element e is row e / BK,
+            // slot (e % BK) / 8, holding chunk slot ^ swz(row)
+            const int r = e / BK, sl = (e % BK) / 8;
+            const int kk = ((sl ^ swz<CH>(r)) * 8) + (e % 8);
+            if (kk >= kv) a[e] = 0;
         }
     };
 
@@ -782,7 +761,7 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
         constexpr int buf = decltype(bufc)::value;
         wait_vmcnt<0>();
         lds_ring_barrier();
-        if ((K % BK) && kt == nk - 1) {
+        if (A_KMAJ && (K % BK) && kt == nk - 1) {
             zero_tail(kt, buf);
             lds_ring_barrier();
         }
@@ -796,10 +775,12 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
         }
     };
     if (nk > 0) issue(0, 0);
-    for (int64_t kt = 0; kt < nk; kt += 2) {
+    int64_t kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
         slice(std::integral_constant<int, 0>{}, kt);
-        if (kt + 1 < nk) slice(std::integral_constant<int, 1>{}, kt + 1);
+        slice(std::integral_constant<int, 1>{}, kt + 1);
     }
+    if (kt < nk) slice(std::integral_constant<int, 0>{}, kt);
     __syncthreads();
 #else
     (void)A, (void)lda, (void)B, (void)ldb, (void)M, (void)N, (void)K, (void)m0, (void)n0;
