@@ -286,6 +286,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
         if (kt + 1 < nk) issue(kt + 1, buf ^ 1);
         // the operands of k-step ks+1 are read while the MFMAs of k-step ks issue
         read_step(bufc, 0, 0);
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int ks = 0; ks < C::KSTEPS; ++ks) {
             const int cs = ks & 1;
@@ -300,6 +301,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
                 }
             }
         }
+        __builtin_amdgcn_s_setprio(0);
     };
     // the loop body has no condition on the accumulators: an odd last slice
     // runs after it (a conditional second slice in the body made the compiler
@@ -767,12 +769,23 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
         }
         if (kt + 1 < nk) issue(kt + 1, buf ^ 1);
         read_step(bufc, 0, 0);
+        __builtin_amdgcn_s_setprio(1);
+        constexpr int NREAD = (A_KMAJ ? C::TM : 2 * C::TM) + 2 * C::TN;
 #pragma unroll
         for (int ks = 0; ks < C::KSTEPS; ++ks) {
             const int cs = ks & 1;
             if (ks < C::KSTEPS - 1) read_step(bufc, ks + 1, cs ^ 1);
             mfmas(cs);
+            if (ks < C::KSTEPS - 1) {
+#pragma unroll
+                for (int g = 0; g < C::TM * C::TN; ++g) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x100, NREAD - C::TM * C::TN, 0);
+            }
         }
+        __builtin_amdgcn_s_setprio(0);
     };
     if (nk > 0) issue(0, 0);
     int64_t kt = 0;
