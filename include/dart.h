@@ -464,11 +464,11 @@ enum { DART_LMHEAD_SKIP_ZERO_ROWS = 1u, DART_LMHEAD_BF16_GRADS = 4u };
  * logp, tok_coef) into the workspace, runs the blocked backward over those
  * rows only, and scatters their dhidden rows back; the rows it skipped are set
  * to 0. The result equals the dense call's up to the order of the GEMMs'
- * fp32 sums. Because the GEMM sizes depend on how many rows are
- * kept, the call copies that count to the host and synchronises the stream
- * once: on a stream that is being captured into a graph it returns
- * DART_ERR_UNSUPPORTED with nothing enqueued. Without this flag the call is
- * asynchronous and can be captured into a HIP graph.
+ * fp32 sums. The kernels read the kept-row count on the device (the launches
+ * cover all T rows; work past the count ends at once), so the call stays
+ * asynchronous and can be captured into a HIP graph, whose replays follow the
+ * coefficients the replay finds. With or without this flag the call can be
+ * captured (unless DART_CHECK=1).
  *
  *   dhidden:    [T, ld_dh] output, float32, or bfloat16 with
  *               DART_LMHEAD_BF16_GRADS; ld_dh >= d.

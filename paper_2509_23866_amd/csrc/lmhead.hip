@@ -451,11 +451,19 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
                       const int32_t* __restrict__ target, const float* __restrict__ lse,
                       const float* __restrict__ logp, const float* __restrict__ coef,
                       float scale, uint16_t* __restrict__ out, int64_t ld_out, int64_t vbase,
-                      int64_t nmt, int64_t nvt) {
+                      int64_t nmt, int64_t nvt, const int32_t* __restrict__ dyn_rows,
+                      int64_t dyn_base) {
     __shared__ typename C::Smem sm;
     int64_t mt, vt;
     tile_of_block(nmt, nvt, mt, vt);
     const int64_t m0 = mt * C::BM, n0 = vt * C::BN;
+    // with dyn_rows, the block holds only rows below *dyn_rows - dyn_base (the
+    // grid covers the most it can hold); tiles past them have nothing to do
+    if (dyn_rows) {
+        const int64_t live = (int64_t)*dyn_rows - dyn_base;
+        M = live < M ? (live > 0 ? live : 0) : M;
+        if (m0 >= M) return;
+    }
     f32x16 acc[C::TM][C::TN];
     gemm_tile<C>(h, M, ldh, w, V, ldw, d, m0, n0, sm, acc);
 
@@ -821,6 +829,11 @@ struct BwdGemm {
     int64_t ldc;
     int vec;
     int64_t nmt, nnt;  // tiles
+    // optional device row count: M (dyn_m) or K (dyn_k) is at most
+    // *dyn - dyn_base (the grid covers the host values, the most there can be)
+    const int32_t* dyn;
+    int64_t dyn_base;
+    bool dyn_m, dyn_k;
 };
 
 // Output modes of a backward GEMM: fp32 written, fp32 added to, bf16 written.
@@ -850,9 +863,18 @@ __device__ __forceinline__ void bwd_gemm_tile(const BwdGemm& g, int64_t b, typen
     int64_t mt, nt;
     tile_of_block_nfast(b, g.nmt, g.nnt, mt, nt);
     const int64_t m0 = mt * C::BM, n0 = nt * C::BN;
-    const int64_t M = g.M, N = g.N;
+    int64_t M = g.M, K = g.K;
+    const int64_t N = g.N;
+    if (g.dyn) {
+        const int64_t live = (int64_t)*g.dyn - g.dyn_base;
+        const int64_t lim = live > 0 ? live : 0;
+        if (g.dyn_m && lim < M) M = lim;
+        if (g.dyn_k && lim < K) K = lim;
+        // no rows of this block: nothing to write, or nothing to add
+        if (m0 >= M || (K == 0 && ACC)) return;
+    }
     f32x16 acc[C::TM][C::TN];
-    gemm_tile_bwd<C, A_KMAJ>(g.A, g.lda, g.B, g.ldb, M, N, g.K, m0, n0, sm, acc);
+    gemm_tile_bwd<C, A_KMAJ>(g.A, g.lda, g.B, g.ldb, M, N, K, m0, n0, sm, acc);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
@@ -1036,13 +1058,15 @@ dart_status_t launch_dlogits(const uint16_t* hidden, int64_t rows, int64_t d, in
                              const uint16_t* weight, int64_t V, int64_t ld_w,
                              const int32_t* target, const float* lse, const float* logp,
                              const float* coef, float scale, uint16_t* out, int64_t ld_out,
-                             int64_t vbase, hipStream_t stream) {
+                             int64_t vbase, hipStream_t stream, const int32_t* dyn_rows = nullptr,
+                             int64_t dyn_base = 0) {
     const int64_t nmt = (rows + LmCfg::BM - 1) / LmCfg::BM, nvt = vocab_tiles(V);
     if (!grid_fits(nmt * nvt, LmCfg::THREADS) || ld_h > kMaxLd || ld_w > kMaxLd)
         return DART_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(lmhead_dlogits_kernel<LmCfg>, dim3((unsigned)(nmt * nvt)),
                        dim3(LmCfg::THREADS), 0, stream, hidden, rows, ld_h, weight, V, ld_w, d,
-                       target, lse, logp, coef, scale, out, ld_out, vbase, nmt, nvt);
+                       target, lse, logp, coef, scale, out, ld_out, vbase, nmt, nvt, dyn_rows,
+                       dyn_base);
     return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
 }
 
@@ -1208,6 +1232,7 @@ BwdGemm make_bwd_gemm(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t
     g.vec = reinterpret_cast<uintptr_t>(out.p) % 16 == 0 && (out.ld * esz) % 16 == 0;
     g.nmt = (M + LmCfg::BM - 1) / LmCfg::BM;
     g.nnt = (N + LmCfg::BN - 1) / LmCfg::BN;
+    g.dyn = nullptr, g.dyn_base = 0, g.dyn_m = g.dyn_k = false;
     return g;
 }
 
@@ -1232,17 +1257,23 @@ void launch_bwd_gemms_dw(int dw_mode, const BwdGemm& dh, const BwdGemm& dw, int6
 
 // One block's dh[rows, d] (+)= dz[rows, cols] W[cols, d] and
 // dW[cols, d] (+)= dz[rows, cols]^T h[rows, d], in one launch. A bf16 output
-// is never added to (sums over blocks go through fp32).
+// is never added to (sums over blocks go through fp32). With dyn_rows, the
+// block's rows are at most *dyn_rows - dyn_base (read on the device).
 dart_status_t launch_bwd_gemms(const uint16_t* dz, int64_t ld_dz, int64_t rows, int64_t cols,
                                const uint16_t* w, int64_t ld_w, const uint16_t* h, int64_t ld_h,
                                int64_t d, const Grad& dh_out, bool dh_acc, const Grad& dw_out,
-                               bool dw_acc, hipStream_t stream) {
+                               bool dw_acc, hipStream_t stream, const int32_t* dyn_rows,
+                               int64_t dyn_base) {
     if ((dh_out.bf16 && dh_acc) || (dw_out.bf16 && dw_acc)) return DART_ERR_INVALID_ARG;
     if (ld_dz > kMaxLd || ld_w > kMaxLd || ld_h > kMaxLd || dh_out.ld > kMaxLd ||
         dw_out.ld > kMaxLd)
         return DART_ERR_UNSUPPORTED;
-    const BwdGemm dh = make_bwd_gemm(dz, ld_dz, w, ld_w, rows, d, cols, dh_out);
-    const BwdGemm dw = make_bwd_gemm(dz, ld_dz, h, ld_h, cols, d, rows, dw_out);
+    BwdGemm dh = make_bwd_gemm(dz, ld_dz, w, ld_w, rows, d, cols, dh_out);
+    BwdGemm dw = make_bwd_gemm(dz, ld_dz, h, ld_h, cols, d, rows, dw_out);
+    // the block's rows are dh's M and dW's K
+    dh.dyn = dw.dyn = dyn_rows;
+    dh.dyn_base = dw.dyn_base = dyn_base;
+    dh.dyn_m = dw.dyn_k = dyn_rows != nullptr;
     const int64_t n_dh = (dh.nmt * dh.nnt + 7) / 8 * 8;
     const int64_t blocks = n_dh + dw.nmt * dw.nnt;
     if (!grid_fits(blocks, LmCfg::THREADS)) return DART_ERR_UNSUPPORTED;
@@ -1266,14 +1297,17 @@ void launch_to_bf16(const float* src, int64_t rows, int64_t cols, const Grad& ds
 // the row blocks of its entries). A sum goes into its fp32 output directly,
 // or, for a bf16 output that more than one block adds to, into acc_h ([T, d])
 // or acc_w ([V, d]) and is rounded to bf16 once at the end; an output that
-// one block writes is that GEMM's fp32 result rounded once.
+// one block writes is that GEMM's fp32 result rounded once. With dyn_rows, T
+// is the most rows there can be and only the first *dyn_rows are formed (the
+// count is read on the device: blocks past it have nothing to do, and the
+// first row block writes dW even when it holds no rows).
 dart_status_t backward_core(const uint16_t* h, int64_t T, int64_t d,
                             int64_t ld_h, const uint16_t* w, int64_t V, int64_t ld_w,
                             const int32_t* target, const float* lse, const float* logp,
                             const float* coef, float scale, const Grad& dh, const Grad& dw,
                             int64_t R,
                             int64_t C, uint16_t* dz, float* acc_h, float* acc_w,
-                            hipStream_t stream) {
+                            hipStream_t stream, const int32_t* dyn_rows = nullptr) {
     if (R > T) R = T;
     if (C > V) C = V;
     const int64_t ld_dz = ceil8(C);
@@ -1288,12 +1322,12 @@ dart_status_t backward_core(const uint16_t* h, int64_t T, int64_t d,
             const uint16_t* wc = w + c0 * ld_w;
             const dart_status_t st =
                 launch_dlogits(hr, rows, d, ld_h, wc, cols, ld_w, target + r0, lse + r0,
-                               logp + r0, coef + r0, scale, dz, ld_dz, c0, stream);
+                               logp + r0, coef + r0, scale, dz, ld_dz, c0, stream, dyn_rows, r0);
             if (st != DART_OK) return st;
             const dart_status_t sg = launch_bwd_gemms(
                 dz, ld_dz, rows, cols, wc, ld_w, hr, ld_h, d,
                 Grad{sum_h.row(r0), sum_h.ld, sum_h.bf16}, c0 > 0,
-                Grad{sum_w.row(c0), sum_w.ld, sum_w.bf16}, r0 > 0, stream);
+                Grad{sum_w.row(c0), sum_w.ld, sum_w.bf16}, r0 > 0, stream, dyn_rows, r0);
             if (sg != DART_OK) return sg;
         }
     }
@@ -1343,9 +1377,6 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     const BackwardPlan P = plan_backward(T, d, V, chunk_rows, chunk_cols, flags);
     if (P.total == 0) return DART_ERR_UNSUPPORTED;
     if (workspace_bytes < P.total) return DART_ERR_INVALID_ARG;
-    // skipping rows waits for the kept-row count: not possible under graph capture
-    if (P.skip)
-        if (const dart_status_t st = may_synchronize(stream); st != DART_OK) return st;
     if (const dart_status_t ck = dart_check::run(
             stream, {{dart_check::Item::Ids, target, T, V}}); ck != DART_OK)
         return ck;
@@ -1381,23 +1412,12 @@ dart_status_t dart_lmhead_backward_ex(const void* hidden, int64_t T, int64_t d, 
     else
         launch_zero_rows<float>(dhidden, T, d, ld_dh, stream);
     if (hipGetLastError() != hipSuccess) return DART_ERR_HIP;
-    // the GEMM sizes are host values: wait for the count
-    int32_t n = 0;
-    if (hipMemcpyAsync(&n, count, sizeof n, hipMemcpyDeviceToHost, stream) != hipSuccess ||
-        hipStreamSynchronize(stream) != hipSuccess)
-        return DART_ERR_HIP;
-    if (n == 0) {
-        if (P.bf16)
-            launch_zero_rows<uint16_t>(dweight, V, d, ld_dw, stream);
-        else
-            launch_zero_rows<float>(dweight, V, d, ld_dw, stream);
-        return hipGetLastError() == hipSuccess ? DART_OK : DART_ERR_HIP;
-    }
+    // the kernels read the kept-row count on the device: T rows at most
     const dart_status_t st =
-        backward_core(h_c, n, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c, inv_temp,
-                      Grad{dh_c, d, false}, dw, P.rows, P.cols, dz, nullptr, acc_w, stream);
+        backward_core(h_c, T, d, d, w, V, ld_w, target_c, lse_c, logp_c, coef_c, inv_temp,
+                      Grad{dh_c, d, false}, dw, P.rows, P.cols, dz, nullptr, acc_w, stream, count);
     if (st != DART_OK) return st;
-    const unsigned nb = (unsigned)(n < kRowBlocks ? n : kRowBlocks);
+    const unsigned nb = (unsigned)(T < kRowBlocks ? T : kRowBlocks);
     if (P.bf16)
         hipLaunchKernelGGL(scatter_rows_kernel<uint16_t>, dim3(nb), dim3(256), 0, stream, map,
                            count, dh_c, d, static_cast<uint16_t*>(dhidden), ld_dh);

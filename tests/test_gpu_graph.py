@@ -72,28 +72,18 @@ def test_graph_replays_match_eager(T):
         torch.cuda.synchronize()
 
 
-def test_synchronising_modes_refused_under_capture(monkeypatch):
-    """The row-skipping LM-head backward and DART_CHECK=1 wait for the host; on a
-    stream that is being captured they return DART_ERR_UNSUPPORTED with nothing
-    enqueued, the capture goes on (a statistics call captured after them
-    replays to the eager bits), and the row-skipping call works eagerly."""
+def test_synchronising_mode_refused_under_capture(monkeypatch):
+    """DART_CHECK=1 waits for the host: on a stream that is being captured a
+    call returns DART_ERR_UNSUPPORTED with nothing enqueued, and the capture
+    goes on (a statistics call captured after it replays to the eager bits)."""
     import torch
 
     import paper_2509_23866_amd as dart
 
-    T, d, V = 64, 64, 300
+    T, V = 64, 300
     rng = np.random.default_rng(5)
-    h = torch.from_numpy(rng.normal(0, 1, (T, d)).astype(np.float32)).cuda().to(torch.bfloat16)
-    w = torch.from_numpy(rng.normal(0, 0.3, (V, d)).astype(np.float32)).cuda().to(torch.bfloat16)
     y = _cuda(rng.integers(0, V, T).astype(np.int32))
     logits = torch.from_numpy(rng.normal(0, 3, (T, V)).astype(np.float32)).cuda()
-    logp, _, lse = dart.dart_lmhead_tok_stats(h, w, y)
-    coef = _cuda(np.where(rng.random(T) < 0.3, 0.0, 1e-2).astype(np.float32))
-    skip = dart.DART_LMHEAD_SKIP_ZERO_ROWS
-    dh = torch.empty((T, d), dtype=torch.float32, device="cuda")
-    dw = torch.empty((V, d), dtype=torch.float32, device="cuda")
-    ws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, T, V, skip),
-                     dtype=torch.uint8, device="cuda")
     out = [torch.empty(T, dtype=torch.float32, device="cuda") for _ in range(3)]
     ref = dart.dart_tok_stats(logits, y)
     side = torch.cuda.Stream()
@@ -102,12 +92,6 @@ def test_synchronising_modes_refused_under_capture(monkeypatch):
     codes = []
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=side):
-        try:
-            dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=T, chunk_cols=V,
-                                         flags=skip, dhidden=dh, dweight=dw, workspace=ws,
-                                         stream=side)
-        except dart.DartError as e:
-            codes.append(e.code)
         monkeypatch.setenv("DART_CHECK", "1")
         try:
             dart.dart_tok_stats(logits, y, *out, stream=side)
@@ -115,7 +99,7 @@ def test_synchronising_modes_refused_under_capture(monkeypatch):
             codes.append(e.code)
         monkeypatch.setenv("DART_CHECK", "0")
         dart.dart_tok_stats(logits, y, *out, stream=side)
-    assert codes == [dart.DART_ERR_UNSUPPORTED, dart.DART_ERR_UNSUPPORTED]
+    assert codes == [dart.DART_ERR_UNSUPPORTED]
     for _ in range(2):
         for o in out:
             o.fill_(-1.0)
@@ -124,10 +108,65 @@ def test_synchronising_modes_refused_under_capture(monkeypatch):
         torch.cuda.synchronize()
         for o, r in zip(out, ref):
             assert torch.equal(o, r)
-    dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=T, chunk_cols=V, flags=skip,
-                                 dhidden=dh, dweight=dw, workspace=ws)
+
+
+@pytest.mark.parametrize("rows,cols,bf16", [(64, 300, False), (32, 128, True)])
+def test_lmhead_skip_rows_graph_follows_the_device_count(rows, cols, bf16):
+    """The row-skipping LM-head backward reads the kept-row count on the
+    device, so it captures into a graph; replays after the coefficients change
+    in place (more, fewer, all and no rows kept) give the bits of an eager call
+    on the new coefficients, in row blocks of 64 or 32 and vocabulary blocks."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    T, d, V = 150, 64, 300
+    rng = np.random.default_rng(21)
+    h = torch.from_numpy(rng.normal(0, 1, (T, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    w = torch.from_numpy(rng.normal(0, 0.3, (V, d)).astype(np.float32)).cuda().to(torch.bfloat16)
+    y = _cuda(rng.integers(0, V, T).astype(np.int32))
+    logp, _, lse = dart.dart_lmhead_tok_stats(h, w, y)
+    flags = dart.DART_LMHEAD_SKIP_ZERO_ROWS | (dart.DART_LMHEAD_BF16_GRADS if bf16 else 0)
+    gdt = torch.bfloat16 if bf16 else torch.float32
+    coef = torch.empty(T, dtype=torch.float32, device="cuda")
+    dh = torch.empty((T, d), dtype=gdt, device="cuda")
+    dw = torch.empty((V, d), dtype=gdt, device="cuda")
+    ws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, flags),
+                     dtype=torch.uint8, device="cuda")
+    patterns = [np.where(rng.random(T) < p, 0.0, rng.uniform(-1e-2, 1e-2, T)) for p in (0.3, 0.8)]
+    patterns += [np.full(T, 3e-3), np.zeros(T)]
+
+    def call(s):
+        dart.dart_lmhead_backward_ex(h, w, y, lse, logp, coef, chunk_rows=rows, chunk_cols=cols,
+                                     flags=flags, dhidden=dh, dweight=dw, workspace=ws, stream=s)
+
+    coef.copy_(torch.from_numpy(patterns[0].astype(np.float32)))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call(side)
     torch.cuda.synchronize()
-    assert torch.all(dh[torch.from_numpy(coef.cpu().numpy() == 0.0).cuda()] == 0.0)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        call(side)
+    torch.cuda.synchronize()
+    for pat in patterns + patterns[:1]:
+        coef.copy_(torch.from_numpy(pat.astype(np.float32)))
+        torch.cuda.synchronize()
+        call(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        eager = (dh.clone(), dw.clone())
+        dh.view(torch.uint8).fill_(0x7F)
+        dw.view(torch.uint8).fill_(0x7F)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dh.view(torch.uint8), eager[0].view(torch.uint8))
+        assert torch.equal(dw.view(torch.uint8), eager[1].view(torch.uint8))
+        zero = torch.from_numpy(pat == 0.0).cuda()
+        assert torch.all(dh[zero] == 0)
+        if not pat.any():  # no row kept: dweight is exactly zero
+            assert torch.all(dw == 0)
 
 
 @pytest.mark.parametrize("rows,cols,bf16", [(256, 300, False), (100, 128, True)])
