@@ -392,10 +392,11 @@ def groups_variant(wl, dev, stream, ent, off, n):
 def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
     """One whole LM-head training step with bf16 gradients, two ways: fused
     (statistics, selection, loss and the blocked backward in its 512 MiB plan;
-    the logits are formed twice and never stored) and through the library
-    (the logits and the dlogits materialised in bf16: GEMM, statistics,
-    selection, loss, gradient pass, two GEMMs), with the workload's steps,
-    advantages and old-policy log-probs."""
+    the logits are formed twice and never stored), also with the rows whose
+    coefficient is zero skipped in the backward, and through the library (the
+    logits and the dlogits materialised in bf16: GEMM, statistics, selection,
+    loss, gradient pass, two GEMMs), with the workload's steps, advantages and
+    old-policy log-probs."""
     import torch
 
     import paper_2509_23866_amd as dart
@@ -428,12 +429,16 @@ def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
                                wl.C, loss=loss, tok_coef=coef, stats=st, workspace=lws,
                                stream=stream)
 
-    def fused():
+    skip = bf | dart.DART_LMHEAD_SKIP_ZERO_ROWS
+    kws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, skip),
+                      dtype=torch.uint8, device=dev)
+
+    def fused(flags=bf, ws=bws):
         dart.dart_lmhead_tok_stats(h, w, target, logp, ent, lse, workspace=sws, stream=stream)
         loss_part()
         dart.dart_lmhead_backward_ex(h, w, target, lse, logp, coef, chunk_rows=rows,
-                                     chunk_cols=cols, flags=bf, dhidden=dh, dweight=dw,
-                                     workspace=bws, stream=stream)
+                                     chunk_cols=cols, flags=flags, dhidden=dh, dweight=dw,
+                                     workspace=ws, stream=stream)
 
     def library():
         with torch.cuda.stream(stream):
@@ -445,7 +450,10 @@ def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
             torch.matmul(dzbuf.t(), h, out=dw)
 
     fused_ms, library_ms = timed(fused), timed(library)
+    skip_ms = timed(lambda: fused(skip, kws))
     return {"fused_ms": fused_ms, "fused_workspace_bytes": sws.numel() + bws.numel(),
+            "fused_skip_zero_rows_ms": skip_ms,
+            "fused_skip_zero_rows_workspace_bytes": sws.numel() + kws.numel(),
             "library_ms": library_ms, "library_logits_bytes": 2 * zbuf.numel() * 2,
             "block": [rows, cols]}
 
