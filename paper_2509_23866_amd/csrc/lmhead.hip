@@ -454,16 +454,19 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
                       int64_t nmt, int64_t nvt, const int32_t* __restrict__ dyn_rows,
                       int64_t dyn_base) {
     __shared__ typename C::Smem sm;
-    int64_t mt, vt;
-    tile_of_block(nmt, nvt, mt, vt);
-    const int64_t m0 = mt * C::BM, n0 = vt * C::BN;
     // with dyn_rows, the block holds only rows below *dyn_rows - dyn_base (the
-    // grid covers the most it can hold); tiles past them have nothing to do
+    // grid covers the most it can hold): the tiles are laid over the live rows'
+    // tiles, so that they spread over every XCD, and the workgroups past them
+    // (the last ones dispatched) have nothing to do
     if (dyn_rows) {
         const int64_t live = (int64_t)*dyn_rows - dyn_base;
         M = live < M ? (live > 0 ? live : 0) : M;
-        if (m0 >= M) return;
+        nmt = (M + C::BM - 1) / C::BM;
+        if ((int64_t)blockIdx.x >= nmt * nvt) return;
     }
+    int64_t mt, vt;
+    tile_of_block(nmt, nvt, mt, vt);
+    const int64_t m0 = mt * C::BM, n0 = vt * C::BN;
     f32x16 acc[C::TM][C::TN];
     gemm_tile<C>(h, M, ldh, w, V, ldw, d, m0, n0, sm, acc);
 
@@ -860,19 +863,24 @@ template <class C, bool A_KMAJ, int OUT>
 __device__ __forceinline__ void bwd_gemm_tile(const BwdGemm& g, int64_t b, typename C::Smem& sm) {
     using OutT = typename std::conditional<OUT == kOutBf16, uint16_t, float>::type;
     constexpr bool ACC = OUT == kOutF32Acc;
-    int64_t mt, nt;
-    tile_of_block_nfast(b, g.nmt, g.nnt, mt, nt);
-    const int64_t m0 = mt * C::BM, n0 = nt * C::BN;
-    int64_t M = g.M, K = g.K;
+    int64_t M = g.M, K = g.K, nmt = g.nmt;
     const int64_t N = g.N;
     if (g.dyn) {
         const int64_t live = (int64_t)*g.dyn - g.dyn_base;
         const int64_t lim = live > 0 ? live : 0;
-        if (g.dyn_m && lim < M) M = lim;
         if (g.dyn_k && lim < K) K = lim;
-        // no rows of this block: nothing to write, or nothing to add
-        if (m0 >= M || (K == 0 && ACC)) return;
+        // no rows of this block to add: nothing to do
+        if (K == 0 && ACC) return;
+        if (g.dyn_m && lim < M) {
+            // the tiles laid over the live rows' tiles (spread over every XCD)
+            M = lim;
+            nmt = (M + C::BM - 1) / C::BM;
+            if (b >= nmt * g.nnt) return;
+        }
     }
+    int64_t mt, nt;
+    tile_of_block_nfast(b, nmt, g.nnt, mt, nt);
+    const int64_t m0 = mt * C::BM, n0 = nt * C::BN;
     f32x16 acc[C::TM][C::TN];
     gemm_tile_bwd<C, A_KMAJ>(g.A, g.lda, g.B, g.ldb, M, N, K, m0, n0, sm, acc);
 
