@@ -24,9 +24,9 @@
 //                         dz = g (onehot - softmax) in bf16.
 // The backward forms dz block by block (rows x vocabulary entries, the blocked
 // entry point optionally over the rows with a non-zero coefficient only) and
-// adds dh = dz W and dW = dz^T h per block with lmhead_bwd_gemm_kernel (the
-// same MFMA tile, its operands stored with K as their row index read through
-// LDS transpose loads).
+// adds dh = dz W and dW = dz^T h per block in one launch of
+// lmhead_bwd_gemms_kernel (the same MFMA tile, its operands stored with K as
+// their row index read through LDS transpose loads).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
