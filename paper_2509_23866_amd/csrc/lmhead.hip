@@ -41,6 +41,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Waits until at most N loads of this wave are outstanding (vmcnt), leaving
@@ -356,20 +357,18 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
+    static_assert(C::EPI == C::RS, "one row block of every wave per pass");
 #pragma unroll
-    for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
-        if (e0) __syncthreads();
-        // rows [e0, e0 + EPI) of the tile to LDS
+    for (int ip = 0; ip < C::TM; ++ip) {
+        const int e0 = ip * C::EPI;
+        if (ip) __syncthreads();
+        // rows [e0, e0 + EPI) of the tile to LDS: row block ip of every wave
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i)
+        for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
-                    if (row >= 0 && row < C::EPI)
-                        sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v] * scale;
-                }
+            for (int v = 0; v < 16; ++v)
+                sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
+                    acc[ip][j][v] * scale;
         __syncthreads();
         // P threads per row; thread p takes the 16-byte pieces p, p + P, ...
         // of the row (columns 16 c + 4 p + u) into registers: maximum over the
@@ -387,23 +386,39 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
         // into a triple (maximum, then the sums in base-2 units against it)
         // and merged; columns past V and the target's column drop out as -inf
         constexpr int NH = NX / 2;
+        // only the tile's last columns past V and a row's target column drop
+        // out: the selects run only in threads that hold such a column
+        const bool masked = vlim < C::BN || (y32 >= 0 && ((y32 >> 2) & (P - 1)) == p);
         Triple mine = {-INFINITY, 0.f, 0.f};
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
+            // the half's eight 16-byte reads, issued together; the empty asm
+            // keeps the compiler from turning the selects below into
+            // per-element predicated reads
+            static_assert(NH / 4 == 8, "eight vectors per half row");
+            f32x4 q[8];
+#pragma unroll
+            for (int c4 = 0; c4 < 8; ++c4)
+                q[c4] = *reinterpret_cast<const f32x4*>(&sm.c[r][16 * (hh * 8 + c4) + 4 * p]);
+            asm volatile("" : "+v"(q[0]), "+v"(q[1]), "+v"(q[2]), "+v"(q[3]), "+v"(q[4]),
+                         "+v"(q[5]), "+v"(q[6]), "+v"(q[7]));
             float x[NH];
+#pragma unroll
+            for (int c4 = 0; c4 < 8; ++c4)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) x[4 * c4 + u] = q[c4][u];
+            if (masked) {
+#pragma unroll
+                for (int c4 = 0; c4 < 8; ++c4)
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int col = 16 * (hh * 8 + c4) + 4 * p + u;
+                        x[4 * c4 + u] = col < vlim && col != y32 ? x[4 * c4 + u] : -INFINITY;
+                    }
+            }
             float mx = -INFINITY;
 #pragma unroll
-            for (int c4 = 0; c4 < NH / 4; ++c4) {
-                const int cc = hh * (NH / 4) + c4;
-                const float4 q = *reinterpret_cast<const float4*>(&sm.c[r][16 * cc + 4 * p]);
-                const float qv[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int col = 16 * cc + 4 * p + u;
-                    x[4 * c4 + u] = col < vlim && col != y32 ? qv[u] : -INFINITY;
-                    mx = fmaxf(mx, x[4 * c4 + u]);
-                }
-            }
+            for (int i = 0; i < NH; ++i) mx = fmaxf(mx, x[i]);
             Triple part_h = {mx, 0.f, 0.f};
             if (mx > -INFINITY) {
                 // e = 2^xl with xl = (x - mx) log2(e) floored at -200, where 2^xl
@@ -473,19 +488,17 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
     constexpr int CHUNKS = C::BN / 8;  // 16-byte output chunks per tile row
+    static_assert(C::EPI == C::RS, "one row block of every wave per pass");
 #pragma unroll
-    for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
-        if (e0) __syncthreads();
+    for (int ip = 0; ip < C::TM; ++ip) {
+        const int e0 = ip * C::EPI;
+        if (ip) __syncthreads();
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i)
+        for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
-                    if (row >= 0 && row < C::EPI)
-                        sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v] * scale;
-                }
+            for (int v = 0; v < 16; ++v)
+                sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
+                    acc[ip][j][v] * scale;
         // per-row constants: -g, -lse log2(e), the target's gradient
         // g (-expm1(logp)) (accurate when p_y -> 1), the target's column here;
         // g carries the inverse temperature (the chain rule through scale z)
@@ -890,18 +903,17 @@ __device__ __forceinline__ void bwd_gemm_tile(const BwdGemm& g, int64_t b, typen
     constexpr int EPV = F32 ? 4 : 8;  // elements per 16-byte vector
     constexpr int VPR = C::BN / EPV;  // vectors per tile row
     OutT* out = static_cast<OutT*>(g.out);
+    static_assert(C::EPI == C::RS, "one row block of every wave per pass");
 #pragma unroll
-    for (int e0 = 0; e0 < C::BM; e0 += C::EPI) {
-        if (e0) __syncthreads();
+    for (int ip = 0; ip < C::TM; ++ip) {
+        const int e0 = ip * C::EPI;
+        if (ip) __syncthreads();
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i)
+        for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = wr + i * C::RS + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3) - e0;
-                    if (row >= 0 && row < C::EPI) sm.c[row][wc + j * 32 + (lane & 31)] = acc[i][j][v];
-                }
+            for (int v = 0; v < 16; ++v)
+                sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
+                    acc[ip][j][v];
         __syncthreads();
         for (int e = tid; e < C::EPI * VPR; e += C::THREADS) {
             const int r = e / VPR, cv = e % VPR;
