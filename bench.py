@@ -2,8 +2,8 @@
 """Benchmark of the DART policy-update hot path on one MI355X (gfx950).
 
 One step = one pass of the whole path over one step group held in HBM:
-dart_tok_stats -> dart_step_select -> dart_tis_loss_fwd -> dart_tis_grad, on
-one stream. The K timed steps run back to back; per-kernel durations come from
+dart_tok_stats -> dart_select_tis_loss_fwd (step means, selection, coefficients
+and loss; one launch up to 16384 tokens) -> dart_tis_grad, on one stream. The K timed steps run back to back; per-kernel durations come from
 a second pass of K steps with HIP events around each kernel. The default workload is the 7B-VLM vocabulary group: T = 4096
 action tokens in 64 steps, V = 152064, bf16 logits, separate gradient buffer.
 
@@ -424,10 +424,9 @@ def training_steps(wl, dev, stream, h, w, target, zbuf, timed):
     dzbuf = torch.empty_like(zbuf)
 
     def loss_part():
-        dart.dart_step_select(ent, off, wl.rho, sh, mask, nk, stream=stream)
-        dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, wl.eps_low, wl.eps_high,
-                               wl.C, loss=loss, tok_coef=coef, stats=st, workspace=lws,
-                               stream=stream)
+        dart.dart_select_tis_loss_fwd(ent, logp, lp_old, lp_roll, adv, off, wl.rho, wl.eps_low,
+                                      wl.eps_high, wl.C, sh, mask, nk, loss, coef, st,
+                                      workspace=lws, stream=stream)
 
     skip = bf | dart.DART_LMHEAD_SKIP_ZERO_ROWS
     kws = torch.empty(dart.dart_lmhead_backward_ex_workspace_bytes(T, d, V, rows, cols, skip),
@@ -523,9 +522,9 @@ def measure_workload(wl, args, dev, headline):
         dart.dart_tok_stats(logits, target, logp, ent, lse, stream=s)
         if ev:
             ev[1].record(s)
-        dart.dart_step_select(ent, off, wl.rho, step_H, mask, n_kept, stream=s)
-        dart.dart_tis_loss_fwd(logp, lp_old, lp_roll, adv, off, mask, eps_low, eps_high, C,
-                               loss, coef, stats, stream=s, workspace=workspace)
+        dart.dart_select_tis_loss_fwd(ent, logp, lp_old, lp_roll, adv, off, wl.rho, eps_low,
+                                      eps_high, C, step_H, mask, n_kept, loss, coef, stats,
+                                      stream=s, workspace=workspace)
         if ev:
             ev[2].record(s)
         dart.dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=s,

@@ -201,6 +201,33 @@ dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, i
                             const float* lse, const float* tok_coef, void* dlogits,
                             int64_t ld_out, hipStream_t stream);
 
+/* dart_step_select followed by dart_tis_loss_fwd on the mask it selects: the
+ * step means and top-rho selection of Sec. 4.3, then the coefficients and loss
+ * of Eq. (2), in one launch of one workgroup when T <= 16384 and S <= 8192
+ * (both calls' work back to back, without the kernel boundaries between them);
+ * larger problems make the two calls in turn.
+ *   Arguments: entropy, T, step_offsets, S, rho, step_entropy, step_mask,
+ *              n_kept_steps as for dart_step_select (step_mask is an output);
+ *              logp, logp_old, logp_rollout, adv, eps_low, eps_high, C, loss,
+ *              tok_coef, stats, workspace, workspace_bytes as for
+ *              dart_tis_loss_fwd. The workspace is used only when the problem
+ *              is too large for one workgroup.
+ *   Results:   step_entropy, step_mask, n_kept_steps and tok_coef equal those
+ *              of the two calls bit for bit; loss and stats are the same sums
+ *              in float64 in the one-workgroup order (the two calls with a
+ *              workspace sum over several workgroups, so the last bits of the
+ *              loss may differ).
+ * Errors: the rules of both calls, all checked before anything is enqueued
+ * (INVALID_ARG); HIP when a launch fails. */
+dart_status_t dart_select_tis_loss_fwd(int64_t T, const float* entropy, const float* logp,
+                                       const float* logp_old, const float* logp_rollout,
+                                       const float* adv, const int32_t* step_offsets, int64_t S,
+                                       double rho, float eps_low, float eps_high, float C,
+                                       float* step_entropy, uint8_t* step_mask,
+                                       int32_t* n_kept_steps, double* loss, float* tok_coef,
+                                       float* stats, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Objective variants and options (same two passes over the logits)
  * ------------------------------------------------------------------------ */

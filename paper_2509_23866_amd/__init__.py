@@ -36,7 +36,7 @@ DART_LMHEAD_SKIP_ZERO_ROWS = 1
 DART_LMHEAD_BF16_GRADS = 4
 
 EXPORTED = ("dart_tok_stats", "dart_step_select", "dart_tis_loss_fwd_bwd", "dart_tis_loss_fwd",
-            "dart_tis_grad", "dart_tis_loss_fwd_bwd_noalloc",
+            "dart_tis_grad", "dart_tis_loss_fwd_bwd_noalloc", "dart_select_tis_loss_fwd",
             "dart_tok_stats_ex", "dart_tis_loss_fwd_ex", "dart_tis_grad_ex",
             "dart_grpo_advantage", "dart_step_select_groups", "dart_tis_loss_workspace_bytes",
             "dart_lmhead_tok_stats", "dart_lmhead_tok_stats_ex", "dart_lmhead_stats_workspace_bytes",
@@ -89,6 +89,10 @@ def load_library():
         lib.dart_tis_loss_fwd.argtypes = [_I64, _P, _P, _P, _P, _P, _I64, _P, ctypes.c_float,
                                           ctypes.c_float, ctypes.c_float, _P, _P, _P, _P,
                                           ctypes.c_size_t, _P]
+        lib.dart_select_tis_loss_fwd.restype = ctypes.c_int
+        lib.dart_select_tis_loss_fwd.argtypes = [
+            _I64, _P, _P, _P, _P, _P, _P, _I64, ctypes.c_double, ctypes.c_float, ctypes.c_float,
+            ctypes.c_float, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
         lib.dart_tis_loss_workspace_bytes.restype = ctypes.c_size_t
         lib.dart_tis_loss_workspace_bytes.argtypes = [_I64]
         lib.dart_tis_grad.restype = ctypes.c_int
@@ -389,6 +393,48 @@ def dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, step_mask
     if rc != DART_OK:
         raise DartError("dart_tis_loss_fwd", rc)
     return loss, tok_coef, stats
+
+
+def dart_select_tis_loss_fwd(entropy, logp, logp_old, logp_rollout, adv, step_offsets, rho,
+                             eps_low, eps_high, C, step_entropy=None, step_mask=None,
+                             n_kept_steps=None, loss=None, tok_coef=None, stats=None,
+                             with_stats=True, stream=None, workspace="auto"):
+    """dart_step_select then dart_tis_loss_fwd in one call (one launch when the
+    problem fits one workgroup). Returns (step_entropy, step_mask,
+    n_kept_steps, loss, tok_coef, stats). ``workspace`` as for
+    dart_tis_loss_fwd_bwd."""
+    torch = _torch()
+    dev = logp.device
+    T = logp.numel()
+    S = step_offsets.numel() - 1
+    for n, v in (("entropy", entropy), ("logp", logp), ("logp_old", logp_old),
+                 ("logp_rollout", logp_rollout), ("adv", adv)):
+        _check_vec(n, v, torch.float32, T, dev)
+    _check_vec("step_offsets", step_offsets, torch.int32, S + 1, dev)
+    step_entropy = torch.empty(S, dtype=torch.float32, device=dev) if step_entropy is None else step_entropy
+    step_mask = torch.empty(S, dtype=torch.uint8, device=dev) if step_mask is None else step_mask
+    n_kept_steps = torch.empty(1, dtype=torch.int32, device=dev) if n_kept_steps is None else n_kept_steps
+    loss = torch.empty(1, dtype=torch.float64, device=dev) if loss is None else loss
+    tok_coef = torch.empty(T, dtype=torch.float32, device=dev) if tok_coef is None else tok_coef
+    if stats is None and with_stats:
+        stats = torch.empty(4, dtype=torch.float32, device=dev)
+    _check_vec("step_entropy", step_entropy, torch.float32, S, dev)
+    _check_vec("step_mask", step_mask, torch.uint8, S, dev)
+    _check_vec("n_kept_steps", n_kept_steps, torch.int32, 1, dev)
+    _check_vec("loss", loss, torch.float64, 1, dev)
+    _check_vec("tok_coef", tok_coef, torch.float32, T, dev)
+    if stats is not None:
+        _check_vec("stats", stats, torch.float32, 4, dev)
+    ws, ws_bytes, _ws = _workspace(workspace, T, dev, stream)
+    rc = load_library().dart_select_tis_loss_fwd(
+        T, entropy.data_ptr(), logp.data_ptr(), logp_old.data_ptr(), logp_rollout.data_ptr(),
+        adv.data_ptr(), step_offsets.data_ptr(), S, float(rho), float(eps_low), float(eps_high),
+        float(C), step_entropy.data_ptr(), step_mask.data_ptr(), n_kept_steps.data_ptr(),
+        loss.data_ptr(), tok_coef.data_ptr(), _ptr(stats), ws, ws_bytes,
+        _stream_handle(stream, dev))
+    if rc != DART_OK:
+        raise DartError("dart_select_tis_loss_fwd", rc)
+    return step_entropy, step_mask, n_kept_steps, loss, tok_coef, stats
 
 
 def dart_tis_loss_fwd_ex(logp, logp_old, logp_rollout, adv, step_offsets, step_mask, eps_low,

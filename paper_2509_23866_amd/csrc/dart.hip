@@ -462,6 +462,18 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t x) {
     return (int64_t)wave_reduce_u64((uint64_t)x, [](uint64_t a, uint64_t b) { return a + b; });
 }
 
+// Workgroup barrier for data exchanged through LDS only: waits for the wave's
+// LDS accesses (lgkmcnt) but not for its global stores, which the fence of
+// __syncthreads would wait for (~1 us each time in the one-workgroup kernels);
+// the empty asm statements keep the compiler from moving memory accesses
+// across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Token range of step s, clamped to [0, T] so that malformed offsets (a broken
 // precondition) give meaningless numbers but never an out-of-bounds access.
 __device__ __forceinline__ void step_bounds(const int32_t* off, int64_t s, int64_t T, int64_t& b,
@@ -510,24 +522,35 @@ __device__ __forceinline__ int64_t kept_steps_dev(int64_t n, double rho) {
 // computes the step means itself, from the token entropies and offsets staged
 // in LDS, in the order of step_mean_kernel (so with bit-identical results),
 // and writes them to step_H.
+// LDS of the selection; with the means fused in, also the token entropies
+// and the clamped offsets (off_l[s] = first token of step s, off_l[S] = end)
+struct SelLds {
+    uint32_t keys[kSelLdsKeys];
+    uint32_t hist[256];
+    uint32_t sel_bin;
+    int64_t sel_remaining;
+    int64_t wave_count[kSelWaves];
+};
+
 template <bool FUSED>
-__global__ void __launch_bounds__(kSelThreads)
-step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
-                   int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
-                   float* __restrict__ step_H, uint8_t* __restrict__ mask,
-                   int32_t* __restrict__ n_kept) {
-    __shared__ uint32_t keys[kSelLdsKeys];
-    __shared__ uint32_t hist[256];
-    __shared__ uint32_t sel_bin;
-    __shared__ int64_t sel_remaining;
-    __shared__ int64_t wave_count[kSelWaves];
+__device__ __forceinline__ void select_steps(const float* __restrict__ H, int64_t T,
+                                             const int32_t* __restrict__ off, int64_t S,
+                                             const int32_t* __restrict__ grp, double rho,
+                                             int64_t k_all, float* __restrict__ step_H,
+                                             uint8_t* __restrict__ mask,
+                                             int32_t* __restrict__ n_kept, SelLds& sl,
+                                             float* H_l, int32_t* off_l,
+                                             uint8_t* mask_l = nullptr) {
+    uint32_t* keys = sl.keys;
+    uint32_t* hist = sl.hist;
+    uint32_t& sel_bin = sl.sel_bin;
+    int64_t& sel_remaining = sl.sel_remaining;
+    int64_t* wave_count = sl.wave_count;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     if constexpr (FUSED) {
-        __shared__ float H_l[kSelLdsTokens];
-        __shared__ int32_t off_l[kSelLdsKeys + 1];
 #pragma unroll 4
         for (int64_t i = tid; i < T; i += kSelThreads) H_l[i] = H[i];
         for (int64_t s = tid; s < S; s += kSelThreads) {
@@ -548,7 +571,7 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
                 keys[s] = float_key(m);
             }
         }
-        __syncthreads();
+        lds_barrier();  // the keys; the step means in global memory are not read here
     }
     int64_t gs = 0, ge = S, k = k_all;
     if (grp) {
@@ -559,7 +582,10 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
     const int64_t Sg = ge - gs;
 
     if (k <= 0 || k >= Sg) {
-        for (int64_t s = gs + tid; s < ge; s += kSelThreads) mask[s] = k > 0 ? 1 : 0;
+        for (int64_t s = gs + tid; s < ge; s += kSelThreads) {
+            mask[s] = k > 0 ? 1 : 0;
+            if (mask_l) mask_l[s] = k > 0 ? 1 : 0;
+        }
         if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)(k > 0 ? Sg : 0);
         return;
     }
@@ -585,6 +611,7 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
                 rank += (kj > ki || (kj == ki && j < i)) ? 1 : 0;
             }
             mask[gs + i] = rank < k ? 1 : 0;
+            if (mask_l) mask_l[gs + i] = rank < k ? 1 : 0;
         }
         if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)k;
         return;
@@ -657,12 +684,31 @@ step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
         }
         if (i < Sg) {
             const int64_t rank = carry + wave_before + before;
-            mask[gs + i] = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
+            const uint8_t m = (key > prefix || (eq && rank < remaining)) ? 1 : 0;
+            mask[gs + i] = m;
+            if (mask_l) mask_l[gs + i] = m;
         }
         carry += total;
         __syncthreads();
     }
     if (tid == 0 && n_kept) n_kept[blockIdx.x] = (int32_t)k;
+}
+
+template <bool FUSED>
+__global__ void __launch_bounds__(kSelThreads)
+step_select_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
+                   int64_t S, const int32_t* __restrict__ grp, double rho, int64_t k_all,
+                   float* __restrict__ step_H, uint8_t* __restrict__ mask,
+                   int32_t* __restrict__ n_kept) {
+    __shared__ SelLds sl;
+    if constexpr (FUSED) {
+        __shared__ float H_l[kSelLdsTokens];
+        __shared__ int32_t off_l[kSelLdsKeys + 1];
+        select_steps<true>(H, T, off, S, grp, rho, k_all, step_H, mask, n_kept, sl, H_l, off_l);
+    } else {
+        select_steps<false>(H, T, off, S, grp, rho, k_all, step_H, mask, n_kept, sl, nullptr,
+                            nullptr);
+    }
 }
 
 // ------------------------------------------------------------------------
@@ -853,6 +899,36 @@ __device__ __forceinline__ void count_kept(const int32_t* __restrict__ off,
     }
 }
 
+// N and K from offsets and mask already in LDS (as count_kept stages them).
+template <int THREADS>
+__device__ __forceinline__ void count_kept_lds(const int32_t* off_l, const uint8_t* mask_l,
+                                               int64_t S, int64_t (*red)[THREADS / 64],
+                                               int64_t& N, int64_t& K) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    int64_t n_local = 0, k_local = 0;
+    // step s ends at max(off_l[s + 1], off_l[s]): the clamped end of step_bounds
+    for (int64_t s = tid; s < S; s += THREADS)
+        if (mask_l[s]) {
+            n_local += (int64_t)max(off_l[s + 1], off_l[s]) - off_l[s];
+            k_local += 1;
+        }
+    n_local = wave_sum_i64(n_local);
+    k_local = wave_sum_i64(k_local);
+    if (lane == 0) {
+        red[0][wave] = n_local;
+        red[1][wave] = k_local;
+    }
+    lds_barrier();
+    N = 0;
+    K = 0;
+    for (int i = 0; i < THREADS / 64; ++i) {
+        N += red[0][i];
+        K += red[1][i];
+    }
+}
+
 // Sums the kParts per-lane values over the block in a fixed order (butterfly
 // within each wave, then a butterfly over the wave totals in wave 0); the
 // result is valid in thread 0.
@@ -869,7 +945,7 @@ __device__ __forceinline__ void block_sum_parts(double (&acc)[kParts],
     if (lane == 0)
 #pragma unroll
         for (int i = 0; i < kParts; ++i) red[i][wave] = acc[i];
-    __syncthreads();
+    lds_barrier();
     if (wave == 0)
 #pragma unroll
         for (int i = 0; i < kParts; ++i) acc[i] = wave_sum(lane < WAVES ? red[i][lane] : 0.0);
@@ -895,46 +971,76 @@ __device__ __forceinline__ void write_loss(const double (&acc)[kParts], double N
 // part != null each workgroup writes its partial sums there (workgroup 0 also
 // N and K); with part == null the grid is one workgroup, which writes the loss
 // and stats itself.
-template <bool GENERAL, int THREADS>
-__global__ void __launch_bounds__(THREADS)
-tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
-                const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
-                const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
-                const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
-                double* __restrict__ part, double* __restrict__ loss, float* __restrict__ stats,
-                int nstats) {
+template <int THREADS>
+struct CoefRed {
+    int64_t i[2][THREADS / 64];
+    double d[kParts][THREADS / 64];
+};
+
+// The lane's tokens of one chunk of THREADS * kCoefBatch tokens (zeros past T).
+struct CoefTokens {
+    float A[kCoefBatch], lp[kCoefBatch], lpo[kCoefBatch], lpr[kCoefBatch], lpf[kCoefBatch];
+};
+
+template <int THREADS>
+__device__ __forceinline__ void load_coef_tokens(CoefTokens& x, int64_t c, int64_t T,
+                                                 const float* __restrict__ logp,
+                                                 const float* __restrict__ lp_old,
+                                                 const float* __restrict__ lp_roll,
+                                                 const float* __restrict__ lp_ref,
+                                                 const float* __restrict__ adv, bool with_kl) {
     constexpr int CHUNK = THREADS * kCoefBatch;
-    __shared__ int32_t off_l[kCoefLdsSteps + 1];
-    __shared__ uint8_t mask_l[kCoefLdsSteps];
-    __shared__ int64_t red_i[2][THREADS / 64];
-    __shared__ double red_d[kParts][THREADS / 64];
+#pragma unroll
+    for (int j = 0; j < kCoefBatch; ++j) {
+        const int64_t t = c * CHUNK + threadIdx.x + (int64_t)j * THREADS;
+        x.A[j] = x.lp[j] = x.lpo[j] = x.lpr[j] = x.lpf[j] = 0.f;
+        if (t < T) {
+            x.A[j] = adv[t];
+            x.lp[j] = logp[t];
+            x.lpo[j] = lp_old[t];
+            x.lpr[j] = lp_roll[t];
+            if (with_kl) x.lpf[j] = lp_ref[t];
+        }
+    }
+}
+
+// PRE: the caller has put the clamped offsets (off_l[s] = first token of step
+// s, off_l[S] = T) and the mask in LDS (S <= kCoefLdsSteps) and loaded this
+// workgroup's first chunk into x; else both happen here.
+template <bool GENERAL, int THREADS, bool PRE = false>
+__device__ __forceinline__ void coef_tokens(
+    int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
+    const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
+    const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
+    const uint8_t* __restrict__ mask, const LossConfig& cfg, float* __restrict__ coef,
+    double* __restrict__ part, double* __restrict__ loss, float* __restrict__ stats, int nstats,
+    int32_t* off_l, uint8_t* mask_l, CoefRed<THREADS>& red, CoefTokens& x) {
+    constexpr int CHUNK = THREADS * kCoefBatch;
+    auto& red_i = red.i;
+    auto& red_d = red.d;
 
     const int tid = threadIdx.x;
     const bool with_kl = GENERAL && cfg.kl != DART_KL_NONE;
     const int64_t nchunks = (T + CHUNK - 1) / CHUNK;
     // the lane's tokens of a chunk: loaded before they are needed (the first
     // chunk's loads are in flight while the kept counts are taken)
-    float A[kCoefBatch], lp[kCoefBatch], lpo[kCoefBatch], lpr[kCoefBatch], lpf[kCoefBatch];
+    float(&A)[kCoefBatch] = x.A;
+    float(&lp)[kCoefBatch] = x.lp;
+    float(&lpo)[kCoefBatch] = x.lpo;
+    float(&lpr)[kCoefBatch] = x.lpr;
+    float(&lpf)[kCoefBatch] = x.lpf;
     auto load_chunk = [&](int64_t c) {
-#pragma unroll
-        for (int j = 0; j < kCoefBatch; ++j) {
-            const int64_t t = c * CHUNK + tid + (int64_t)j * THREADS;
-            A[j] = lp[j] = lpo[j] = lpr[j] = lpf[j] = 0.f;
-            if (t < T) {
-                A[j] = adv[t];
-                lp[j] = logp[t];
-                lpo[j] = lp_old[t];
-                lpr[j] = lp_roll[t];
-                if (with_kl) lpf[j] = lp_ref[t];
-            }
-        }
+        load_coef_tokens<THREADS>(x, c, T, logp, lp_old, lp_roll, lp_ref, adv, with_kl);
     };
-    if ((int64_t)blockIdx.x < nchunks) load_chunk(blockIdx.x);
+    if (!PRE && (int64_t)blockIdx.x < nchunks) load_chunk(blockIdx.x);
 
-    const bool staged = S <= kCoefLdsSteps;
+    const bool staged = PRE || S <= kCoefLdsSteps;
     int64_t N, K;
-    count_kept<THREADS>(off, mask, S, T, staged ? off_l : nullptr, staged ? mask_l : nullptr,
-                        red_i, N, K);
+    if constexpr (PRE)
+        count_kept_lds<THREADS>(off_l, mask_l, S, red_i, N, K);
+    else
+        count_kept<THREADS>(off, mask, S, T, staged ? off_l : nullptr, staged ? mask_l : nullptr,
+                            red_i, N, K);
     if (part && blockIdx.x == 0 && tid == 0) {
         part[(int64_t)gridDim.x * kParts] = (double)N;
         part[(int64_t)gridDim.x * kParts + 1] = (double)K;
@@ -1027,6 +1133,54 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
         for (int i = 0; i < kParts; ++i) part[(int64_t)blockIdx.x * kParts + i] = acc[i];
     else
         write_loss(acc, (double)N, (double)K, loss, stats, nstats);
+}
+
+template <bool GENERAL, int THREADS>
+__global__ void __launch_bounds__(THREADS)
+tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restrict__ lp_old,
+                const float* __restrict__ lp_roll, const float* __restrict__ lp_ref,
+                const float* __restrict__ adv, const int32_t* __restrict__ off, int64_t S,
+                const uint8_t* __restrict__ mask, LossConfig cfg, float* __restrict__ coef,
+                double* __restrict__ part, double* __restrict__ loss, float* __restrict__ stats,
+                int nstats) {
+    __shared__ int32_t off_l[kCoefLdsSteps + 1];
+    __shared__ uint8_t mask_l[kCoefLdsSteps];
+    __shared__ CoefRed<THREADS> red;
+    CoefTokens x;
+    coef_tokens<GENERAL, THREADS>(T, logp, lp_old, lp_roll, lp_ref, adv, off, S, mask, cfg, coef,
+                                  part, loss, stats, nstats, off_l, mask_l, red, x);
+}
+
+// Step selection and token coefficients of one group in one workgroup (T <=
+// kSelLdsTokens, S <= kSelLdsKeys, token ratios, token mean over kept
+// tokens): select_steps with the means fused in, then coef_tokens of the
+// one-workgroup launch, the two sharing the staged offsets. Its outputs are
+// those of step_select_kernel<true> followed by tis_coef_kernel<false,
+// kCoefOneThreads>, bit for bit.
+__global__ void __launch_bounds__(kSelThreads)
+select_coef_kernel(const float* __restrict__ H, int64_t T, const int32_t* __restrict__ off,
+                   int64_t S, double rho, int64_t k, float* __restrict__ step_H,
+                   uint8_t* __restrict__ mask, int32_t* __restrict__ n_kept,
+                   const float* __restrict__ logp, const float* __restrict__ lp_old,
+                   const float* __restrict__ lp_roll, const float* __restrict__ adv,
+                   LossConfig cfg, float* __restrict__ coef, double* __restrict__ loss,
+                   float* __restrict__ stats, int nstats) {
+    static_assert(kSelThreads == kCoefOneThreads, "one workgroup size for both parts");
+    static_assert(kSelLdsKeys <= kCoefLdsSteps, "the staged offsets serve both parts");
+    __shared__ SelLds sl;
+    __shared__ float H_l[kSelLdsTokens];
+    __shared__ int32_t off_l[kSelLdsKeys + 1];
+    __shared__ uint8_t mask_l[kCoefLdsSteps];
+    __shared__ CoefRed<kCoefOneThreads> red;
+    // the first chunk of tokens is in flight during the selection
+    CoefTokens x;
+    load_coef_tokens<kCoefOneThreads>(x, 0, T, logp, lp_old, lp_roll, nullptr, adv, false);
+    select_steps<true>(H, T, off, S, nullptr, rho, k, step_H, mask, n_kept, sl, H_l, off_l,
+                       mask_l);
+    lds_barrier();  // the staged offsets and the mask in LDS
+    coef_tokens<false, kCoefOneThreads, true>(T, logp, lp_old, lp_roll, nullptr, adv, off, S,
+                                              mask, cfg, coef, nullptr, loss, stats, nstats,
+                                              off_l, mask_l, red, x);
 }
 
 // Step ratios: one workgroup, one wave per step, the step's sums first.
@@ -1300,6 +1454,21 @@ bool bad_fwd_bwd_args(const void* logits, dart_dtype_t dtype, int64_t T, int64_t
     return bad_overlap(logits, ld, dlogits, ld_out, T, V, es);
 }
 
+// The loss of dart_tis_loss_fwd: token ratios, token mean over kept tokens,
+// no KL term.
+LossConfig plain_loss_config(float eps_low, float eps_high, float C) {
+    LossConfig cfg;
+    cfg.eps_low = eps_low;
+    cfg.eps_high = eps_high;
+    cfg.C = C;
+    cfg.log_C = isinf(C) ? INFINITY : (float)log((double)C);
+    cfg.kl = DART_KL_NONE;
+    cfg.beta = 0.f;
+    cfg.agg = DART_AGG_TOKEN_MEAN;
+    cfg.ratio = DART_RATIO_TOKEN;
+    return cfg;
+}
+
 }  // namespace
 
 // Scratch of dart_tis_loss_fwd_bwd_noalloc: the loss kernels' per-workgroup
@@ -1519,17 +1688,46 @@ dart_status_t dart_tis_loss_fwd(int64_t T, const float* logp, const float* logp_
             stream, {{dart_check::Item::Offsets, step_offsets, S, T},
                      {dart_check::Item::Mask, step_mask, S, 0}}); ck != DART_OK)
         return ck;
-    LossConfig cfg;
-    cfg.eps_low = eps_low;
-    cfg.eps_high = eps_high;
-    cfg.C = C;
-    cfg.log_C = isinf(C) ? INFINITY : (float)log((double)C);
-    cfg.kl = DART_KL_NONE;
-    cfg.beta = 0.f;
-    cfg.agg = DART_AGG_TOKEN_MEAN;
-    cfg.ratio = DART_RATIO_TOKEN;
     return launch_tis_coef(false, T, logp, logp_old, logp_rollout, nullptr, adv, step_offsets, S,
-                           step_mask, cfg, tok_coef, loss, stats, 4, workspace, stream);
+                           step_mask, plain_loss_config(eps_low, eps_high, C), tok_coef, loss,
+                           stats, 4, workspace, stream);
+}
+
+dart_status_t dart_select_tis_loss_fwd(int64_t T, const float* entropy, const float* logp,
+                                       const float* logp_old, const float* logp_rollout,
+                                       const float* adv, const int32_t* step_offsets, int64_t S,
+                                       double rho, float eps_low, float eps_high, float C,
+                                       float* step_entropy, uint8_t* step_mask,
+                                       int32_t* n_kept_steps, double* loss, float* tok_coef,
+                                       float* stats, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream) {
+    // the argument rules of dart_step_select and dart_tis_loss_fwd, all checked
+    // before anything is enqueued
+    if (!entropy || !step_offsets || !step_entropy || !step_mask || !logp || !logp_old ||
+        !logp_rollout || !adv || !loss || !tok_coef)
+        return DART_ERR_INVALID_ARG;
+    if (T < 1 || S < 1 || S > T || T > 0x7FFFFFFFll) return DART_ERR_INVALID_ARG;
+    const int64_t k = dart_kept_steps(S, rho);
+    if (k < 0) return DART_ERR_INVALID_ARG;
+    if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
+    if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
+    if (T > kSelLdsTokens || S > kSelLdsKeys) {
+        // too large for one workgroup: the two calls in turn
+        const dart_status_t st = dart_step_select(entropy, T, step_offsets, S, rho, step_entropy,
+                                                  step_mask, n_kept_steps, stream);
+        if (st != DART_OK) return st;
+        return dart_tis_loss_fwd(T, logp, logp_old, logp_rollout, adv, step_offsets, S, step_mask,
+                                 eps_low, eps_high, C, loss, tok_coef, stats, workspace,
+                                 workspace_bytes, stream);
+    }
+    if (const dart_status_t ck = dart_check::run(
+            stream, {{dart_check::Item::Offsets, step_offsets, S, T}}); ck != DART_OK)
+        return ck;
+    hipLaunchKernelGGL(select_coef_kernel, dim3(1), dim3(kSelThreads), 0, stream, entropy, T,
+                       step_offsets, S, rho, k, step_entropy, step_mask, n_kept_steps, logp,
+                       logp_old, logp_rollout, adv, plain_loss_config(eps_low, eps_high, C),
+                       tok_coef, loss, stats, 4);
+    return launch_status();
 }
 
 dart_status_t dart_tis_grad_ex(const void* logits, dart_dtype_t dtype, int64_t T, int64_t V,

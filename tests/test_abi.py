@@ -137,6 +137,33 @@ def test_tis_loss_noalloc_rejects_before_any_hip_call(kw):
     assert lib.dart_tis_loss_fwd_bwd_noalloc(*args, None) == dart.DART_ERR_INVALID_ARG
 
 
+def _select_loss_args(**kw):
+    a = dict(T=4, entropy=P, logp=P, lp_old=P, lp_roll=P, adv=P, off=P, S=2, rho=0.5,
+             eps_low=0.2, eps_high=0.2, C=2.0, step_entropy=P, mask=P, n_kept=0, loss=P, coef=P,
+             stats=0, workspace=0, workspace_bytes=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.skipif("_gpu_visible()")
+@pytest.mark.parametrize("kw", [
+    dict(entropy=0), dict(logp=0), dict(lp_old=0), dict(lp_roll=0), dict(adv=0), dict(off=0),
+    dict(step_entropy=0), dict(mask=0), dict(loss=0), dict(coef=0), dict(T=0), dict(T=1 << 31),
+    dict(S=0), dict(S=5), dict(rho=1.01), dict(rho=-0.01), dict(rho=float("nan")),
+    dict(eps_low=-0.1), dict(eps_high=float("nan")), dict(C=0.0), dict(C=float("nan")),
+    dict(workspace=1 << 24, workspace_bytes=55),  # one byte short for T = 4
+    dict(workspace=(1 << 24) + 4, workspace_bytes=1 << 16),  # not 8-byte aligned
+    # too large for one workgroup: still rejected before the two calls begin
+    dict(T=20000, S=20001), dict(T=20000, S=3, rho=2.0), dict(T=20000, S=3, C=-1.0),
+])
+def test_select_tis_loss_rejects(kw):
+    """The fused selection and loss call applies the rules of dart_step_select
+    and dart_tis_loss_fwd on the host before anything is enqueued."""
+    lib = dart.load_library()
+    assert lib.dart_select_tis_loss_fwd(*_select_loss_args(**kw), None) == \
+        dart.DART_ERR_INVALID_ARG
+
+
 def test_workspace_bytes():
     """kParts = 5 doubles per workgroup of 1024 tokens (at most 1024
     workgroups), then N and K."""

@@ -14,8 +14,9 @@ def _cuda(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
+@pytest.mark.parametrize("fused", [False, True])  # selection and loss in one call
 @pytest.mark.parametrize("T", [700, 6000])  # one-workgroup and many-workgroup loss
-def test_graph_replays_match_eager(T):
+def test_graph_replays_match_eager(T, fused):
     import torch
 
     import paper_2509_23866_amd as dart
@@ -42,9 +43,14 @@ def test_graph_replays_match_eager(T):
 
     def step(b, s=None):
         dart.dart_tok_stats(logits, target, b["logp"], b["ent"], b["lse"], stream=s)
-        dart.dart_step_select(b["ent"], off, 0.8, b["sh"], b["mask"], b["nk"], stream=s)
-        dart.dart_tis_loss_fwd(b["logp"], lp_old, lp_roll, adv, off, b["mask"], 0.2, 0.28, 2.0,
-                               b["loss"], b["coef"], b["st"], stream=s, workspace=b["ws"])
+        if fused:
+            dart.dart_select_tis_loss_fwd(b["ent"], b["logp"], lp_old, lp_roll, adv, off, 0.8,
+                                          0.2, 0.28, 2.0, b["sh"], b["mask"], b["nk"], b["loss"],
+                                          b["coef"], b["st"], stream=s, workspace=b["ws"])
+        else:
+            dart.dart_step_select(b["ent"], off, 0.8, b["sh"], b["mask"], b["nk"], stream=s)
+            dart.dart_tis_loss_fwd(b["logp"], lp_old, lp_roll, adv, off, b["mask"], 0.2, 0.28,
+                                   2.0, b["loss"], b["coef"], b["st"], stream=s, workspace=b["ws"])
         dart.dart_tis_grad(logits, target, b["logp"], b["lse"], b["coef"], b["dz"], stream=s)
 
     eager = buffers()
