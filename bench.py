@@ -3,7 +3,7 @@
 
 One step = one pass of the whole path over one step group held in HBM:
 dart_tok_stats -> dart_select_tis_loss_fwd (step means, selection, coefficients
-and loss; one launch up to 16384 tokens) -> dart_tis_grad, on one stream. The K timed steps run back to back; per-kernel durations come from
+and loss; one launch up to 4096 tokens) -> dart_tis_grad, on one stream. The K timed steps run back to back; per-kernel durations come from
 a second pass of K steps with HIP events around each kernel. The default workload is the 7B-VLM vocabulary group: T = 4096
 action tokens in 64 steps, V = 152064, bf16 logits, separate gradient buffer.
 

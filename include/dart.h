@@ -203,8 +203,9 @@ dart_status_t dart_tis_grad(const void* logits, dart_dtype_t dtype, int64_t T, i
 
 /* dart_step_select followed by dart_tis_loss_fwd on the mask it selects: the
  * step means and top-rho selection of Sec. 4.3, then the coefficients and loss
- * of Eq. (2), in one launch of one workgroup when T <= 16384 and S <= 8192
- * (both calls' work back to back, without the kernel boundaries between them);
+ * of Eq. (2), in one launch of one workgroup when T <= 4096 and S <= 8192
+ * (both calls' work back to back, without the kernel boundaries between them;
+ * beyond ~5000 tokens the one workgroup is slower than the two calls' launches);
  * larger problems make the two calls in turn.
  *   Arguments: entropy, T, step_offsets, S, rho, step_entropy, step_mask,
  *              n_kept_steps as for dart_step_select (step_mask is an output);

@@ -399,8 +399,8 @@ def dart_select_tis_loss_fwd(entropy, logp, logp_old, logp_rollout, adv, step_of
                              eps_low, eps_high, C, step_entropy=None, step_mask=None,
                              n_kept_steps=None, loss=None, tok_coef=None, stats=None,
                              with_stats=True, stream=None, workspace="auto"):
-    """dart_step_select then dart_tis_loss_fwd in one call (one launch when the
-    problem fits one workgroup). Returns (step_entropy, step_mask,
+    """dart_step_select then dart_tis_loss_fwd in one call (one launch up to
+    4096 tokens and 8192 steps). Returns (step_entropy, step_mask,
     n_kept_steps, loss, tok_coef, stats). ``workspace`` as for
     dart_tis_loss_fwd_bwd."""
     torch = _torch()

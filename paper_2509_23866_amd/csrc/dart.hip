@@ -823,6 +823,11 @@ constexpr int kCoefMaxBlocks = 1024;
 // MI355X: at T = 512 one workgroup saves ~2.5 us a step; at T = 4096 the
 // many-workgroup launch saves ~5 us.
 constexpr int64_t kCoefOneBlockMaxT = 2048;
+// up to this many tokens the selection and the loss run in one workgroup in
+// dart_select_tis_loss_fwd. Measured on MI355X (back to back, S = T / 64):
+// 11.0 vs 14.8 us for the two calls at T = 2048, 14.2 vs 16.6 at 4096, 21.0 vs
+// 17.7 at 6144, 44 vs 29 at 16384 (the one workgroup's arithmetic grows with T).
+constexpr int64_t kSelCoefMaxT = 4096;
 constexpr int kCoefLdsSteps = 8192;  // offsets and mask of up to this many steps go to LDS
 constexpr int kStepCoefThreads = 1024;
 constexpr int kStepCoefWaves = kStepCoefThreads / 64;
@@ -1152,8 +1157,8 @@ tis_coef_kernel(int64_t T, const float* __restrict__ logp, const float* __restri
 }
 
 // Step selection and token coefficients of one group in one workgroup (T <=
-// kSelLdsTokens, S <= kSelLdsKeys, token ratios, token mean over kept
-// tokens): select_steps with the means fused in, then coef_tokens of the
+// kSelCoefMaxT <= kSelLdsTokens, S <= kSelLdsKeys, token ratios, token mean
+// over kept tokens): select_steps with the means fused in, then coef_tokens of the
 // one-workgroup launch, the two sharing the staged offsets. Its outputs are
 // those of step_select_kernel<true> followed by tis_coef_kernel<false,
 // kCoefOneThreads>, bit for bit.
@@ -1166,6 +1171,7 @@ select_coef_kernel(const float* __restrict__ H, int64_t T, const int32_t* __rest
                    LossConfig cfg, float* __restrict__ coef, double* __restrict__ loss,
                    float* __restrict__ stats, int nstats) {
     static_assert(kSelThreads == kCoefOneThreads, "one workgroup size for both parts");
+    static_assert(kSelCoefMaxT <= kSelLdsTokens, "the entropies fit the selection's LDS");
     static_assert(kSelLdsKeys <= kCoefLdsSteps, "the staged offsets serve both parts");
     __shared__ SelLds sl;
     __shared__ float H_l[kSelLdsTokens];
@@ -1711,8 +1717,8 @@ dart_status_t dart_select_tis_loss_fwd(int64_t T, const float* entropy, const fl
     if (k < 0) return DART_ERR_INVALID_ARG;
     if (!(eps_low >= 0.f) || !(eps_high >= 0.f) || !(C > 0.f)) return DART_ERR_INVALID_ARG;
     if (bad_workspace(workspace, workspace_bytes, T)) return DART_ERR_INVALID_ARG;
-    if (T > kSelLdsTokens || S > kSelLdsKeys) {
-        // too large for one workgroup: the two calls in turn
+    if (T > kSelCoefMaxT || S > kSelLdsKeys) {
+        // beyond what one workgroup does faster: the two calls in turn
         const dart_status_t st = dart_step_select(entropy, T, step_offsets, S, rho, step_entropy,
                                                   step_mask, n_kept_steps, stream);
         if (st != DART_OK) return st;

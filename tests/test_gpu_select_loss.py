@@ -5,7 +5,7 @@ dart_tis_loss_fwd gives: the step means, mask, kept count and coefficients bit
 for bit; the loss bit for bit against the one-workgroup loss and within 1e-12
 of the many-workgroup one; and it matches the oracle's selection (exactly, on
 the same float32 entropies) and loss. The layouts reach both sides of the
-one-workgroup limits (16384 tokens, 8192 steps) and of the selection's
+one-workgroup limits (4096 tokens, 8192 steps) and of the selection's
 direct-rank limit (256 steps), ties between step means, rho 0 and 1, and
 steps of one token."""
 
@@ -47,18 +47,20 @@ def _inputs(rng, lens, tie_frac=0.3):
 
 
 CASES = [
-    # (name, step lengths, rho); T <= 16384 and S <= 8192 run in one workgroup
+    # (name, step lengths, rho); T <= 4096 and S <= 8192 run in one workgroup
     ("one_token", lambda r: np.ones(1, np.int64), 0.5),
-    ("vlm7b_steps", lambda r: r.integers(16, 129, 64), 0.8),
-    ("rank_limit_256", lambda r: r.integers(1, 65, 256), 0.5),
-    ("radix_257", lambda r: r.integers(1, 65, 257), 0.5),
+    ("vlm7b_steps", lambda r: r.integers(16, 33, 64), 0.8),
+    ("rank_limit_256", lambda r: r.integers(1, 17, 256), 0.5),
+    ("radix_257", lambda r: r.integers(1, 16, 257), 0.5),
     ("rho_zero", lambda r: r.integers(1, 40, 37), 0.0),
     ("rho_one", lambda r: r.integers(1, 40, 37), 1.0),
-    ("max_fit", lambda r: np.full(8192, 2, np.int64), 0.8),
-    ("microbatch_steps", lambda r: r.integers(64, 129, 128), 0.8),
+    ("max_tokens", lambda r: np.r_[np.full(63, 64, np.int64), [4096 - 63 * 64]], 0.8),
+    ("steps_of_one_4096", lambda r: np.ones(4096, np.int64), 0.8),
     # past the limits: the two calls in turn
-    ("tokens_16385", lambda r: np.r_[np.full(99, 165, np.int64), [16385 - 99 * 165]], 0.8),
+    ("tokens_4097", lambda r: np.r_[np.full(63, 64, np.int64), [4097 - 63 * 64]], 0.8),
+    ("vlm7b_4600", lambda r: r.integers(16, 129, 64), 0.8),
     ("steps_8193", lambda r: np.ones(8193, np.int64), 0.3),
+    ("microbatch_steps", lambda r: r.integers(64, 129, 128), 0.8),
 ]
 
 
@@ -88,7 +90,7 @@ def test_fused_equals_the_two_calls_and_the_oracle(name, gen, rho, ws):
     assert np.array_equal(bits(mask), bits(mask2))
     assert int(nk.item()) == int(nk2.item())
     assert np.array_equal(bits(coef), bits(coef2))
-    one_wg = T <= 16384 and S <= 8192
+    one_wg = T <= 4096 and S <= 8192
     if ws is None or not one_wg or T <= 2048:
         # the same summation order on both sides
         assert np.array_equal(bits(loss), bits(loss2)) and np.array_equal(bits(st), bits(st2))
