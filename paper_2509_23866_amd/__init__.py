@@ -778,12 +778,12 @@ def lmhead_backward_plan(T: int, V: int, budget_bytes: int = 512 << 20):
 
 def policy_update(logits, target, logp_old, logp_rollout, adv, step_offsets, rho, eps_low,
                   eps_high, C, dlogits=None, stream=None):
-    """tok_stats -> step_select -> tis_loss_fwd_bwd on one stream. Returns a dict
+    """tok_stats -> select_tis_loss_fwd -> tis_grad on one stream. Returns a dict
     of device tensors (nothing is synchronised)."""
     logp, ent, lse = dart_tok_stats(logits, target, stream=stream)
-    step_ent, mask, n_kept = dart_step_select(ent, step_offsets, rho, stream=stream)
-    loss, dz, coef, stats = dart_tis_loss_fwd_bwd(
-        logits, target, logp, lse, logp_old, logp_rollout, adv, step_offsets, mask, eps_low,
-        eps_high, C, dlogits=dlogits, stream=stream)
+    step_ent, mask, n_kept, loss, coef, stats = dart_select_tis_loss_fwd(
+        ent, logp, logp_old, logp_rollout, adv, step_offsets, rho, eps_low, eps_high, C,
+        stream=stream)
+    dz = dart_tis_grad(logits, target, logp, lse, coef, dlogits, stream=stream)
     return dict(logp=logp, entropy=ent, lse=lse, step_entropy=step_ent, step_mask=mask,
                 n_kept_steps=n_kept, loss=loss, dlogits=dz, tok_coef=coef, stats=stats)

@@ -27,8 +27,7 @@ that lmhead_backward_plan picks for a 512 MiB workspace.
 import torch
 
 from . import (DART_LMHEAD_BF16_GRADS, dart_lmhead_backward_ex, dart_lmhead_tok_stats_ex,
-               dart_step_select, dart_tis_grad, dart_tis_loss_fwd, dart_tok_stats,
-               lmhead_backward_plan)
+               dart_select_tis_loss_fwd, dart_tis_grad, dart_tok_stats, lmhead_backward_plan)
 
 
 def _scaled(coef, grad):
@@ -40,9 +39,9 @@ def _scaled(coef, grad):
 
 
 def _loss(logp, ent, logp_old, logp_rollout, adv, step_offsets, rho, eps_low, eps_high, C):
-    _, mask, _ = dart_step_select(ent, step_offsets, rho)
-    loss, coef, _ = dart_tis_loss_fwd(logp, logp_old, logp_rollout, adv, step_offsets, mask,
-                                      eps_low, eps_high, C, with_stats=False)
+    _, _, _, loss, coef, _ = dart_select_tis_loss_fwd(ent, logp, logp_old, logp_rollout, adv,
+                                                      step_offsets, rho, eps_low, eps_high, C,
+                                                      with_stats=False)
     return loss.reshape(()), coef
 
 
