@@ -113,19 +113,28 @@ class GpuSide:
         self.eps_low, self.eps_high, self.C = ors.eps_low, ors.eps_high, ors.C
         del recipe
 
-    def run(self, mask=None, keep_rows=None):
+    def run(self, mask=None, keep_rows=None, fused=True):
         """One pass; ``mask`` (numpy) replaces the GPU's own selection as the
-        input of the loss call. Returns numpy outputs; dlogits only for
+        input of the loss call. With the GPU's own selection and ``fused`` the
+        pass is the benchmark's: dart_tok_stats -> dart_select_tis_loss_fwd ->
+        dart_tis_grad; else dart_tok_stats -> dart_step_select ->
+        dart_tis_loss_fwd_bwd. Returns numpy outputs; dlogits only for
         ``keep_rows`` (all rows if None)."""
         torch, dart = self.torch, self.dart
         logp, ent, lse = dart.dart_tok_stats(self.logits, self.target)
-        step_H, step_mask, n_kept = dart.dart_step_select(ent, self.off, self.wl.rho)
-        use_mask = step_mask if mask is None else torch.from_numpy(
-            np.ascontiguousarray(mask, dtype=np.uint8)).to(self.logits.device)
         dl = self.logits if self.inplace else None
-        loss, dz, coef, stats = dart.dart_tis_loss_fwd_bwd(
-            self.logits, self.target, logp, lse, self.lp_old, self.lp_roll, self.adv, self.off,
-            use_mask, self.eps_low, self.eps_high, self.C, dlogits=dl)
+        if mask is None and fused:
+            step_H, step_mask, n_kept, loss, coef, stats = dart.dart_select_tis_loss_fwd(
+                ent, logp, self.lp_old, self.lp_roll, self.adv, self.off, self.wl.rho,
+                self.eps_low, self.eps_high, self.C)
+            dz = dart.dart_tis_grad(self.logits, self.target, logp, lse, coef, dlogits=dl)
+        else:
+            step_H, step_mask, n_kept = dart.dart_step_select(ent, self.off, self.wl.rho)
+            use_mask = step_mask if mask is None else torch.from_numpy(
+                np.ascontiguousarray(mask, dtype=np.uint8)).to(self.logits.device)
+            loss, dz, coef, stats = dart.dart_tis_loss_fwd_bwd(
+                self.logits, self.target, logp, lse, self.lp_old, self.lp_roll, self.adv,
+                self.off, use_mask, self.eps_low, self.eps_high, self.C, dlogits=dl)
         torch.cuda.synchronize()
         rows = slice(None) if keep_rows is None else torch.from_numpy(
             np.asarray(keep_rows, dtype=np.int64)).to(self.logits.device)

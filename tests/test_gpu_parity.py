@@ -18,11 +18,11 @@ from tests import _harness as H
 pytestmark = pytest.mark.gpu
 
 
-def _full_check(wl, ld=None, misalign=0, inplace=None, dz_rows=None):
+def _full_check(wl, ld=None, misalign=0, inplace=None, dz_rows=None, fused=True):
     ors = H.OracleSide(wl)
     gpu_side = H.GpuSide(wl, ors, ld=ld, misalign=misalign, inplace=inplace)
     rows = dz_rows if dz_rows is not None else np.arange(wl.T)
-    gpu = gpu_side.run(keep_rows=rows)
+    gpu = gpu_side.run(keep_rows=rows, fused=fused)
     stats_err = H.check_token_stats(gpu, ors)
     same_mask = H.check_mask(gpu, ors)
     res = ors.res
@@ -115,11 +115,12 @@ def test_strided_and_unaligned_rows(dtype, V, ld, misalign):
     _full_check(wl, ld=ld, misalign=misalign, inplace=True)
 
 
+@pytest.mark.parametrize("fused", [True, False])  # the benchmark's calls, and the separate ones
 @pytest.mark.parametrize("name", ["tiny", "vlm7b", "edge"])
-def test_named_workload(name):
+def test_named_workload(name, fused):
     wl = synth.make_workload(name)
     rows = None if wl.T * wl.V <= (1 << 22) else H.sample_rows(wl, _oracle_g_placeholder(wl))
-    _full_check(wl, dz_rows=rows)
+    _full_check(wl, dz_rows=rows, fused=fused)
 
 
 def _oracle_g_placeholder(wl):
