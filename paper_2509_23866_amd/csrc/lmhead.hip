@@ -208,22 +208,43 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
     const uint32_t qstride_b = (uint32_t)(C::WAVES * C::LROWS * ldb * 2);
     const __amdgpu_buffer_rsrc_t rsrc_a = tile_rsrc(A + m0 * lda, (M - m0) * lda * 2);
     const __amdgpu_buffer_rsrc_t rsrc_b = tile_rsrc(B + n0 * ldb, (N - n0) * ldb * 2);
-    auto lds_a = [&](int buf, int q) { return &sm.in.a[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
-    auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][(q * C::WAVES + wave) * C::LROWS][0]; };
+    // rows of instruction q of wave `wave + hh * HW`
+    auto lds_a = [&](int buf, int q, int hh) {
+        return &sm.in.a[buf][(q * C::WAVES + wave + hh * (C::WAVES / 2)) * C::LROWS][0];
+    };
+    auto lds_b = [&](int buf, int q, int hh) {
+        return &sm.in.b[buf][(q * C::WAVES + wave + hh * (C::WAVES / 2)) * C::LROWS][0];
+    };
     const int64_t nk = (K + BK - 1) / BK;
     // slice kt into buffer buf; a slice that ends past K reads chunks past K
     // (in the row padding, the next row or, at the end, as zero) that are
     // zeroed after landing
+    // The first half of the waves (one per SIMD) issue every load of a
+    // slice: their own rows and those of the wave HW above, with the same lane
+    // offsets (the rows between them are a whole number of swizzle periods).
+    // Issuing a slice's 64 loads holds each issuing wave for ~700 cycles; the
+    // other wave of its SIMD multiplies meanwhile.
+    constexpr int HW = C::WAVES / 2;
+    static_assert((HW * C::LROWS) % 16 == 0, "swizzle period");
+    const uint32_t hstride_a = (uint32_t)(HW * C::LROWS * lda * 2);
+    const uint32_t hstride_b = (uint32_t)(HW * C::LROWS * ldb * 2);
     auto issue = [&](int64_t kt, int buf) {
+        if (wave >= HW) return;
         const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
         for (int q = 0; q < C::IA; ++q)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_a, lds_ptr(lds_a(buf, q)), 16, voff_a,
-                                                    kb + q * qstride_a, 0, 0);
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_a, lds_ptr(lds_a(buf, q, hh)), 16,
+                                                        voff_a, kb + q * qstride_a + hh * hstride_a,
+                                                        0, 0);
 #pragma unroll
         for (int q = 0; q < C::IB; ++q)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_b, lds_ptr(lds_b(buf, q)), 16, voff_b,
-                                                    kb + q * qstride_b, 0, 0);
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_b, lds_ptr(lds_b(buf, q, hh)), 16,
+                                                        voff_b, kb + q * qstride_b + hh * hstride_b,
+                                                        0, 0);
     };
     // a partial last slice: zero the chunks past K
     auto zero_tail = [&](int64_t kt, int buf) {
@@ -691,31 +712,52 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
         return tile_rsrc(X + first, (end - first) * 2);
     };
 
-    auto lds_a = [&](int buf, int q) {
+    // instruction q of wave `wave + hh * HW`
+    constexpr int HW = C::WAVES / 2;
+    auto lds_a = [&](int buf, int q, int hh) {
         constexpr int per = A_KMAJ ? C::LROWS * BK : 2 * kTw;  // elements per instruction
-        return &sm.in.a[buf][0][0] + (q * C::WAVES + wave) * per;
+        return &sm.in.a[buf][0][0] + (q * C::WAVES + wave + hh * HW) * per;
     };
-    auto lds_b = [&](int buf, int q) { return &sm.in.b[buf][0][0] + (q * C::WAVES + wave) * 2 * kTw; };
+    auto lds_b = [&](int buf, int q, int hh) {
+        return &sm.in.b[buf][0][0] + (q * C::WAVES + wave + hh * HW) * 2 * kTw;
+    };
 
+    // As in gemm_tile, the first half of the waves issue every load, their
+    // own rows and those of the wave HW above (HW * LROWS K-major rows or
+    // 2 HW transposed rows further: whole swizzle periods, so the same lane
+    // offsets)
+    static_assert((HW * C::LROWS) % 16 == 0 && (2 * HW) % 4 == 0, "swizzle periods");
+    const uint32_t hstride_ak = (uint32_t)(HW * C::LROWS * lda * 2);
+    const uint32_t hstride_at = (uint32_t)(2 * HW * lda * 2);
+    const uint32_t hstride_b = (uint32_t)(2 * HW * ldb * 2);
     auto issue = [&](int64_t kt, int buf) {
+        if (wave >= HW) return;
         if constexpr (A_KMAJ) {
             const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
             for (int q = 0; q < C::IA; ++q)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_ak, lds_ptr(lds_a(buf, q)), 16,
-                                                        voff_a, kb + q * qstride_a, 0, 0);
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rsrc_ak, lds_ptr(lds_a(buf, q, hh)), 16, voff_a,
+                        kb + q * qstride_a + hh * hstride_ak, 0, 0);
         } else {
             const __amdgpu_buffer_rsrc_t ra = tr_rsrc(A, lda, m0, M, kt);
 #pragma unroll
             for (int q = 0; q < TQ; ++q)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, lds_ptr(lds_a(buf, q)), 16, voff_a,
-                                                        q * qstride_a, 0, 0);
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, lds_ptr(lds_a(buf, q, hh)), 16,
+                                                            voff_a, q * qstride_a + hh * hstride_at,
+                                                            0, 0);
         }
         const __amdgpu_buffer_rsrc_t rb = tr_rsrc(B, ldb, n0, N, kt);
 #pragma unroll
         for (int q = 0; q < TQ; ++q)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, lds_ptr(lds_b(buf, q)), 16, voff_b,
-                                                    q * qstride_b, 0, 0);
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, lds_ptr(lds_b(buf, q, hh)), 16, voff_b,
+                                                        q * qstride_b + hh * hstride_b, 0, 0);
     };
     // the partial last slice of a K-major A: k >= K set to 0, also inside the
     // chunk that straddles K (transposed operands read zero rows there)
