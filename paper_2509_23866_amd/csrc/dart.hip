@@ -16,6 +16,9 @@
 //                       loss coefficient; partial sums of the loss in fp64
 //                       (tis_coef_step_kernel: one workgroup, step-level ratios).
 //   tis_loss_finalize_kernel  adds the partial sums in a fixed order.
+//   select_coef_kernel  one workgroup: step_select_kernel's and tis_coef_kernel's
+//                       device code back to back (up to 4096 tokens), the
+//                       offsets and mask handed over in LDS.
 //   tis_grad_kernel     one workgroup per 4 KB chunk of a row; second streaming
 //                       pass writing coef * (onehot - softmax) in the logits dtype.
 // The two streaming kernels are HBM-bound (no matrix contraction anywhere):
