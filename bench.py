@@ -720,7 +720,10 @@ def main():
     threads = args.cpu_threads or min(CPU_SHARE, affinity)
 
     # every other workload first (in the same process; each one's buffers are
-    # freed before the next), then the headline workload
+    # freed before the next), then the headline workload; the oracle baselines
+    # run on the host after all of them, so that the GPU work follows the
+    # sweep without the ~25 s host-only pauses in between (during which the
+    # GPU's clocks fall, and 5 warm-up steps do not bring them back)
     sweep = {}
     if not args.headline_only:
         for name in SWEEP_ORDER:
@@ -728,17 +731,19 @@ def main():
                 continue
             wl = synth.make_workload(name)
             print(f"[bench] workload {name}: T={wl.T} V={wl.V}", file=sys.stderr, flush=True)
-            r = measure_workload(wl, args, dev, headline=False)
-            cpu = None if args.no_cpu_baseline else cpu_baseline(wl, threads)
-            sweep[name] = workload_summary(r, cpu)
+            sweep[name] = (wl, measure_workload(wl, args, dev, headline=False))
 
     wl = synth.make_workload(args.workload)
     print(f"[bench] headline {wl.name}: T={wl.T} V={wl.V}", file=sys.stderr, flush=True)
     r = measure_workload(wl, args, dev, headline=True)
+    sweep_lines = {}
+    for name, (swl, sr) in sweep.items():
+        scpu = None if args.no_cpu_baseline else cpu_baseline(swl, threads)
+        sweep_lines[name] = workload_summary(sr, scpu)
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl, threads)
     if cpu is not None:
         cpu["affinity_cores"] = affinity
-    workloads = {**sweep, wl.name: workload_summary(r, cpu)}
+    workloads = {**sweep_lines, wl.name: workload_summary(r, cpu)}
     workloads = {k: workloads[k] for k in ("tiny", "vlm7b", "microbatch", "longhorizon", "edge")
                  if k in workloads}
 
