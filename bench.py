@@ -722,8 +722,8 @@ def main():
     # every other workload first (in the same process; each one's buffers are
     # freed before the next), then the headline workload; the oracle baselines
     # run on the host after all of them, so that the GPU work follows the
-    # sweep without the ~25 s host-only pauses in between (during which the
-    # GPU's clocks fall, and 5 warm-up steps do not bring them back)
+    # sweep without the host-only pauses in between (~1.5-2 s each, during
+    # which the GPU's clocks fall, and 5 warm-up steps do not bring them back)
     sweep = {}
     if not args.headline_only:
         for name in SWEEP_ORDER:
