@@ -71,6 +71,28 @@ def test_step_offsets_malformed(checks_on, case):
     _invalid(e)
 
 
+@pytest.mark.parametrize("T", [40, 5000])  # one launch, and the two calls beyond 4096 tokens
+@pytest.mark.parametrize("case", ["repeat", "end", "decrease"])
+def test_select_loss_offsets_malformed(checks_on, case, T):
+    """The fused selection and loss call validates the offsets before either
+    part runs."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    off = np.array([0, 5, 12, 30, T], np.int32)
+    if case == "repeat":
+        off[2] = off[1]
+    elif case == "end":
+        off[-1] = T - 1
+    else:
+        off[2], off[3] = off[3], off[2]
+    v = [torch.rand(T, device="cuda") for _ in range(5)]
+    with pytest.raises(dart.DartError) as e:
+        dart.dart_select_tis_loss_fwd(*v, _cuda(off), 0.5, 0.2, 0.28, 2.0)
+    _invalid(e)
+
+
 def test_mask_values(checks_on):
     import torch
 
@@ -154,8 +176,10 @@ def test_valid_inputs_unchanged(monkeypatch):
         loss, dz, coef, st = dart.dart_tis_loss_fwd_bwd(
             logits, _cuda(target), logp, lse, lp_old, lp_old, torch.ones_like(logp), _cuda(off),
             mask, 0.2, 0.28, 2.0)
+        fused = dart.dart_select_tis_loss_fwd(ent, logp, lp_old, lp_old, torch.ones_like(logp),
+                                              _cuda(off), 0.6, 0.2, 0.28, 2.0)
         torch.cuda.synchronize()
-        outs.append([x.cpu() for x in (logp, ent, lse, sh, mask, nk, loss, dz, coef)])
+        outs.append([x.cpu() for x in (logp, ent, lse, sh, mask, nk, loss, dz, coef, *fused)])
     for a, b in zip(*outs):
         assert torch.equal(a, b)
     assert int(outs[0][5].item()) == dart.dart_kept_steps(S, 0.6)
