@@ -6,9 +6,10 @@
 // entropy, the target's log-prob of Eq. 1) for logits z = h W^T, where h [T, d]
 // are the final hidden states of the T action tokens and W [V, d] the LM-head
 // weight of the policy (the 7B VLM of Sec. 5.1); the gradient is the chain
-// rule of Eq. 2's loss through them. Both kernels scale the fp32 tile by an
-// inverse sampling temperature before the epilogue (1 in the paper, App. A.4;
-// multiplying by 1 changes no bit).
+// rule of Eq. 2's loss through them. Both kernels apply an inverse sampling
+// temperature s (1 in the paper, App. A.4) in their epilogues: the fp32 tile
+// stays unscaled, and s enters the factor of the base-2 exponent (s log2 e)
+// and the row maximum (s > 0), so that s = 1 changes no bit.
 //
 //   lmhead_stats_kernel   one 256 x 256 tile of z per workgroup on MFMA
 //                         (v_mfma_f32_32x32x16_bf16, fp32 accumulation), K = d
@@ -264,18 +265,26 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
     // 2 ks + l / 32. The rows' swizzle depends only on l % 32 (blocks start at
     // multiples of 32), so one byte offset per k-step serves every block, the
     // block and the buffer entering as immediate offsets.
+    // The B offsets include the B buffers' start (64 KB into the LDS) and are
+    // kept opaque to the compiler, so that the buffer and the 32-column block
+    // enter as the read's 16-bit immediate (below 64 KB); folded into the
+    // immediate, they did not fit, and every B read cost an address add.
     uint32_t rda[C::KSTEPS], rdb[C::KSTEPS];
+    const char* const lds0 = reinterpret_cast<const char*>(&sm);
+    const uint32_t b_at = (uint32_t)(reinterpret_cast<const char*>(&sm.in.b[0][0][0]) - lds0);
 #pragma unroll
     for (int ks = 0; ks < C::KSTEPS; ++ks) {
         const int c = ks * 2 + (lane >> 5), ra = wr + (lane & 31), rb = wc + (lane & 31);
         rda[ks] = (uint32_t)(ra * BK + (c ^ swz<CH>(ra)) * 8) * 2;
-        rdb[ks] = (uint32_t)(rb * BK + (c ^ swz<CH>(rb)) * 8) * 2;
+        rdb[ks] = b_at + (uint32_t)(rb * BK + (c ^ swz<CH>(rb)) * 8) * 2;
+        asm volatile("" : "+v"(rdb[ks]));
     }
+    static_assert((C::NS - 1) * C::BN * BK * 2 + (C::TN - 1) * 32 * BK * 2 < 65536,
+                  "B read immediates");
     bf16x8 af[2][C::TM], bfr[2][C::TN];
     auto read_step = [&](auto bufc, int ks, int set) {
         constexpr int buf = decltype(bufc)::value;
         const char* ba = reinterpret_cast<const char*>(&sm.in.a[buf][0][0]);
-        const char* bb = reinterpret_cast<const char*>(&sm.in.b[buf][0][0]);
 #pragma unroll
         for (int i = 0; i < C::TM; ++i)
             af[set][i] = __builtin_bit_cast(
@@ -283,16 +292,23 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
             bfr[set][j] = __builtin_bit_cast(
-                bf16x8, *reinterpret_cast<const u32x4*>(bb + rdb[ks] + j * 32 * BK * 2));
+                bf16x8, *reinterpret_cast<const u32x4*>(lds0 + rdb[ks] + buf * C::BN * BK * 2 +
+                                                        j * 32 * BK * 2));
     };
-    auto mfmas = [&](int set) {
+    // the MFMAs of row blocks [i0, i1) of one k-step
+    auto mfmas = [&](int set, int i0 = 0, int i1 = C::TM) {
 #pragma unroll
         for (int i = 0; i < C::TM; ++i)
 #pragma unroll
             for (int j = 0; j < C::TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][i], bfr[set][j],
-                                                                    acc[i][j], 0, 0, 0);
+                if (i >= i0 && i < i1)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][i], bfr[set][j],
+                                                                        acc[i][j], 0, 0, 0);
     };
+    // Every wave holds back the last k-step's MFMAs of its last row block
+    // and issues them after the next slice's barrier (and its loads), while
+    // the first operand reads of that slice are in flight.
+    constexpr int LASTSET = (C::KSTEPS - 1) & 1;
 
     // two LDS buffers: slice kt+1 loads while slice kt is multiplied
     auto slice = [&](auto bufc, int64_t kt) {
@@ -309,11 +325,12 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
         // the operands of k-step ks+1 are read while the MFMAs of k-step ks issue
         read_step(bufc, 0, 0);
         __builtin_amdgcn_s_setprio(1);
+        if (kt > 0) mfmas(LASTSET, C::TM - 1, C::TM);
 #pragma unroll
         for (int ks = 0; ks < C::KSTEPS; ++ks) {
             const int cs = ks & 1;
             if (ks < C::KSTEPS - 1) read_step(bufc, ks + 1, cs ^ 1);
-            mfmas(cs);
+            mfmas(cs, 0, ks == C::KSTEPS - 1 ? C::TM - 1 : C::TM);
             if (ks < C::KSTEPS - 1) {
                 // interleave: one LDS read, then a share of the MFMAs
 #pragma unroll
@@ -335,6 +352,7 @@ __device__ __forceinline__ void gemm_tile(const uint16_t* __restrict__ A, int64_
         slice(std::integral_constant<int, 1>{}, kt + 1);
     }
     if (kt < nk) slice(std::integral_constant<int, 0>{}, kt);
+    mfmas(LASTSET, C::TM - 1, C::TM);
     __syncthreads();
 #else
     (void)A, (void)M, (void)lda, (void)B, (void)N, (void)ldb, (void)K, (void)m0, (void)n0;
@@ -382,15 +400,17 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
 #pragma unroll
     for (int ip = 0; ip < C::TM; ++ip) {
         const int e0 = ip * C::EPI;
-        if (ip) __syncthreads();
+        // LDS-only barriers: the workgroup exchanges nothing but LDS here, and a
+        // __syncthreads fence would also wait for the previous pass's stores
+        if (ip) lds_ring_barrier();
         // rows [e0, e0 + EPI) of the tile to LDS: row block ip of every wave
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
-                    acc[ip][j][v] * scale;
-        __syncthreads();
+                    acc[ip][j][v];
+        lds_ring_barrier();
         // P threads per row; thread p takes the 16-byte pieces p, p + P, ...
         // of the row (columns 16 c + 4 p + u) into registers: maximum over the
         // row's columns other than the target, then the sums in base-2 units
@@ -410,6 +430,9 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
         // only the tile's last columns past V and a row's target column drop
         // out: the selects run only in threads that hold such a column
         const bool masked = vlim < C::BN || (y32 >= 0 && ((y32 >> 2) & (P - 1)) == p);
+        // the tile stays unscaled in LDS: the inverse temperature enters the
+        // base-2 exponent's factor (1 at scale 1: the same bits)
+        const float c2 = scale * 1.4426950408889634f;
         Triple mine = {-INFINITY, 0.f, 0.f};
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
@@ -440,19 +463,30 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
             float mx = -INFINITY;
 #pragma unroll
             for (int i = 0; i < NH; ++i) mx = fmaxf(mx, x[i]);
-            Triple part_h = {mx, 0.f, 0.f};
+            // scale > 0: the maximum of the scaled row is the scaled maximum
+            Triple part_h = {mx * scale, 0.f, 0.f};
             if (mx > -INFINITY) {
-                // e = 2^xl with xl = (x - mx) log2(e) floored at -200, where 2^xl
-                // is already 0 in fp32, so that dropped columns add 0
-                constexpr float kLog2e = 1.4426950408889634f;
-                const float ml = mx * kLog2e;
+                // e = 2^xl with xl = (x - mx) scale log2(e); where a column was
+                // dropped (-inf) xl is floored at -200, where 2^xl is already 0
+                // in fp32, so that it adds 0 (other columns are finite)
+                const float ml = mx * c2;
                 float s2 = 0.f, w2 = 0.f;
+                if (masked) {
 #pragma unroll
-                for (int i = 0; i < NH; ++i) {
-                    const float xl = fmaxf(fmaf(x[i], kLog2e, -ml), -200.f);
-                    const float e = __builtin_amdgcn_exp2f(xl);
-                    s2 += e;
-                    w2 = fmaf(e, xl, w2);
+                    for (int i = 0; i < NH; ++i) {
+                        const float xl = fmaxf(fmaf(x[i], c2, -ml), -200.f);
+                        const float e = __builtin_amdgcn_exp2f(xl);
+                        s2 += e;
+                        w2 = fmaf(e, xl, w2);
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < NH; ++i) {
+                        const float xl = fmaf(x[i], c2, -ml);
+                        const float e = __builtin_amdgcn_exp2f(xl);
+                        s2 += e;
+                        w2 = fmaf(e, xl, w2);
+                    }
                 }
                 part_h.s = s2;
                 part_h.w = w2 * 0.6931471805599453f;
@@ -468,7 +502,7 @@ lmhead_stats_kernel(const uint16_t* __restrict__ h, int64_t T, int64_t ldh,
             mine = (p & off) ? merge(o, mine) : merge(mine, o);
         }
         if (t < T && p == 0) part[t * nvt + vt] = make_float4(mine.m, mine.s, mine.w, 0.f);
-        if (t < T && y32 >= 0 && ((y32 >> 2) & (P - 1)) == p) z_y[t] = sm.c[r][y32];
+        if (t < T && y32 >= 0 && ((y32 >> 2) & (P - 1)) == p) z_y[t] = sm.c[r][y32] * scale;
     }
 }
 
@@ -510,16 +544,21 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
     const int wr = (wave / C::WN) * 32, wc = (wave % C::WN) * (C::BN / C::WN);
     constexpr int CHUNKS = C::BN / 8;  // 16-byte output chunks per tile row
     static_assert(C::EPI == C::RS, "one row block of every wave per pass");
+    // the tile stays unscaled in LDS: the inverse temperature enters the
+    // base-2 exponent's factor (1 at scale 1: the same bits)
+    const float c2 = scale * 1.4426950408889634f;
 #pragma unroll
     for (int ip = 0; ip < C::TM; ++ip) {
         const int e0 = ip * C::EPI;
-        if (ip) __syncthreads();
+        // LDS-only barriers: a __syncthreads fence here would also wait for
+        // the previous pass's gradient stores
+        if (ip) lds_ring_barrier();
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
-                    acc[ip][j][v] * scale;
+                    acc[ip][j][v];
         // per-row constants: -g, -lse log2(e), the target's gradient
         // g (-expm1(logp)) (accurate when p_y -> 1), the target's column here;
         // g carries the inverse temperature (the chain rule through scale z)
@@ -534,7 +573,7 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
             }
             sm.rowp[tid] = rp;
         }
-        __syncthreads();
+        lds_ring_barrier();
         for (int e = tid; e < C::EPI * CHUNKS; e += C::THREADS) {
             const int r = e / CHUNKS, ch = e % CHUNKS;
             const int64_t t = m0 + e0 + r;
@@ -553,7 +592,7 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
             float dz[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
-                const float e2 = __builtin_amdgcn_exp2f(fmaf(xs[q], 1.4426950408889634f, rp.y));
+                const float e2 = __builtin_amdgcn_exp2f(fmaf(xs[q], c2, rp.y));
                 dz[q] = q == yc ? rp.z : rp.x * e2;
             }
             uint16_t* dst = out + t * ld_out + col0;
@@ -795,8 +834,19 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
 #pragma unroll
         for (int i = 0; i < C::TM; ++i) rda[i] = tr_off(wr + i * C::RS);
     }
+    // B's offsets carry its buffers' start (64 KB into the LDS), opaque to the
+    // compiler, so that the buffer, the k-step and the half enter as the
+    // read's 16-bit immediate (as in gemm_tile)
+    const char* const lds0 = reinterpret_cast<const char*>(&sm);
+    const uint32_t b_at = (uint32_t)(reinterpret_cast<const char*>(&sm.in.b[0][0][0]) - lds0);
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j) rdb[j] = tr_off(wc + j * 32);
+    for (int j = 0; j < C::TN; ++j) {
+        rdb[j] = b_at + tr_off(wc + j * 32);
+        asm volatile("" : "+v"(rdb[j]));
+    }
+    static_assert((C::NS - 1) * C::BN * BK * 2 + (C::KSTEPS - 1) * 16 * kTw * 2 + 4 * kTw * 2 <
+                      65536,
+                  "B read immediates");
 
     auto tr_pair = [&](const char* base, uint32_t off, int ks) -> bf16x8 {
         const int k0 = ks * 16 * kTw * 2;
@@ -812,7 +862,7 @@ __device__ __forceinline__ void gemm_tile_bwd(const uint16_t* __restrict__ A, in
     auto read_step = [&](auto bufc, int ks, int set) {
         constexpr int buf = decltype(bufc)::value;
         const char* ba = reinterpret_cast<const char*>(&sm.in.a[buf][0][0]);
-        const char* bb = reinterpret_cast<const char*>(&sm.in.b[buf][0][0]);
+        const char* bb = lds0 + buf * C::BN * BK * 2;
 #pragma unroll
         for (int i = 0; i < C::TM; ++i) {
             if constexpr (A_KMAJ)
@@ -949,14 +999,16 @@ __device__ __forceinline__ void bwd_gemm_tile(const BwdGemm& g, int64_t b, typen
 #pragma unroll
     for (int ip = 0; ip < C::TM; ++ip) {
         const int e0 = ip * C::EPI;
-        if (ip) __syncthreads();
+        // LDS-only barriers: a __syncthreads fence here would also wait for
+        // the previous pass's stores
+        if (ip) lds_ring_barrier();
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 sm.c[wr + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)][wc + j * 32 + (lane & 31)] =
                     acc[ip][j][v];
-        __syncthreads();
+        lds_ring_barrier();
         for (int e = tid; e < C::EPI * VPR; e += C::THREADS) {
             const int r = e / VPR, cv = e % VPR;
             const int64_t m = m0 + e0 + r, n = n0 + (int64_t)cv * EPV;
