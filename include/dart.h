@@ -373,10 +373,10 @@ dart_status_t dart_lmhead_tok_stats(const void* hidden, int64_t T, int64_t d, in
                                     hipStream_t stream);
 
 /* dart_lmhead_tok_stats for softmax(inv_temp * h W^T), as dart_tok_stats_ex
- * is for materialised logits: each fp32 tile of z is multiplied by inv_temp
- * before it is reduced, so lse, logp and entropy are those of inv_temp * z
- * (inv_temp = 1 gives the bits of dart_lmhead_tok_stats). inv_temp: finite
- * and > 0, else INVALID_ARG. Other arguments and errors as
+ * is for materialised logits: lse, logp and entropy are those of inv_temp * z
+ * for the fp32 z (inv_temp enters the kernel's base-2 exponent and the row
+ * maximum; inv_temp = 1 gives the bits of dart_lmhead_tok_stats). inv_temp:
+ * finite and > 0, else INVALID_ARG. Other arguments and errors as
  * dart_lmhead_tok_stats. */
 dart_status_t dart_lmhead_tok_stats_ex(const void* hidden, int64_t T, int64_t d, int64_t ld_h,
                                        const void* weight, int64_t V, int64_t ld_w,
