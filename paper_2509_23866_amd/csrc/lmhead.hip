@@ -140,16 +140,19 @@ struct Triple {
     float m, s, w;  // reference, sum of e^{z-m}, sum of e^{z-m} (z-m), natural units
 };
 
-// float -> bf16 bits, round to nearest even (NaN kept a quiet NaN)
+// float -> bf16 bits, round to nearest even, a NaN kept quiet with its
+// payload: the __bf16 conversion, which is gfx950's v_cvt_pk_bf16_f32 (two
+// values per instruction; the same bits as the integer rounding
+// u + 0x7FFF + ((u >> 16) & 1) for every one of the 2^32 fp32 inputs, checked
+// on the GPU)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint16_t bf16_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return (uint32_t)bf16_bits(lo) | ((uint32_t)bf16_bits(hi) << 16);
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // Exact merge of two partial triples; an empty triple has s == 0.
