@@ -590,6 +590,28 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
             const int sw = (ch >> 3) & 1;
             const float4 a = *reinterpret_cast<const float4*>(&sm.c[r][ch * 8 + 4 * sw]);
             const float4 b = *reinterpret_cast<const float4*>(&sm.c[r][ch * 8 + 4 - 4 * sw]);
+            uint16_t* dst = out + t * ld_out + col0;
+            if ((unsigned)yc >= 8u && col0 + 8 <= V) {
+                // no target here (all but one chunk of a row): every element
+                // takes the same formula, each half is rounded in the order
+                // it was read, and only the four packed words follow the swap
+                const float xa[4] = {a.x, a.y, a.z, a.w}, xb[4] = {b.x, b.y, b.z, b.w};
+                float da[4], db[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    da[q] = rp.x * __builtin_amdgcn_exp2f(fmaf(xa[q], c2, rp.y));
+                    db[q] = rp.x * __builtin_amdgcn_exp2f(fmaf(xb[q], c2, rp.y));
+                }
+                const uint32_t a01 = pack_bf16x2(da[0], da[1]), a23 = pack_bf16x2(da[2], da[3]);
+                const uint32_t b01 = pack_bf16x2(db[0], db[1]), b23 = pack_bf16x2(db[2], db[3]);
+                u32x4 pk;
+                pk.x = sw ? b01 : a01;
+                pk.y = sw ? b23 : a23;
+                pk.z = sw ? a01 : b01;
+                pk.w = sw ? a23 : b23;
+                __builtin_nontemporal_store(pk, reinterpret_cast<u32x4*>(dst));
+                continue;
+            }
             const float4 lo = sw ? b : a, hi = sw ? a : b;
             const float xs[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
             float dz[8];
@@ -598,7 +620,6 @@ lmhead_dlogits_kernel(const uint16_t* __restrict__ h, int64_t M, int64_t ldh,
                 const float e2 = __builtin_amdgcn_exp2f(fmaf(xs[q], c2, rp.y));
                 dz[q] = q == yc ? rp.z : rp.x * e2;
             }
-            uint16_t* dst = out + t * ld_out + col0;
             if (col0 + 8 <= V) {
                 u32x4 pk;
                 pk.x = pack_bf16x2(dz[0], dz[1]);
