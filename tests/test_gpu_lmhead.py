@@ -123,3 +123,55 @@ def test_lmhead_stats_vlm7b_shape_sampled_rows():
     wb = sn.gaussian_bits_host(wl.seed, STREAM_WEIGHT, wl.V, d, prob.sigma_w)
     ref = oracle.lmhead_token_stats(hb, wb, wl.target[rows].astype(np.int32))
     _check(got, ref, rows=rows)
+
+
+def _rne_bf16(x):
+    """fp32 -> bf16 bits, round to nearest even on the bit pattern (a NaN
+    stays a quiet NaN with its upper payload): the rounding the header states."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
+    nan = np.isnan(np.asarray(x, dtype=np.float32))
+    r[nan] = ((u[nan] >> 16) | 0x40) & 0xFFFF
+    return r.astype(np.uint16)
+
+
+@pytest.mark.parametrize("inv_temp", [None, 2.0])
+def test_lmhead_dlogits_bf16_rounding(inv_temp):
+    """The bf16 rounding of dz in the dlogits epilogue, bit for bit. With
+    hidden rows of zeros every logit is exactly 0 and with lse = 0 every
+    softmax term is exactly 1, so dz = -s g on every column but the target,
+    where logp = -inf makes it s g (-expm1(-inf) = 1); s = 1 or 2 keeps s g
+    exact. The coefficients sit on and beside rounding ties, in the fp32
+    denormal range, and at the top of the range (rounding up to infinity);
+    V = 300 ends each row with a partial 8-column chunk, and the target's
+    chunk takes the epilogue's other path."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    e = lambda k: math.ldexp(1.0, k)  # noqa: E731
+    g = np.array([1.0 + e(-8), 1.0 + 3 * e(-8), 1.0 + e(-8) + e(-23), 1.0 + e(-8) - e(-23),
+                  -(1.0 + e(-8)), -(1.0 + 3 * e(-8)), 1.5, 0.3, -0.7, 1e-3, 65504.0, 1e10,
+                  e(-126), e(-127), e(-133) + e(-149), 3 * e(-134), e(-134), e(-149),
+                  -e(-130), 1e-30, 3.0e38, 3.4028235e38, -3.4028235e38, 0.0, -0.0],
+                 dtype=np.float32)
+    T, d, V = len(g), 16, 300
+    h = np.zeros((T, d), dtype=np.uint16)
+    w = gaussian_bits(5, STREAM_WEIGHT, V, d, 0.1)
+    y = np.random.default_rng(5).integers(0, V, T).astype(np.int32)
+    lse = np.zeros(T, dtype=np.float32)
+    logp = np.full(T, -np.inf, dtype=np.float32)
+    # the output's rows padded to a multiple of 8 elements (V = 300)
+    out = torch.empty((T, V + 4), dtype=torch.bfloat16, device="cuda")[:, :V]
+    dz = dart.dart_lmhead_dlogits(_dev_bf16(h), _dev_bf16(w), _cuda(y), _cuda(lse), _cuda(logp),
+                                  _cuda(g), dlogits=out, inv_temp=inv_temp)
+    torch.cuda.synchronize()
+    got = dz.view(torch.int16).cpu().numpy().view(np.uint16)
+    with np.errstate(over="ignore"):  # 2 x the fp32 maximum is inf, as on the GPU
+        sg = g * np.float32(1.0 if inv_temp is None else inv_temp)
+    want = np.repeat(_rne_bf16(-sg)[:, None], V, axis=1)
+    want[np.arange(T), y] = _rne_bf16(sg)
+    bad = np.argwhere(got != want)
+    H.log(f"dlogits bf16 rounding (inv_temp={inv_temp}): {len(bad)} of {got.size} differ")
+    assert len(bad) == 0, [(int(r), int(c), hex(got[r, c]), hex(want[r, c]), float(sg[r]))
+                           for r, c in bad[:8]]
