@@ -152,6 +152,30 @@ class GpuSide:
 
 # ---------------------------------------------------------------- checks
 
+def rne_bf16_bits(x):
+    """fp32 -> bf16 bits, round to nearest even on the bit pattern (a NaN
+    stays a quiet NaN with its upper payload): the rounding the header states
+    for every bf16 output."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
+    nan = np.isnan(np.asarray(x, dtype=np.float32))
+    r[nan] = ((u[nan] >> 16) | 0x40) & 0xFFFF
+    return r.astype(np.uint16)
+
+
+def rounding_coefs():
+    """Coefficients g on and beside bf16 rounding ties, in the fp32 denormal
+    range and at the top of the range, of both signs."""
+    import math
+
+    e = lambda k: math.ldexp(1.0, k)  # noqa: E731
+    return np.array([1.0 + e(-8), 1.0 + 3 * e(-8), 1.0 + e(-8) + e(-23), 1.0 + e(-8) - e(-23),
+                     -(1.0 + e(-8)), -(1.0 + 3 * e(-8)), 1.5, 0.3, -0.7, 1e-3, 65504.0, 1e10,
+                     e(-126), e(-127), e(-133) + e(-149), 3 * e(-134), e(-134), e(-149),
+                     -e(-130), 1e-30, 3.0e38, 3.4028235e38, -3.4028235e38, 0.0, -0.0],
+                    dtype=np.float32)
+
+
 def check_token_stats(gpu, ors, rows=None):
     sl = slice(None) if rows is None else rows
     dl = np.abs(gpu["logp"][sl] - ors.logp[sl])

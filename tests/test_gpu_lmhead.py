@@ -125,15 +125,6 @@ def test_lmhead_stats_vlm7b_shape_sampled_rows():
     _check(got, ref, rows=rows)
 
 
-def _rne_bf16(x):
-    """fp32 -> bf16 bits, round to nearest even on the bit pattern (a NaN
-    stays a quiet NaN with its upper payload): the rounding the header states."""
-    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
-    nan = np.isnan(np.asarray(x, dtype=np.float32))
-    r[nan] = ((u[nan] >> 16) | 0x40) & 0xFFFF
-    return r.astype(np.uint16)
-
 
 @pytest.mark.parametrize("inv_temp", [None, 2.0])
 def test_lmhead_dlogits_bf16_rounding(inv_temp):
@@ -149,12 +140,7 @@ def test_lmhead_dlogits_bf16_rounding(inv_temp):
 
     import paper_2509_23866_amd as dart
 
-    e = lambda k: math.ldexp(1.0, k)  # noqa: E731
-    g = np.array([1.0 + e(-8), 1.0 + 3 * e(-8), 1.0 + e(-8) + e(-23), 1.0 + e(-8) - e(-23),
-                  -(1.0 + e(-8)), -(1.0 + 3 * e(-8)), 1.5, 0.3, -0.7, 1e-3, 65504.0, 1e10,
-                  e(-126), e(-127), e(-133) + e(-149), 3 * e(-134), e(-134), e(-149),
-                  -e(-130), 1e-30, 3.0e38, 3.4028235e38, -3.4028235e38, 0.0, -0.0],
-                 dtype=np.float32)
+    g = H.rounding_coefs()
     T, d, V = len(g), 16, 300
     h = np.zeros((T, d), dtype=np.uint16)
     w = gaussian_bits(5, STREAM_WEIGHT, V, d, 0.1)
@@ -169,8 +155,8 @@ def test_lmhead_dlogits_bf16_rounding(inv_temp):
     got = dz.view(torch.int16).cpu().numpy().view(np.uint16)
     with np.errstate(over="ignore"):  # 2 x the fp32 maximum is inf, as on the GPU
         sg = g * np.float32(1.0 if inv_temp is None else inv_temp)
-    want = np.repeat(_rne_bf16(-sg)[:, None], V, axis=1)
-    want[np.arange(T), y] = _rne_bf16(sg)
+    want = np.repeat(H.rne_bf16_bits(-sg)[:, None], V, axis=1)
+    want[np.arange(T), y] = H.rne_bf16_bits(sg)
     bad = np.argwhere(got != want)
     H.log(f"dlogits bf16 rounding (inv_temp={inv_temp}): {len(bad)} of {got.size} differ")
     assert len(bad) == 0, [(int(r), int(c), hex(got[r, c]), hex(want[r, c]), float(sg[r]))

@@ -9,7 +9,9 @@ do not reach:
   coefficient is 0 -- tokens of steps the indicator of Eq. (2) drops, tokens on
   the clipped branch of Eq. (1) -- written as zeros without reading their
   logits) at the edge workload's full size, separate and in place, against the
-  oracle's gradient.
+  oracle's gradient;
+* the gradient pass's bf16 rounding, bit for bit, in the vector, head and
+  tail paths of its rows.
 """
 
 import numpy as np
@@ -222,3 +224,35 @@ def test_skip_zero_rows_edge_against_oracle(inplace):
     sel = skip[torch.from_numpy(rows).to(skip.device)]
     got = sel.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     H.check_dz(got, ref64, "bf16", row_ok=~res["boundary"][rows])
+
+
+@pytest.mark.parametrize("V,ld,out_ld", [(1000, 1000, 1000), (1003, 1011, 1011), (1003, 1011, 1003)])
+def test_tis_grad_bf16_rounding(V, ld, out_ld):
+    """dlogits leave the gradient pass rounded to bf16 to nearest even, bit for
+    bit: with logits of exactly 0 and lse = 0 every softmax term is exactly 1,
+    so dz = -g on every column but the target, where logp = -inf makes it g
+    (-expm1(-inf) = 1). The coefficients sit on and beside rounding ties, in
+    the fp32 denormal range and at the top of the range. Rows ld = 1011
+    elements apart start unaligned: with the output rows as far apart their
+    heads and tails take the kernel's scalar paths around the vector body,
+    with contiguous output rows (other heads) the whole row takes them."""
+    import torch
+
+    import paper_2509_23866_amd as dart
+
+    g = H.rounding_coefs()
+    T = len(g)
+    logits = torch.zeros((T, ld), dtype=torch.bfloat16, device="cuda")[:, :V]
+    y = np.random.default_rng(7).integers(0, V, T).astype(np.int32)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    out = torch.empty((T, out_ld), dtype=torch.bfloat16, device="cuda")[:, :V]
+    dz = dart.dart_tis_grad(logits, dev(y), dev(np.full(T, -np.inf, dtype=np.float32)),
+                            dev(np.zeros(T, dtype=np.float32)), dev(g), dlogits=out)
+    torch.cuda.synchronize()
+    got = dz.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    want = np.repeat(H.rne_bf16_bits(-g)[:, None], V, axis=1)
+    want[np.arange(T), y] = H.rne_bf16_bits(g)
+    bad = np.argwhere(got != want)
+    H.log(f"tis_grad bf16 rounding V={V} ld={ld} out_ld={out_ld}: {len(bad)} of {got.size} differ")
+    assert len(bad) == 0, [(int(r), int(c), hex(got[r, c]), hex(want[r, c]), float(g[r]))
+                           for r, c in bad[:8]]
